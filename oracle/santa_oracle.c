@@ -1,0 +1,333 @@
+/*
+ * santa_oracle.c -- plain double-precision CPU oracle for one decode step of
+ * SANTA / S2ANTA attention ("Stochastic Sparse Attention for Memory-Bound
+ * Inference", arXiv 2605.01910).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may load this
+ * library: only the tests, the package smoke check and the benchmark's CPU
+ * baseline leg use it.  It shares no code, header, table or helper with the
+ * GPU library; inputs reach it as raw arrays produced by the seeded input
+ * generator.
+ *
+ * Every function below is one step of the method written from its plain
+ * definition, in double precision, one query row at a time, with no blocking,
+ * fusion or reordering:
+ *
+ *   orc_scores            s_j = scale * <q, k_j>                  (Sec. 2, SDPA equation)
+ *   orc_softmax           p = softmax(s), max-shifted             (Sec. 2, SDPA equation)
+ *   orc_weighted_sum      sum_j p_j v_j  (dense AV)               (Sec. 2, SDPA equation)
+ *   orc_cdf               F(j) = sum_{i<=j} p_i                   (Sec. 2.1, "Construction")
+ *   orc_thresholds        T_m for systematic / stratified / iid   (Sec. 2.1; Sec. 2 i.i.d. draws)
+ *   orc_inverse_cdf       J = F^{-1}(T): the j with F(j-1) <= T < F(j)
+ *                                                                  (App. A, "Unbiasedness of S2ANTA")
+ *   orc_gather_mean       (1/S) sum_m v_{J_m}                     (Sec. 2, Eq. "stochastic-add-only-attn")
+ *   orc_bernoulli_weights ternary / mean-group query weights      (Sec. 5, Eq. "qk_estimator";
+ *                                                                  App. C, Eq. "mean_group_query")
+ *   orc_decode            all of the above over the rows of a batch
+ *
+ * Readings of points the paper leaves open:
+ *   - F^{-1}(T) counts the CDF values <= T ("right" side of a boundary), so a
+ *     key of zero mass is never chosen; a threshold at or above the last CDF
+ *     value (rounding) takes the last key.
+ *   - Systematic thresholds are T_m = (m + u)/S with one u in [0,1) per row
+ *     (U = u/S is uniform on [0, 1/S)); stratified ones are (m + u_m)/S.
+ *   - The i.i.d. estimator draws its S categorical samples by inverting the
+ *     CDF at S sorted independent uniforms (same multiset as S i.i.d. draws).
+ *   - Bernoulli decisions b = [u < pi] are taken in float32, the precision of
+ *     the inputs, so that a GPU taking the same decision in float32 agrees bit
+ *     for bit; everything after the decision is double precision.
+ *   - A row with zero context length has no attention distribution: its
+ *     output is zero and its indices are -1.
+ *
+ * Element arrays hold bfloat16 bit patterns (uint16, is_f32 = 0) or float32
+ * values (is_f32 = 1); both widen to double exactly.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* Exact widening of one stored element to double. */
+static double elem(const void *base, int is_f32, int64_t i) {
+  if (is_f32) return (double)((const float *)base)[i];
+  uint32_t w = (uint32_t)((const uint16_t *)base)[i] << 16;
+  float f;
+  memcpy(&f, &w, sizeof f);
+  return (double)f;
+}
+
+/* Same widening, but to float (used where a decision is taken in float32). */
+static float elemf(const void *base, int is_f32, int64_t i) {
+  if (is_f32) return ((const float *)base)[i];
+  uint32_t w = (uint32_t)((const uint16_t *)base)[i] << 16;
+  float f;
+  memcpy(&f, &w, sizeof f);
+  return f;
+}
+
+/* Score stage (Sec. 2, SDPA equation): s_j = scale * sum_i w_i k_{j,i} for j < L, with
+ * the query given in double; key j starts at element j*row_stride of k. */
+void orc_scores(const double *w, int d, const void *k, int k_f32, int64_t row_stride, int L,
+                double scale, double *s) {
+  for (int j = 0; j < L; ++j) {
+    double acc = 0.0;
+    for (int i = 0; i < d; ++i) acc += w[i] * elem(k, k_f32, (int64_t)j * row_stride + i);
+    s[j] = scale * acc;
+  }
+}
+
+/* Softmax of the SDPA equation (Sec. 2) in its numerically stable form: p_j = exp(s_j - m) / Z,
+ * m = max_j s_j, Z = sum_j exp(s_j - m). */
+void orc_softmax(const double *s, int L, double *p) {
+  if (L <= 0) return;
+  double m = s[0];
+  for (int j = 1; j < L; ++j)
+    if (s[j] > m) m = s[j];
+  double Z = 0.0;
+  for (int j = 0; j < L; ++j) {
+    p[j] = exp(s[j] - m);
+    Z += p[j];
+  }
+  for (int j = 0; j < L; ++j) p[j] /= Z;
+}
+
+/* Dense value aggregation AV (Sec. 2, SDPA equation): out_i = sum_j p_j v_{j,i}. */
+void orc_weighted_sum(const double *p, const void *v, int v_f32, int64_t row_stride, int L, int d,
+                      double *out) {
+  for (int i = 0; i < d; ++i) out[i] = 0.0;
+  for (int j = 0; j < L; ++j)
+    for (int i = 0; i < d; ++i) out[i] += p[j] * elem(v, v_f32, (int64_t)j * row_stride + i);
+}
+
+/* CDF of the attention distribution (Sec. 2.1, "Construction"): F(j) = sum_{i<=j} p_i,
+ * accumulated in index order. */
+void orc_cdf(const double *p, int L, double *C) {
+  double acc = 0.0;
+  for (int j = 0; j < L; ++j) {
+    acc += p[j];
+    C[j] = acc;
+  }
+}
+
+/* Sampling thresholds on [0,1) (Sec. 2.1, "Construction"):
+ *   scheme 0, systematic:  T_m = U + m/S with U = u[0]/S uniform on [0, 1/S);
+ *   scheme 1, stratified:  T_m uniform on I_m = [m/S, (m+1)/S): T_m = (m + u[m])/S;
+ *   scheme 2, i.i.d.:      S independent uniforms u[0..S) in increasing order, whose
+ *                          inverse-CDF images are S i.i.d. categorical draws (Sec. 2). */
+static int cmp_double(const void *a, const void *b) {
+  double x = *(const double *)a, y = *(const double *)b;
+  return (x > y) - (x < y);
+}
+
+void orc_thresholds(int scheme, const float *u, int S, double *T) {
+  for (int m = 0; m < S; ++m) {
+    if (scheme == 0)
+      T[m] = ((double)m + (double)u[0]) / (double)S;
+    else if (scheme == 1)
+      T[m] = ((double)m + (double)u[m]) / (double)S;
+    else
+      T[m] = (double)u[m];
+  }
+  if (scheme == 2) qsort(T, (size_t)S, sizeof(double), cmp_double);
+}
+
+/* Inverse CDF (App. A, "Unbiasedness of S2ANTA"): J = F^{-1}(T) is the key j
+ * whose interval [F(j-1), F(j)) contains T, i.e. J = #{j : F(j) <= T}, taken as the
+ * last key L-1 when T is at or above F(L-1). */
+void orc_inverse_cdf(const double *C, int L, const double *T, int S, int32_t *idx) {
+  for (int m = 0; m < S; ++m) {
+    int count = 0;
+    for (int j = 0; j < L; ++j)
+      if (C[j] <= T[m]) ++count;
+    idx[m] = count < L ? count : L - 1;
+  }
+}
+
+/* SANTA value estimate (Sec. 2, Eq. "stochastic-add-only-attn"):
+ * out_i = (1/S) sum_m v_{idx_m, i}. */
+void orc_gather_mean(const void *v, int v_f32, int64_t row_stride, int d, const int32_t *idx,
+                     int S, double *out) {
+  for (int i = 0; i < d; ++i) out[i] = 0.0;
+  for (int m = 0; m < S; ++m)
+    for (int i = 0; i < d; ++i) out[i] += elem(v, v_f32, (int64_t)idx[m] * row_stride + i);
+  for (int i = 0; i < d; ++i) out[i] /= (double)S;
+}
+
+/* Bernoulli query weights for one GQA group of G heads (query rows q_g at
+ * q + g*d), returned as w[g*d + i] such that the estimated score is
+ * p_hat = scale * <w_g, k_j>.
+ *
+ * mode 0, per-head ternary query (Sec. 5, Eq. "qk_estimator"; App. C):
+ *   norm = max_i |q_i|, pi_i = |q_i| / norm, b_i^(n) ~ Bernoulli(pi_i),
+ *   w_i = (norm / B) * sign(q_i) * sum_n b_i^(n).
+ * mode 1, mean group query (Sec. 5, "Mean Group Query", Eq. "mean_group_query"; App. C, GQA subsection):
+ *   m_i = mean_g |q_{g,i}|, norm = max_i m_i, pi_i = m_i / norm,
+ *   m_hat_i = (norm / B) * sum_n b_i^(n),  w_{g,i} = m_hat_i * q_{g,i} / m_i  (0 if m_i = 0).
+ *
+ * Draws: iid = 0 uses one uniform per feature and the stratified count
+ * #{n < B : (n + u_i)/B < pi_i}; iid = 1 uses B independent uniforms per feature,
+ * u[n*d + i], and counts #{n : u^(n)_i < pi_i}.  u is laid out per head
+ * (mode 0: G blocks) or per group (mode 1: one block).  The decision and the
+ * quantities it depends on (|q|, m, norm, pi) are float32.
+ * mask[i] = 1 when some head of the group has w_{g,i} != 0. */
+void orc_bernoulli_weights(const void *q, int q_f32, int G, int d, const float *u, int B,
+                           int iid, int mode, double *w, uint8_t *mask) {
+  for (int i = 0; i < d; ++i) mask[i] = 0;
+  if (mode == 0) {
+    for (int g = 0; g < G; ++g) {
+      float norm = 0.0f;
+      for (int i = 0; i < d; ++i) {
+        float a = fabsf(elemf(q, q_f32, (int64_t)g * d + i));
+        if (a > norm) norm = a;
+      }
+      const float *ug = u + (int64_t)g * d * (iid ? B : 1);
+      for (int i = 0; i < d; ++i) {
+        float qi = elemf(q, q_f32, (int64_t)g * d + i);
+        float pi = norm > 0.0f ? fabsf(qi) / norm : 0.0f;
+        int c = 0;
+        for (int n = 0; n < B; ++n) {
+          int hit = iid ? (ug[(int64_t)n * d + i] < pi) : ((((float)n + ug[i]) / (float)B) < pi);
+          c += hit;
+        }
+        double sgn = qi > 0.0f ? 1.0 : (qi < 0.0f ? -1.0 : 0.0);
+        w[(int64_t)g * d + i] = ((double)norm / (double)B) * sgn * (double)c;
+        if (w[(int64_t)g * d + i] != 0.0) mask[i] = 1;
+      }
+    }
+  } else {
+    float *m = (float *)malloc(sizeof(float) * (size_t)d);
+    float norm = 0.0f;
+    for (int i = 0; i < d; ++i) {
+      float acc = 0.0f;
+      for (int g = 0; g < G; ++g) acc += fabsf(elemf(q, q_f32, (int64_t)g * d + i));
+      m[i] = acc / (float)G;
+      if (m[i] > norm) norm = m[i];
+    }
+    for (int i = 0; i < d; ++i) {
+      float pi = norm > 0.0f ? m[i] / norm : 0.0f;
+      int c = 0;
+      for (int n = 0; n < B; ++n) {
+        int hit = iid ? (u[(int64_t)n * d + i] < pi) : ((((float)n + u[i]) / (float)B) < pi);
+        c += hit;
+      }
+      double mhat = ((double)norm / (double)B) * (double)c;
+      for (int g = 0; g < G; ++g) {
+        double qg = elem(q, q_f32, (int64_t)g * d + i);
+        double wg = m[i] > 0.0f ? mhat * qg / (double)m[i] : 0.0;
+        w[(int64_t)g * d + i] = wg;
+        if (wg != 0.0) mask[i] = 1;
+      }
+    }
+    free(m);
+  }
+}
+
+/* ------------------------------------------------------------------------- */
+/* Batch driver                                                              */
+/* ------------------------------------------------------------------------- */
+
+typedef struct {
+  int32_t B, Hq, Hkv, d, n_max;
+  int32_t is_f32;        /* element type of q, k, v */
+  const void *q;         /* [B, Hq, d] */
+  const void *k;         /* logical keys: element (b, j, kv, i) at b*sb + j*sn + kv*sh + i */
+  const void *v;         /* logical values, same strides */
+  int64_t sb, sn, sh;
+  const int32_t *ctx_len; /* [B] */
+  double scale;
+} orc_problem_t;
+
+enum { ORC_DENSE = 0, ORC_SYSTEMATIC = 1, ORC_STRATIFIED = 2, ORC_IID = 3, ORC_BERNOULLI_SYS = 4 };
+
+/* One decode step for the listed rows (row = b*Hq + h; rows == NULL means all):
+ *   kind dense:        out = AV
+ *   kind systematic:   u[b*Hq + h], thresholds (m+u)/S
+ *   kind stratified:   u[(b*Hq + h)*S + m]
+ *   kind iid:          u[(b*Hq + h)*S + m], sorted
+ *   kind bernoulli:    Bernoulli scores from u_q (mode 0: [B, Hq, d*(iid?B:1)]; mode 1:
+ *                      [B, Hkv, d*(iid?B:1)]) followed by systematic sampling with u[b*Hq + h].
+ * Outputs are compact over the listed rows: out[r*d], idx[r*S] (sampled kinds),
+ * cdf[r*n_max] (optional), and for bernoulli w[r*d] and mask[r*d] (optional).
+ * Returns the number of OpenMP threads used. */
+int orc_decode(const orc_problem_t *P, int kind, int S, const float *u, const float *u_q,
+               int B_draws, int mode, int iid_draws, int nrows, const int32_t *rows, double *out,
+               int32_t *idx, double *cdf, double *w_out, uint8_t *mask_out) {
+  const int G = P->Hq / P->Hkv;
+  const int total = nrows > 0 ? nrows : P->B * P->Hq;
+  int threads = 1;
+#pragma omp parallel
+  {
+#ifdef _OPENMP
+#pragma omp single
+    threads = omp_get_num_threads();
+#endif
+    double *qd = (double *)malloc(sizeof(double) * (size_t)P->d);
+    double *wg = (double *)malloc(sizeof(double) * (size_t)P->d * (size_t)G);
+    uint8_t *mk = (uint8_t *)malloc((size_t)P->d);
+    double *s = (double *)malloc(sizeof(double) * (size_t)(P->n_max > 0 ? P->n_max : 1));
+    double *p = (double *)malloc(sizeof(double) * (size_t)(P->n_max > 0 ? P->n_max : 1));
+    double *C = (double *)malloc(sizeof(double) * (size_t)(P->n_max > 0 ? P->n_max : 1));
+    double *T = (double *)malloc(sizeof(double) * (size_t)(S > 0 ? S : 1));
+#pragma omp for schedule(dynamic, 1)
+    for (int r = 0; r < total; ++r) {
+      const int row = rows ? rows[r] : r;
+      const int b = row / P->Hq, h = row % P->Hq, kv = h / G;
+      const int L = P->ctx_len[b];
+      double *o = out + (int64_t)r * P->d;
+      const int64_t base = (int64_t)b * P->sb + (int64_t)kv * P->sh;
+      if (L <= 0) {
+        for (int i = 0; i < P->d; ++i) o[i] = 0.0;
+        if (idx && kind != ORC_DENSE)
+          for (int m = 0; m < S; ++m) idx[(int64_t)r * S + m] = -1;
+        continue;
+      }
+      /* query weights */
+      const double *wq = qd;
+      if (kind == ORC_BERNOULLI_SYS) {
+        const float *ub = mode == 0
+                              ? u_q + ((int64_t)b * P->Hq + (int64_t)kv * G) * P->d * (iid_draws ? B_draws : 1)
+                              : u_q + ((int64_t)b * P->Hkv + kv) * P->d * (iid_draws ? B_draws : 1);
+        const size_t esz = P->is_f32 ? 4 : 2;
+        const char *qg = (const char *)P->q + ((int64_t)b * P->Hq + (int64_t)kv * G) * P->d * esz;
+        orc_bernoulli_weights(qg, P->is_f32, G, P->d, ub, B_draws, iid_draws, mode, wg, mk);
+        wq = wg + (int64_t)(h - kv * G) * P->d;
+        if (w_out)
+          for (int i = 0; i < P->d; ++i) w_out[(int64_t)r * P->d + i] = wq[i];
+        if (mask_out)
+          for (int i = 0; i < P->d; ++i) mask_out[(int64_t)r * P->d + i] = mk[i];
+      } else {
+        for (int i = 0; i < P->d; ++i) qd[i] = elem(P->q, P->is_f32, ((int64_t)b * P->Hq + h) * P->d + i);
+      }
+      const size_t esz = P->is_f32 ? 4 : 2;
+      const void *kb = (const char *)P->k + base * (int64_t)esz;
+      const void *vb = (const char *)P->v + base * (int64_t)esz;
+      orc_scores(wq, P->d, kb, P->is_f32, P->sn, L, P->scale, s);
+      orc_softmax(s, L, p);
+      if (kind == ORC_DENSE) {
+        orc_weighted_sum(p, vb, P->is_f32, P->sn, L, P->d, o);
+        continue;
+      }
+      orc_cdf(p, L, C);
+      if (cdf)
+        for (int j = 0; j < L; ++j) cdf[(int64_t)r * P->n_max + j] = C[j];
+      if (kind == ORC_SYSTEMATIC || kind == ORC_BERNOULLI_SYS)
+        orc_thresholds(0, u + (int64_t)row, S, T);
+      else
+        orc_thresholds(kind == ORC_STRATIFIED ? 1 : 2, u + (int64_t)row * S, S, T);
+      int32_t *ix = idx + (int64_t)r * S;
+      orc_inverse_cdf(C, L, T, S, ix);
+      orc_gather_mean(vb, P->is_f32, P->sn, P->d, ix, S, o);
+    }
+    free(qd);
+    free(wg);
+    free(mk);
+    free(s);
+    free(p);
+    free(C);
+    free(T);
+  }
+  return threads;
+}
