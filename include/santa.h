@@ -1,0 +1,181 @@
+/*
+ * santa.h -- C ABI of libsanta: one decode step of SANTA / S2ANTA attention on
+ * an AMD Instinct MI355X (gfx950).
+ *
+ * Method: "Stochastic Sparse Attention for Memory-Bound Inference" (arXiv
+ * 2605.01910).  A decode step computes, for every query row (batch b, query
+ * head h) with context length L = ctx_len[b] and KV head k = h / (Hq / Hkv):
+ *
+ *   scores   s_j = scale * <q_h, K_{b,j,k}>,  j < L             (Sec. 2, SDPA equation)
+ *   softmax  p = softmax(s)                                      (Sec. 2, SDPA equation)
+ *   dense    out = sum_j p_j V_{b,j,k}                           (Sec. 2, SDPA equation)
+ *   sampled  out = (1/S) sum_m V_{b,J_m,k},  J_m = F^{-1}(T_m)   (Sec. 2, Eq. "stochastic-add-only-attn";
+ *            F = CDF of p; T_m systematic or stratified          Sec. 2.1, "Construction")
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Every pointer argument except `stream` and the `shape`/`kv`/`kt` structs is
+ *   a DEVICE pointer owned by the caller.  The library never allocates, frees
+ *   or synchronises; all kernels are enqueued on `stream` (a hipStream_t,
+ *   NULL = the null stream) and the call returns before they finish.
+ * - Element type: `shape->dtype` (SANTA_BF16 or SANTA_F32) is the type of q, K,
+ *   V and out.  Accumulation is float32.
+ * - q is [batch, num_q_heads, head_dim] contiguous; out is the same shape and
+ *   type; idx_out (optional, NULL to skip) is int32 [batch, num_q_heads, S].
+ * - head_dim must be 128; num_q_heads / num_kv_heads must be 1, 2, 4 or 8.
+ * - Errors: arguments are validated on the host before any launch; on error
+ *   nothing is enqueued and a status code is returned (santa_last_error() gives
+ *   a message).  A launch failure returns SANTA_ERR_HIP.  No C++ exception
+ *   crosses this interface.
+ * - Not checked on the device (preconditions): u values in [0, 1),
+ *   0 <= ctx_len[b] <= n_k, block-table entries naming valid pages.  A row with
+ *   ctx_len 0 yields a zero output and idx -1.
+ * - Workspace: `ws` must be at least santa_workspace_size(...) bytes, 256-byte
+ *   aligned, and initialised once by santa_workspace_init() (or zero-filled)
+ *   before its first use.  Every call leaves it ready for the next call.  Calls
+ *   that share one workspace must be ordered (same stream or synchronised).
+ * - The library is stateless apart from the thread-local error message.
+ */
+#ifndef SANTA_H
+#define SANTA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SANTA_OK = 0,
+  SANTA_ERR_INVALID_ARG = 1, /* null pointer, bad size, inconsistent shape   */
+  SANTA_ERR_UNSUPPORTED = 2, /* valid but not implemented (head_dim, G, ...) */
+  SANTA_ERR_WORKSPACE = 3,   /* workspace missing, too small or misaligned   */
+  SANTA_ERR_HIP = 4          /* a HIP runtime call or kernel launch failed    */
+} santa_status_t;
+
+typedef enum { SANTA_BF16 = 0, SANTA_F32 = 1 } santa_dtype_t;
+
+typedef enum {
+  SANTA_KIND_DENSE = 0,
+  SANTA_KIND_SYSTEMATIC = 1,
+  SANTA_KIND_STRATIFIED = 2,
+  SANTA_KIND_BERNOULLI = 3
+} santa_kind_t;
+
+/* Problem shape.  dtype is a santa_dtype_t. */
+typedef struct {
+  int32_t batch;
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t dtype;
+} santa_shape_t;
+
+/* KV cache descriptor (device pointers, caller-owned).  The feature dimension
+ * is always contiguous (stride 1); strides are in ELEMENTS and must keep every
+ * 128-feature row 16-byte aligned.
+ *
+ * Contiguous cache (block_table == NULL): element (b, j, k, i) of K or V is at
+ *   base + b*stride_b + j*stride_n + k*stride_h + i,
+ * so the sequence-major layout [B, n, Hkv, d] of the paper's microbenchmark and
+ * the head-major layout [B, Hkv, n, d] are both expressible.
+ *
+ * Paged cache (block_table != NULL, int32 [batch, max_pages]): token j of
+ * sequence b lives in page P = block_table[b*max_pages + j/page_size]; its
+ * element (k, i) is at
+ *   base + P*stride_b + (j % page_size)*stride_n + k*stride_h + i,
+ * e.g. stride_b = Hkv*page_size*d, stride_h = page_size*d, stride_n = d for a
+ * [pages, Hkv, page_size, d] pool.  page_size must be a power of two.
+ *
+ * ctx_len: int32 [batch] per-sequence lengths, or NULL for "every sequence has
+ * n_k keys".  n_k (host value) is the maximum length; it sizes the launch. */
+typedef struct {
+  const void *k;
+  const void *v;
+  int64_t stride_b, stride_n, stride_h;
+  const int32_t *ctx_len;
+  const int32_t *block_table;
+  int32_t page_size;
+  int32_t max_pages;
+  int32_t n_k;
+} santa_kv_t;
+
+/* Feature-major key cache for the Bernoulli score stage: element (b, k, i, j)
+ * (feature i of key j) at k_t + b*stride_b + k*stride_h + i*stride_d + j; keys
+ * are contiguous so that skipping a feature skips a contiguous row of K^T
+ * (Sec. 5: features whose query sample is zero need not be read). */
+typedef struct {
+  const void *k_t;
+  int64_t stride_b, stride_h, stride_d;
+} santa_kt_t;
+
+/* Bytes of workspace the given call needs (kind: santa_kind_t; S ignored for
+ * SANTA_KIND_DENSE).  Returns 0 if the arguments are invalid. */
+size_t santa_workspace_size(const santa_shape_t *shape, const santa_kv_t *kv, int32_t S,
+                            int32_t kind);
+
+/* Prepare a workspace for first use (zero-fills it on `stream`). */
+santa_status_t santa_workspace_init(void *ws, size_t ws_bytes, void *stream);
+
+/* Exact decode attention (Sec. 2, SDPA equation): out = softmax(scale q K^T) V,
+ * computed split-K with a max/sum-exp merge.  The like-for-like dense baseline
+ * of the sampled entry points below. */
+santa_status_t santa_decode_dense(const void *q, const santa_kv_t *kv, const santa_shape_t *shape,
+                                  float scale, void *out, void *ws, size_t ws_bytes,
+                                  void *stream);
+
+/* S2ANTA-sys (Sec. 2.1, "Construction", systematic): one uniform u per row
+ * (u: float32 [batch, num_q_heads], in [0,1)); thresholds T_m = (m + u)/S for
+ * m = 0..S-1; J_m = F^{-1}(T_m) is the key whose CDF interval [F(j-1), F(j))
+ * contains T_m (App. A, "Unbiasedness of S2ANTA"); out = (1/S) sum_m V_{J_m}.
+ * Samples are assigned to KV splits by the exact global CDF, so the estimator
+ * is the paper's systematic one for any split size.  1 <= S <= 2^24. */
+santa_status_t santa_decode_systematic(const void *q, const santa_kv_t *kv,
+                                       const santa_shape_t *shape, float scale, int32_t S,
+                                       const float *u, int32_t *idx_out, void *out, void *ws,
+                                       size_t ws_bytes, void *stream);
+
+/* S2ANTA-strat (Sec. 2.1, "Construction", independent stratified): S uniforms
+ * per row (u: float32 [batch, num_q_heads, S]); T_m = (m + u_m)/S lies in
+ * stratum [m/S, (m+1)/S); otherwise as santa_decode_systematic. */
+santa_status_t santa_decode_stratified(const void *q, const santa_kv_t *kv,
+                                       const santa_shape_t *shape, float scale, int32_t S,
+                                       const float *u, int32_t *idx_out, void *out, void *ws,
+                                       size_t ws_bytes, void *stream);
+
+/* Bernoulli qK^T score sampling (Sec. 5, Eq. "qk_estimator"; App. C) followed
+ * by the systematic value stage.
+ *   mode 0, per-head ternary query: norm = max_i |q_i|, pi_i = |q_i|/norm,
+ *           w_i = (norm/B) * sign(q_i) * c_i;
+ *   mode 1, mean group query (Sec. 5, Eq. "mean_group_query"; App. C, GQA):
+ *           m_i = mean over the group of |q_{g,i}|, norm = max_i m_i,
+ *           pi_i = m_i/norm, w_{g,i} = (norm/B) c_i q_{g,i} / m_i (0 if m_i = 0);
+ *   with B = B_draws and the stratified count c_i = #{n < B : (n + u_i)/B < pi_i}
+ *   (for B = 1 this is one Bernoulli(pi_i) draw).  The decision is taken in
+ *   float32.  Scores s_j = scale * <w, k_j> read only the features in the
+ *   union over the GQA group of nonzero weights, from the feature-major cache kt.
+ * u_q: float32 [batch, num_q_heads, head_dim] (mode 0) or
+ *      [batch, num_kv_heads, head_dim] (mode 1).
+ * kv:  supplies V (kv->k is ignored), ctx_len and n_k; contiguous only.
+ * u:   systematic uniforms [batch, num_q_heads].
+ * feat_mask_out: optional uint8 [batch, num_kv_heads, head_dim], 1 where the
+ *      feature row of K^T was read.  1 <= B_draws <= 64. */
+santa_status_t santa_decode_bernoulli_qk(const void *q, const santa_kt_t *kt,
+                                         const santa_kv_t *kv, const santa_shape_t *shape,
+                                         float scale, int32_t B_draws, int32_t mode,
+                                         const float *u_q, int32_t S, const float *u,
+                                         int32_t *idx_out, uint8_t *feat_mask_out, void *out,
+                                         void *ws, size_t ws_bytes, void *stream);
+
+/* Human-readable name of a status code. */
+const char *santa_status_string(santa_status_t status);
+
+/* Message describing the last error returned on the calling thread ("" if none). */
+const char *santa_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SANTA_H */

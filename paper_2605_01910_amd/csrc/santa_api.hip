@@ -1,0 +1,264 @@
+// santa_api.hip -- C ABI of libsanta (declared in include/santa.h): argument
+// validation, launch plan, workspace carve-up and kernel dispatch.  Nothing
+// here allocates device memory or synchronises.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <string>
+
+#include "santa.h"
+#include "santa_kernels.h"
+#include "santa_plan.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+santa_status_t fail(santa_status_t s, const std::string &msg) {
+  g_last_error = msg;
+  return s;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
+
+int ilog2(int64_t x) {
+  int r = 0;
+  while ((int64_t(1) << (r + 1)) <= x) ++r;
+  return r;
+}
+
+// Split length: enough workgroups to cover the chip several times over (256 CUs),
+// at most kSplitMax keys (the LDS tile), at least 256.
+int choose_split(int64_t rows, int64_t n_k) {
+  const int64_t target_wg = 2048;
+  int64_t ls = (n_k * rows) / target_wg;
+  int p = 256;
+  while (p < santa::kSplitMax && p * 2 <= ls) p *= 2;
+  return p;
+}
+
+santa_status_t check_shape(const santa_shape_t *sh) {
+  if (!sh) return fail(SANTA_ERR_INVALID_ARG, "shape is NULL");
+  if (sh->batch < 1 || sh->num_q_heads < 1 || sh->num_kv_heads < 1)
+    return fail(SANTA_ERR_INVALID_ARG, "batch and head counts must be >= 1");
+  if (sh->num_q_heads % sh->num_kv_heads)
+    return fail(SANTA_ERR_INVALID_ARG, "num_q_heads must be a multiple of num_kv_heads");
+  const int G = sh->num_q_heads / sh->num_kv_heads;
+  if (G != 1 && G != 2 && G != 4 && G != 8)
+    return fail(SANTA_ERR_UNSUPPORTED, "GQA group size must be 1, 2, 4 or 8");
+  if (sh->head_dim != santa::kHeadDim) return fail(SANTA_ERR_UNSUPPORTED, "head_dim must be 128");
+  if (sh->dtype != SANTA_BF16 && sh->dtype != SANTA_F32)
+    return fail(SANTA_ERR_INVALID_ARG, "dtype must be SANTA_BF16 or SANTA_F32");
+  return SANTA_OK;
+}
+
+santa_status_t check_kv(const santa_kv_t *kv, const santa_shape_t *sh, bool need_k) {
+  if (!kv) return fail(SANTA_ERR_INVALID_ARG, "kv is NULL");
+  if ((need_k && !kv->k) || !kv->v) return fail(SANTA_ERR_INVALID_ARG, "kv->k or kv->v is NULL");
+  if (kv->n_k < 1) return fail(SANTA_ERR_INVALID_ARG, "n_k must be >= 1");
+  const int64_t esz = sh->dtype == SANTA_BF16 ? 2 : 4;
+  const int64_t a = 16 / esz;  // elements per 16 bytes
+  if (kv->stride_b < 0 || kv->stride_n < 0 || kv->stride_h < 0)
+    return fail(SANTA_ERR_INVALID_ARG, "strides must be non-negative");
+  if (kv->stride_b % a || kv->stride_n % a || kv->stride_h % a)
+    return fail(SANTA_ERR_UNSUPPORTED, "strides must keep every row 16-byte aligned");
+  if ((need_k && (reinterpret_cast<uintptr_t>(kv->k) & 15)) ||
+      (reinterpret_cast<uintptr_t>(kv->v) & 15))
+    return fail(SANTA_ERR_UNSUPPORTED, "k and v must be 16-byte aligned");
+  if (kv->block_table) {
+    if (!is_pow2(kv->page_size)) return fail(SANTA_ERR_UNSUPPORTED, "page_size must be a power of two");
+    if (kv->max_pages < 1) return fail(SANTA_ERR_INVALID_ARG, "max_pages must be >= 1");
+    if ((int64_t)kv->max_pages * kv->page_size < kv->n_k)
+      return fail(SANTA_ERR_INVALID_ARG, "max_pages * page_size < n_k");
+  }
+  return SANTA_OK;
+}
+
+santa::Plan make_plan(const santa_shape_t *sh, const santa_kv_t *kv, int S, int kind) {
+  santa::Plan p{};
+  p.B = sh->batch;
+  p.Hq = sh->num_q_heads;
+  p.Hkv = sh->num_kv_heads;
+  p.G = p.Hq / p.Hkv;
+  p.dtype = sh->dtype;
+  p.n_k = kv->n_k;
+  p.Ls = choose_split((int64_t)p.B * p.Hkv, p.n_k);
+  p.T = (int)((p.n_k + p.Ls - 1) / p.Ls);
+  p.S = kind == SANTA_KIND_DENSE ? 0 : S;
+  p.kind = kind;
+  const size_t rows = (size_t)p.B * p.Hq;
+  const size_t D = santa::kHeadDim;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align256(off + bytes);
+    return o;
+  };
+  p.off_stats = take(rows * p.T * 8);
+  p.off_part = take((size_t)p.B * p.Hkv * p.T * p.G * D * 4);
+  if (kind != SANTA_KIND_DENSE) {
+    p.off_stash = take(rows * (size_t)p.T * p.Ls * 4);
+    p.off_offs = take(rows * (size_t)(p.T + 1) * 4);
+    p.off_alpha = take(rows * (size_t)p.T * 4);
+    p.off_rowst = take(rows * 8);
+    p.off_flag = take((size_t)p.B * p.Hkv * p.T * 4);
+  }
+  if (kind == SANTA_KIND_BERNOULLI) {
+    p.off_bw = take(rows * D * 4);
+    p.off_blist = take((size_t)p.B * p.Hkv * D * 4);
+    p.off_bn = take((size_t)p.B * p.Hkv * 4);
+  }
+  p.total = off;
+  return p;
+}
+
+santa_status_t check_ws(const santa::Plan &p, void *ws, size_t ws_bytes) {
+  if (!ws) return fail(SANTA_ERR_WORKSPACE, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) & 255) return fail(SANTA_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (ws_bytes < p.total)
+    return fail(SANTA_ERR_WORKSPACE, "workspace too small: need " + std::to_string(p.total) +
+                                         " bytes, got " + std::to_string(ws_bytes));
+  return SANTA_OK;
+}
+
+santa::KvView make_view(const santa_kv_t *kv) {
+  santa::KvView v{};
+  v.k = kv->k;
+  v.v = kv->v;
+  v.sb = kv->stride_b;
+  v.sn = kv->stride_n;
+  v.sh = kv->stride_h;
+  v.ctx = kv->ctx_len;
+  v.bt = kv->block_table;
+  v.ps_log2 = kv->block_table ? ilog2(kv->page_size) : 0;
+  v.max_pages = kv->max_pages;
+  v.n_k = kv->n_k;
+  return v;
+}
+
+santa_status_t hip_status(hipError_t e) {
+  if (e != hipSuccess) return fail(SANTA_ERR_HIP, std::string("HIP: ") + hipGetErrorString(e));
+  return SANTA_OK;
+}
+
+float log2_scale(float scale) { return scale * 1.44269504088896340736f; }
+
+santa_status_t common_checks(const void *q, const santa_kv_t *kv, const santa_shape_t *sh,
+                             float scale, void *out, bool need_k) {
+  g_last_error.clear();
+  santa_status_t s = check_shape(sh);
+  if (s != SANTA_OK) return s;
+  s = check_kv(kv, sh, need_k);
+  if (s != SANTA_OK) return s;
+  if (!q || !out) return fail(SANTA_ERR_INVALID_ARG, "q or out is NULL");
+  if ((reinterpret_cast<uintptr_t>(q) & 15)) return fail(SANTA_ERR_UNSUPPORTED, "q must be 16-byte aligned");
+  if (!std::isfinite(scale)) return fail(SANTA_ERR_INVALID_ARG, "scale must be finite");
+  return SANTA_OK;
+}
+
+santa_status_t sampled(const void *q, const santa_kv_t *kv, const santa_shape_t *sh, float scale,
+                       int32_t S, const float *u, int32_t *idx_out, void *out, void *ws,
+                       size_t ws_bytes, void *stream, bool strat) {
+  santa_status_t s = common_checks(q, kv, sh, scale, out, true);
+  if (s != SANTA_OK) return s;
+  if (S < 1 || S > (1 << 24)) return fail(SANTA_ERR_INVALID_ARG, "S must be in [1, 2^24]");
+  if (!u) return fail(SANTA_ERR_INVALID_ARG, "u is NULL");
+  const santa::Plan p = make_plan(sh, kv, S, strat ? SANTA_KIND_STRATIFIED : SANTA_KIND_SYSTEMATIC);
+  s = check_ws(p, ws, ws_bytes);
+  if (s != SANTA_OK) return s;
+  return hip_status(santa::launch_sampled(p, make_view(kv), q, log2_scale(scale), strat, u, idx_out,
+                                          out, static_cast<char *>(ws),
+                                          static_cast<hipStream_t>(stream)));
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t santa_workspace_size(const santa_shape_t *shape, const santa_kv_t *kv, int32_t S,
+                            int32_t kind) {
+  if (check_shape(shape) != SANTA_OK || !kv || kv->n_k < 1) return 0;
+  if (kind < SANTA_KIND_DENSE || kind > SANTA_KIND_BERNOULLI) return 0;
+  if (kind != SANTA_KIND_DENSE && (S < 1 || S > (1 << 24))) return 0;
+  return make_plan(shape, kv, S, kind).total;
+}
+
+santa_status_t santa_workspace_init(void *ws, size_t ws_bytes, void *stream) {
+  g_last_error.clear();
+  if (!ws) return fail(SANTA_ERR_WORKSPACE, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) & 255) return fail(SANTA_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  return hip_status(santa::launch_zero(ws, ws_bytes & ~size_t(15), static_cast<hipStream_t>(stream)));
+}
+
+santa_status_t santa_decode_dense(const void *q, const santa_kv_t *kv, const santa_shape_t *shape,
+                                  float scale, void *out, void *ws, size_t ws_bytes,
+                                  void *stream) {
+  santa_status_t s = common_checks(q, kv, shape, scale, out, true);
+  if (s != SANTA_OK) return s;
+  const santa::Plan p = make_plan(shape, kv, 0, SANTA_KIND_DENSE);
+  s = check_ws(p, ws, ws_bytes);
+  if (s != SANTA_OK) return s;
+  return hip_status(santa::launch_dense(p, make_view(kv), q, log2_scale(scale), out,
+                                        static_cast<char *>(ws), static_cast<hipStream_t>(stream)));
+}
+
+santa_status_t santa_decode_systematic(const void *q, const santa_kv_t *kv,
+                                       const santa_shape_t *shape, float scale, int32_t S,
+                                       const float *u, int32_t *idx_out, void *out, void *ws,
+                                       size_t ws_bytes, void *stream) {
+  return sampled(q, kv, shape, scale, S, u, idx_out, out, ws, ws_bytes, stream, false);
+}
+
+santa_status_t santa_decode_stratified(const void *q, const santa_kv_t *kv,
+                                       const santa_shape_t *shape, float scale, int32_t S,
+                                       const float *u, int32_t *idx_out, void *out, void *ws,
+                                       size_t ws_bytes, void *stream) {
+  return sampled(q, kv, shape, scale, S, u, idx_out, out, ws, ws_bytes, stream, true);
+}
+
+santa_status_t santa_decode_bernoulli_qk(const void *q, const santa_kt_t *kt,
+                                         const santa_kv_t *kv, const santa_shape_t *shape,
+                                         float scale, int32_t B_draws, int32_t mode,
+                                         const float *u_q, int32_t S, const float *u,
+                                         int32_t *idx_out, uint8_t *feat_mask_out, void *out,
+                                         void *ws, size_t ws_bytes, void *stream) {
+  santa_status_t s = common_checks(q, kv, shape, scale, out, false);
+  if (s != SANTA_OK) return s;
+  if (kv->block_table) return fail(SANTA_ERR_UNSUPPORTED, "Bernoulli scores need a contiguous cache");
+  if (!kt || !kt->k_t) return fail(SANTA_ERR_INVALID_ARG, "kt or kt->k_t is NULL");
+  const int64_t a = shape->dtype == SANTA_BF16 ? 8 : 4;
+  if (kt->stride_b < 0 || kt->stride_h < 0 || kt->stride_d < kv->n_k)
+    return fail(SANTA_ERR_INVALID_ARG, "kt strides must be >= 0 and stride_d >= n_k");
+  if (kt->stride_b % a || kt->stride_h % a || kt->stride_d % a ||
+      (reinterpret_cast<uintptr_t>(kt->k_t) & 15))
+    return fail(SANTA_ERR_UNSUPPORTED, "kt rows must be 16-byte aligned");
+  if (mode != 0 && mode != 1) return fail(SANTA_ERR_INVALID_ARG, "mode must be 0 or 1");
+  if (B_draws < 1 || B_draws > 64) return fail(SANTA_ERR_INVALID_ARG, "B_draws must be in [1, 64]");
+  if (!u_q || !u) return fail(SANTA_ERR_INVALID_ARG, "u_q or u is NULL");
+  if (S < 1 || S > (1 << 24)) return fail(SANTA_ERR_INVALID_ARG, "S must be in [1, 2^24]");
+  const santa::Plan p = make_plan(shape, kv, S, SANTA_KIND_BERNOULLI);
+  s = check_ws(p, ws, ws_bytes);
+  if (s != SANTA_OK) return s;
+  santa::KtView ktv{kt->k_t, kt->stride_b, kt->stride_h, kt->stride_d};
+  return hip_status(santa::launch_bernoulli(p, make_view(kv), ktv, q, log2_scale(scale), B_draws,
+                                            mode, u_q, u, idx_out, feat_mask_out, out,
+                                            static_cast<char *>(ws),
+                                            static_cast<hipStream_t>(stream)));
+}
+
+const char *santa_status_string(santa_status_t status) {
+  switch (status) {
+    case SANTA_OK: return "SANTA_OK";
+    case SANTA_ERR_INVALID_ARG: return "SANTA_ERR_INVALID_ARG";
+    case SANTA_ERR_UNSUPPORTED: return "SANTA_ERR_UNSUPPORTED";
+    case SANTA_ERR_WORKSPACE: return "SANTA_ERR_WORKSPACE";
+    case SANTA_ERR_HIP: return "SANTA_ERR_HIP";
+  }
+  return "SANTA_ERR_UNKNOWN";
+}
+
+const char *santa_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

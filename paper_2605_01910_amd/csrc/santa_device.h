@@ -1,0 +1,166 @@
+// santa_device.h -- gfx950 device helpers for the SANTA decode kernels:
+// 16-byte row-chunk loads, bf16 dot products, DPP reductions within 16-lane
+// rows, wave reductions and scans.  Wave size is 64 (CDNA).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "santa_plan.h"
+
+namespace santa {
+
+constexpr float kInf = __builtin_huge_valf();
+
+typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2_t;
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// a.x*b.x + a.y*b.y + c on packed bf16 pairs (v_dot2c_f32_bf16)
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
+                                         __builtin_bit_cast(bf16x2_t, b), c, false);
+}
+
+// ---------------------------------------------------------------------------
+// 8 consecutive features of one row, loaded with 128-bit loads.
+// bf16: one dwordx4 of packed pairs; f32: two dwordx4.
+// ---------------------------------------------------------------------------
+template <typename E>
+struct Chunk;
+
+template <>
+struct Chunk<uint16_t> {
+  uint4 w;
+  __device__ __forceinline__ static Chunk zero() { return Chunk{make_uint4(0, 0, 0, 0)}; }
+  __device__ __forceinline__ static Chunk load(const uint16_t *p) {
+    return Chunk{*reinterpret_cast<const uint4 *>(p)};
+  }
+  __device__ __forceinline__ void to_float(float (&f)[8]) const {
+    f[0] = bf16_lo(w.x); f[1] = bf16_hi(w.x); f[2] = bf16_lo(w.y); f[3] = bf16_hi(w.y);
+    f[4] = bf16_lo(w.z); f[5] = bf16_hi(w.z); f[6] = bf16_lo(w.w); f[7] = bf16_hi(w.w);
+  }
+  // <this, q> over the 8 features
+  __device__ __forceinline__ float dot(const Chunk &q) const {
+    float a = dot2_bf16(w.x, q.w.x, 0.0f);
+    a = dot2_bf16(w.y, q.w.y, a);
+    a = dot2_bf16(w.z, q.w.z, a);
+    return dot2_bf16(w.w, q.w.w, a);
+  }
+};
+
+template <>
+struct Chunk<float> {
+  float4 a, b;
+  __device__ __forceinline__ static Chunk zero() {
+    return Chunk{make_float4(0, 0, 0, 0), make_float4(0, 0, 0, 0)};
+  }
+  __device__ __forceinline__ static Chunk load(const float *p) {
+    return Chunk{reinterpret_cast<const float4 *>(p)[0], reinterpret_cast<const float4 *>(p)[1]};
+  }
+  __device__ __forceinline__ void to_float(float (&f)[8]) const {
+    f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w; f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
+  }
+  __device__ __forceinline__ float dot(const Chunk &q) const {
+    float s = a.x * q.a.x;
+    s = fmaf(a.y, q.a.y, s); s = fmaf(a.z, q.a.z, s); s = fmaf(a.w, q.a.w, s);
+    s = fmaf(b.x, q.b.x, s); s = fmaf(b.y, q.b.y, s); s = fmaf(b.z, q.b.z, s);
+    return fmaf(b.w, q.b.w, s);
+  }
+};
+
+// ---------------------------------------------------------------------------
+// Cross-lane helpers.  DPP controls (gfx9 encoding): quad_perm [1,0,3,2] = 0xB1,
+// quad_perm [2,3,0,1] = 0x4E, row_half_mirror = 0x141, row_mirror = 0x140.
+// ---------------------------------------------------------------------------
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL,
+                                                               0xf, 0xf, false));
+}
+
+// Sum over the 16 lanes of a DPP row; every lane of the row gets the total.
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp<0xB1>(v);
+  v += dpp<0x4E>(v);
+  v += dpp<0x141>(v);
+  v += dpp<0x140>(v);
+  return v;
+}
+
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, dpp<0xB1>(v));
+  v = fmaxf(v, dpp<0x4E>(v));
+  v = fmaxf(v, dpp<0x141>(v));
+  v = fmaxf(v, dpp<0x140>(v));
+  return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+  v = row16_max(v);
+  v = fmaxf(v, __shfl_xor(v, 16, 64));
+  v = fmaxf(v, __shfl_xor(v, 32, 64));
+  return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+  v = row16_sum(v);
+  v += __shfl_xor(v, 16, 64);
+  v += __shfl_xor(v, 32, 64);
+  return v;
+}
+
+// Inclusive prefix sum over the 64 lanes (fixed order of operations).
+__device__ __forceinline__ float wave_incl_scan(float v, int lane) {
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    float t = __shfl_up(v, off, 64);
+    if (lane >= off) v += t;
+  }
+  return v;
+}
+
+// Inclusive prefix max over the 64 lanes (exact).
+__device__ __forceinline__ float wave_incl_max(float v, int lane) {
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    float t = __shfl_up(v, off, 64);
+    if (lane >= off) v = fmaxf(v, t);
+  }
+  return v;
+}
+
+__device__ __forceinline__ int wave_incl_scan_int(int v, int lane) {
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    int t = __shfl_up(v, off, 64);
+    if (lane >= off) v += t;
+  }
+  return v;
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// ---------------------------------------------------------------------------
+// KV addressing
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int seq_len(const KvView &kv, int b) {
+  if (!kv.ctx) return kv.n_k;
+  int L = kv.ctx[b];
+  return L < 0 ? 0 : (L > kv.n_k ? kv.n_k : L);
+}
+
+// Element offset of token `pos` of sequence b, KV head kvh (feature 0).
+template <bool PAGED>
+__device__ __forceinline__ int64_t row_offset(const KvView &kv, int b, int kvh, int pos) {
+  if constexpr (PAGED) {
+    const int page = kv.bt[(int64_t)b * kv.max_pages + (pos >> kv.ps_log2)];
+    return (int64_t)page * kv.sb + (int64_t)(pos & ((1 << kv.ps_log2) - 1)) * kv.sn +
+           (int64_t)kvh * kv.sh;
+  } else {
+    return (int64_t)b * kv.sb + (int64_t)pos * kv.sn + (int64_t)kvh * kv.sh;
+  }
+}
+
+}  // namespace santa

@@ -1,0 +1,56 @@
+// santa_plan.h -- internal definitions shared by the host dispatcher and the
+// kernels of libsanta: the launch plan (split length, workspace carve-up) and
+// the by-value views the kernels receive.  Not part of the public ABI.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+namespace santa {
+
+constexpr int kHeadDim = 128;   // supported head dimension
+constexpr int kThreads = 256;   // threads per workgroup (4 waves of 64)
+constexpr int kSplitMax = 1024; // largest KV split (keys) handled by one workgroup
+
+// Per-call launch plan.  The KV sequence of every (batch, kv head) row is cut
+// into T splits of Ls keys; each split is one workgroup.  All sizes below are
+// a pure function of (shape, n_k, S, kind), so santa_workspace_size() and the
+// decode calls agree on the layout.
+struct Plan {
+  int B, Hq, Hkv, G, dtype;
+  int n_k;      // max context length
+  int Ls;       // keys per split (multiple of 16, <= kSplitMax)
+  int T;        // splits per row for n_k keys
+  int S;        // samples per row (0 for dense)
+  int kind;     // santa_kind_t
+  // workspace carve-up (byte offsets, 256-aligned)
+  size_t off_stats;  // float2 [B*Hq*T]     per-split (max, sum) in log2 units
+  size_t off_stash;  // float  [B*Hq*T*Ls]  split-local CDF of each row
+  size_t off_offs;   // float  [B*Hq*(T+1)] global split offsets of the CDF
+  size_t off_alpha;  // float  [B*Hq*T]     per-split rescale exp2(m_t - m*)
+  size_t off_rowst;  // float2 [B*Hq]       (m*, Z) per row
+  size_t off_part;   // float  [B*Hkv*T*G*128] per-split partial outputs
+  size_t off_flag;   // int    [B*Hkv*T]    1 if the split holds samples
+  size_t off_bw;     // float  [B*Hq*128]   Bernoulli query weights
+  size_t off_blist;  // int    [B*Hkv*128]  Bernoulli feature list
+  size_t off_bn;     // int    [B*Hkv]      Bernoulli feature count
+  size_t total;
+};
+
+// KV cache as the kernels see it (see santa_kv_t for the addressing rules).
+struct KvView {
+  const void *k, *v;
+  int64_t sb, sn, sh;
+  const int32_t *ctx;   // nullable
+  const int32_t *bt;    // nullable (contiguous)
+  int32_t ps_log2;      // log2(page_size)
+  int32_t max_pages;
+  int32_t n_k;
+};
+
+struct KtView {
+  const void *kt;
+  int64_t sb, sh, sd;
+};
+
+}  // namespace santa

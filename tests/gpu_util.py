@@ -1,0 +1,147 @@
+"""Helpers for the GPU parity tests: move a seeded workload to the device, run
+one entry point through the C ABI, and compare with the CPU oracle under the
+acceptance rules:
+
+  indices  bit-exact, except that index g is also accepted for threshold T
+           when F(g-1) - 1e-5 <= T < F(g) + 1e-5 (F: the oracle's float64 CDF)
+  dense    max |out - oracle| <= 2e-2 and relative L2 <= 5e-3
+  sampled  max |out - oracle_gather(GPU indices)| <= 2e-2
+"""
+
+from __future__ import annotations
+
+import sys
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+from oracle import oracle as O
+from paper_2605_01910_amd import santa as S
+from workload import bf16_bits_to_f32
+
+BAND = 1e-5
+DENSE_MAX_ABS, DENSE_REL_L2, SAMPLED_MAX_ABS = 2e-2, 5e-3, 2e-2
+KIND_CODE = {"dense": S.SANTA_KIND_DENSE, "systematic": S.SANTA_KIND_SYSTEMATIC,
+             "stratified": S.SANTA_KIND_STRATIFIED, "bernoulli": S.SANTA_KIND_BERNOULLI}
+
+
+def log(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def dev_elems(a: np.ndarray) -> torch.Tensor:
+    """numpy bf16 bits (uint16) or float32 -> device tensor of bfloat16 / float32."""
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+    return torch.from_numpy(a).cuda()
+
+
+class DeviceWorkload:
+    """Device copies of a workload plus the C descriptors that point at them."""
+
+    def __init__(self, w, layout: str = "nhd", pass_ctx: bool = True):
+        self.w = w
+        self.q = dev_elems(w.q)
+        self.ctx = torch.from_numpy(w.ctx_len.astype(np.int32)).cuda()
+        self.u = None if w.u is None else torch.from_numpy(w.u).cuda()
+        if w.paged:
+            self.kp, self.vp = dev_elems(w.k_pages), dev_elems(w.v_pages)
+            self.bt = torch.from_numpy(w.block_table).cuda()
+            self.kv = S.kv_paged(self.kp, self.vp, self.bt, self.ctx, w.n_max)
+        else:
+            k, v = dev_elems(w.k), dev_elems(w.v)
+            if layout == "hnd":
+                k, v = k.transpose(1, 2).contiguous(), v.transpose(1, 2).contiguous()
+            self.k, self.v = k, v
+            self.kv = S.kv_contiguous(k, v, self.ctx if pass_ctx else None, layout)
+        if w.kind == "bernoulli":
+            self.kt_t = dev_elems(w.k_t)
+            self.kt = S.kt_feature_major(self.kt_t)
+            self.u_q = torch.from_numpy(w.u_q).cuda()
+        self.shape = S.shape_of(self.q, w.Hkv)
+
+
+def run(w, kind: Optional[str] = None, layout: str = "nhd", want_idx: bool = True,
+        dw: Optional[DeviceWorkload] = None, ws: Optional[torch.Tensor] = None,
+        want_mask: bool = False):
+    """Run one decode step on the GPU; returns (out float64 [rows, d], idx or None, mask)."""
+    kind = kind or w.kind
+    dw = dw or DeviceWorkload(w, layout)
+    out = torch.empty_like(dw.q)
+    Sn = w.S if kind != "dense" else 0
+    if ws is None:
+        ws = S.alloc_workspace(dw.shape, dw.kv, max(Sn, 1), KIND_CODE[kind])
+    idx = None
+    if want_idx and kind != "dense":
+        idx = torch.full((w.B, w.Hq, Sn), -7, dtype=torch.int32, device="cuda")
+    mask = None
+    if kind == "dense":
+        S.santa_decode_dense(dw.q, dw.kv, dw.shape, w.scale, out, ws)
+    elif kind == "systematic":
+        S.santa_decode_systematic(dw.q, dw.kv, dw.shape, w.scale, Sn, dw.u, idx, out, ws)
+    elif kind == "stratified":
+        S.santa_decode_stratified(dw.q, dw.kv, dw.shape, w.scale, Sn, dw.u, idx, out, ws)
+    elif kind == "bernoulli":
+        if want_mask:
+            mask = torch.full((w.B, w.Hkv, w.d), 7, dtype=torch.uint8, device="cuda")
+        S.santa_decode_bernoulli_qk(dw.q, dw.kt, dw.kv, dw.shape, w.scale, w.B_draws, w.mode,
+                                    dw.u_q, Sn, dw.u, idx, mask, out, ws)
+    torch.cuda.synchronize()
+    o = out.float().cpu().numpy().astype(np.float64).reshape(w.B * w.Hq, w.d)
+    ix = None if idx is None else idx.cpu().numpy().reshape(w.B * w.Hq, Sn)
+    mk = None if mask is None else mask.cpu().numpy()
+    return o, ix, mk
+
+
+def check_dense(w, out: np.ndarray, rows: Optional[Sequence[int]] = None) -> dict:
+    res = O.decode_workload(w, "dense", rows=rows)
+    sel = out if rows is None else out[np.asarray(rows)]
+    err = np.abs(sel - res.out)
+    rel = float(np.linalg.norm(sel - res.out) / max(np.linalg.norm(res.out), 1e-300))
+    assert np.all(np.isfinite(sel)), "non-finite GPU output"
+    assert err.max() <= DENSE_MAX_ABS, f"dense max abs error {err.max():.3e}"
+    assert rel <= DENSE_REL_L2, f"dense relative L2 error {rel:.3e}"
+    return {"max_abs": float(err.max()), "rel_l2": rel}
+
+
+def _thresholds(w, kind: str, row: int) -> np.ndarray:
+    if kind == "stratified":
+        return O.thresholds("stratified", w.u.reshape(-1, w.S)[row], w.S)
+    return O.thresholds("systematic", w.u.reshape(-1)[row:row + 1], w.S)
+
+
+def check_sampled(w, out: np.ndarray, idx: np.ndarray, kind: Optional[str] = None,
+                  rows: Optional[Sequence[int]] = None) -> dict:
+    """Band-rule check of every index and gather check of every output row."""
+    kind = kind or w.kind
+    rows = list(range(w.B * w.Hq)) if rows is None else list(rows)
+    res = O.decode_workload(w, kind, rows=rows, want_cdf=True)
+    band, worst = 0, 0.0
+    for i, r in enumerate(rows):
+        b, h = divmod(r, w.Hq)
+        L = int(w.ctx_len[b])
+        g = idx[r]
+        if L == 0:
+            assert np.all(g == -1) and np.all(out[r] == 0), f"row {r}: empty row convention"
+            continue
+        assert np.all((g >= 0) & (g < L)), f"row {r}: index out of range {g.min()}..{g.max()}"
+        o_idx = res.idx[i]
+        C = res.cdf[i, :L]
+        T = _thresholds(w, "stratified" if kind == "stratified" else "systematic", r)
+        diff = np.nonzero(g != o_idx)[0]
+        for m in diff:
+            gm = int(g[m])
+            lo = C[gm - 1] if gm > 0 else 0.0
+            ok = (lo - BAND <= T[m] < C[gm] + BAND) or (gm == L - 1 and T[m] >= C[gm] - BAND)
+            assert ok, (f"row {r} sample {m}: GPU index {gm}, oracle {o_idx[m]}, T={T[m]!r}, "
+                        f"F(g-1)={lo!r}, F(g)={C[gm]!r}")
+        band += len(diff)
+        _, vb = w.logical_kv(b)
+        ref = O.gather_mean(np.ascontiguousarray(vb[:, h // w.G, :]), g)
+        e = float(np.abs(out[r] - ref).max())
+        worst = max(worst, e)
+        assert e <= SAMPLED_MAX_ABS, f"row {r}: sampled max abs error {e:.3e}"
+    return {"band_accepted": band, "max_abs": worst, "rows": len(rows)}

@@ -1,0 +1,109 @@
+"""CPU checks of the C ABI: the library loads, exports every symbol the header
+declares, and rejects bad arguments on the host before any launch."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2605_01910_amd import santa as S
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_symbols():
+    text = open(os.path.join(ROOT, "include", "santa.h")).read()
+    return sorted(set(re.findall(r"\b(santa_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declarations_match_binding_exports():
+    assert declared_symbols() == sorted(S.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = S.load()
+    for name in declared_symbols():
+        assert hasattr(lib, name), name
+
+
+def _shape(B=1, Hq=32, Hkv=8, d=128, dtype=0):
+    return S.santa_shape_t(B, Hq, Hkv, d, dtype)
+
+
+def _kv(n=32768, k=16, v=16, ctx=None, bt=None, ps=0, mp=0, sn=8 * 128):
+    return S.santa_kv_t(k, v, n * 8 * 128, sn, 128, ctx, bt, ps, mp, n)
+
+
+def ws_size(shape, kv, Sn, kind):
+    return S.load().santa_workspace_size(ctypes.byref(shape), ctypes.byref(kv), Sn, kind)
+
+
+def test_workspace_size_is_positive_and_grows_with_batch():
+    a = ws_size(_shape(B=1), _kv(), 256, S.SANTA_KIND_STRATIFIED)
+    b = ws_size(_shape(B=16), _kv(), 256, S.SANTA_KIND_STRATIFIED)
+    assert 0 < a < b
+    assert ws_size(_shape(), _kv(), 256, S.SANTA_KIND_DENSE) > 0
+    assert ws_size(_shape(), _kv(), 256, S.SANTA_KIND_BERNOULLI) >= a
+
+
+@pytest.mark.parametrize("shape,kv,Sn,kind", [
+    (_shape(d=64), _kv(), 256, 1),           # head_dim != 128
+    (_shape(Hq=12, Hkv=8), _kv(), 256, 1),   # Hq not a multiple of Hkv
+    (_shape(Hq=48, Hkv=3), _kv(), 256, 1),   # G = 16 unsupported
+    (_shape(), _kv(n=0), 256, 1),            # empty cache
+    (_shape(), _kv(), 0, 1),                 # S = 0
+    (_shape(), _kv(), (1 << 24) + 1, 2),     # S too large
+    (_shape(), _kv(), 256, 7),               # bad kind
+    (_shape(dtype=5), _kv(), 256, 0),        # bad dtype
+])
+def test_workspace_size_rejects_invalid(shape, kv, Sn, kind):
+    assert ws_size(shape, kv, Sn, kind) == 0
+
+
+def call_sys(shape, kv, Sn=256, u=16, out=16, ws=256, ws_bytes=1 << 40, q=16):
+    lib = S.load()
+    st = lib.santa_decode_systematic(q, ctypes.byref(kv), ctypes.byref(shape), 0.088, Sn, u, None,
+                                     out, ws, ws_bytes, None)
+    return st, lib.santa_last_error().decode()
+
+
+def test_host_validation_errors_before_any_launch():
+    # all of these fail in host validation, so no device pointer is touched
+    assert call_sys(_shape(), _kv(), q=None)[0] == S.SANTA_ERR_INVALID_ARG
+    assert call_sys(_shape(), _kv(), u=None)[0] == S.SANTA_ERR_INVALID_ARG
+    assert call_sys(_shape(), _kv(), Sn=0)[0] == S.SANTA_ERR_INVALID_ARG
+    assert call_sys(_shape(d=256), _kv())[0] == S.SANTA_ERR_UNSUPPORTED
+    assert call_sys(_shape(), _kv(k=None))[0] == S.SANTA_ERR_INVALID_ARG
+    assert call_sys(_shape(), _kv(k=24))[0] == S.SANTA_ERR_UNSUPPORTED        # misaligned
+    assert call_sys(_shape(), _kv(sn=100))[0] == S.SANTA_ERR_UNSUPPORTED      # stride breaks alignment
+    assert call_sys(_shape(), _kv(), ws=None)[0] == S.SANTA_ERR_WORKSPACE
+    assert call_sys(_shape(), _kv(), ws=64)[0] == S.SANTA_ERR_WORKSPACE       # misaligned workspace
+    st, msg = call_sys(_shape(), _kv(), ws_bytes=100)
+    assert st == S.SANTA_ERR_WORKSPACE and "too small" in msg
+    # paged: page size must be a power of two, table must cover n_k
+    assert call_sys(_shape(), _kv(bt=16, ps=12, mp=4096))[0] == S.SANTA_ERR_UNSUPPORTED
+    assert call_sys(_shape(), _kv(bt=16, ps=16, mp=10))[0] == S.SANTA_ERR_INVALID_ARG
+
+
+def test_bernoulli_validation():
+    lib = S.load()
+    sh, kv = _shape(), _kv()
+    kt = S.santa_kt_t(16, 8 * 128 * 32768, 128 * 32768, 32768)
+
+    def call(kt_=kt, Bd=1, mode=0, uq=16, kvx=kv):
+        return lib.santa_decode_bernoulli_qk(16, ctypes.byref(kt_), ctypes.byref(kvx), ctypes.byref(sh),
+                                             0.088, Bd, mode, uq, 256, 16, None, None, 16, 256,
+                                             1 << 40, None)
+
+    assert call(mode=2) == S.SANTA_ERR_INVALID_ARG
+    assert call(Bd=0) == S.SANTA_ERR_INVALID_ARG
+    assert call(uq=None) == S.SANTA_ERR_INVALID_ARG
+    assert call(kt_=S.santa_kt_t(16, 0, 0, 100)) == S.SANTA_ERR_INVALID_ARG      # stride_d < n_k
+    assert call(kvx=_kv(bt=16, ps=16, mp=4096)) == S.SANTA_ERR_UNSUPPORTED       # paged
+
+
+def test_status_strings():
+    lib = S.load()
+    assert lib.santa_status_string(0) == b"SANTA_OK"
+    assert lib.santa_status_string(3) == b"SANTA_ERR_WORKSPACE"

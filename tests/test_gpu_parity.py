@@ -1,0 +1,126 @@
+"""GPU parity of every entry point against the CPU oracle, through the C ABI.
+
+Sizes span several splits and a ragged tail; edge cases cover single-key
+rows, S > L, S = 1, empty rows, fp32 and bf16, G in {1, 2, 4, 8}, both
+contiguous layouts and the paged cache."""
+
+import numpy as np
+import pytest
+import torch
+
+from tests.gpu_util import (DeviceWorkload, check_dense, check_sampled, log, run)
+from workload import make_workload
+
+pytestmark = pytest.mark.gpu
+
+DENSE_CASES = {
+    "cfg1_f32": (1, {}),
+    "cfg2_ragged_b2": (2, dict(B=2, n=3000, ctx_len=[3000, 1234])),
+    "cfg2_g8": (2, dict(B=1, Hq=16, Hkv=2, n=2100)),
+    "cfg2_g2": (2, dict(B=2, Hq=8, Hkv=4, n=700)),
+    "cfg2_single_key": (2, dict(B=2, n=17, ctx_len=[1, 17])),
+    "cfg4_paged": (4, dict(B=3, len_lo=900, len_hi=2600)),
+}
+
+
+@pytest.mark.parametrize("case", sorted(DENSE_CASES))
+def test_dense_parity(case):
+    cfg, over = DENSE_CASES[case]
+    log(f"[dense] {case} cfg={cfg} {over}")
+    w = make_workload(cfg, seed=11, **over)
+    out, _, _ = run(w, "dense")
+    log(f"  {check_dense(w, out)}")
+
+
+def test_dense_head_major_layout():
+    w = make_workload(2, B=2, n=1500, seed=12)
+    log("[dense] head-major layout")
+    out_h, _, _ = run(w, "dense", layout="hnd")
+    check_dense(w, out_h)
+
+
+SAMPLED_CASES = {
+    "cfg1_sys": (1, "systematic", {}),
+    "cfg2_strat_small": (2, "stratified", dict(B=2, n=2500, ctx_len=[2500, 777])),
+    "cfg3_sys_s128": (3, "systematic", dict(B=3, n=3000, S=128)),
+    "cfg3_sys_s512": (3, "systematic", dict(B=2, n=5000, S=512)),
+    "sys_S_gt_L": (2, "systematic", dict(B=2, n=40, S=256, ctx_len=[40, 3])),
+    "strat_S1": (2, "stratified", dict(B=2, n=900, S=1)),
+    "sys_single_key": (2, "systematic", dict(B=2, n=33, S=16, ctx_len=[1, 33])),
+    "sys_g8": (2, "systematic", dict(B=1, Hq=16, Hkv=2, n=2100, S=64)),
+    "strat_g1_bf16": (2, "stratified", dict(B=2, Hq=4, Hkv=4, n=1100, S=32)),
+    "sys_empty_row": (2, "systematic", dict(B=3, n=600, S=32, ctx_len=[600, 0, 5])),
+    "cfg4_paged_sys": (4, "systematic", dict(B=4, len_lo=700, len_hi=3000)),
+}
+
+
+@pytest.mark.parametrize("case", sorted(SAMPLED_CASES))
+def test_sampled_parity(case):
+    cfg, kind, over = SAMPLED_CASES[case]
+    log(f"[{kind}] {case} cfg={cfg} {over}")
+    w = make_workload(cfg, seed=21, kind=kind, **over)
+    out, idx, _ = run(w, kind)
+    log(f"  {check_sampled(w, out, idx, kind)}")
+
+
+def test_sampled_head_major_layout():
+    w = make_workload(2, B=2, n=1800, kind="systematic", S=64, seed=22)
+    log("[systematic] head-major layout")
+    out, idx, _ = run(w, layout="hnd")
+    check_sampled(w, out, idx)
+
+
+BERN_CASES = {
+    "mode0_B1": dict(B=2, n=1500, mode=0, B_draws=1),
+    "mode1_B1": dict(B=2, n=1500, mode=1, B_draws=1),
+    "mode0_B4": dict(B=1, n=2100, mode=0, B_draws=4, ctx_len=[2001]),
+    "mode1_B8_ragged": dict(B=2, n=999, mode=1, B_draws=8, ctx_len=[999, 123]),
+}
+
+
+@pytest.mark.parametrize("case", sorted(BERN_CASES))
+def test_bernoulli_parity(case):
+    over = BERN_CASES[case]
+    log(f"[bernoulli] {case} {over}")
+    w = make_workload(5, seed=31, **over)
+    out, idx, mask = run(w, "bernoulli", want_mask=True)
+    log(f"  {check_sampled(w, out, idx, 'bernoulli')}")
+    from oracle import oracle as O
+    res = O.decode_workload(w, "bernoulli", rows=[b * w.Hq + kv * w.G for b in range(w.B)
+                                                  for kv in range(w.Hkv)], want_weights=True)
+    ref_mask = res.mask.reshape(w.B, w.Hkv, w.d)
+    assert np.array_equal(mask, ref_mask), "feature mask differs from the oracle"
+
+
+def test_repeat_calls_are_bitwise_identical():
+    w = make_workload(2, B=2, n=4000, kind="stratified", S=256, seed=41)
+    dw = DeviceWorkload(w)
+    log("[determinism] stratified x2, dense x2")
+    o1, i1, _ = run(w, dw=dw)
+    o2, i2, _ = run(w, dw=dw)
+    assert np.array_equal(o1, o2) and np.array_equal(i1, i2)
+    d1, _, _ = run(w, "dense", dw=dw)
+    d2, _, _ = run(w, "dense", dw=dw)
+    assert np.array_equal(d1, d2)
+
+
+def test_ctx_len_null_means_full_length():
+    w = make_workload(2, B=2, n=1300, kind="systematic", S=64, seed=42)
+    dw = DeviceWorkload(w, pass_ctx=False)
+    log("[systematic] ctx_len = NULL")
+    out, idx, _ = run(w, dw=dw)
+    check_sampled(w, out, idx)
+
+
+def test_workspace_reuse_across_shapes():
+    """One workspace sized for the larger call serves a smaller call next."""
+    from paper_2605_01910_amd import santa as S
+    big = make_workload(2, B=2, n=3000, kind="systematic", S=128, seed=43)
+    small = make_workload(2, B=1, n=700, kind="systematic", S=128, seed=44)
+    dwb, dws = DeviceWorkload(big), DeviceWorkload(small)
+    ws = S.alloc_workspace(dwb.shape, dwb.kv, 128, S.SANTA_KIND_SYSTEMATIC)
+    log("[workspace] big then small")
+    ob, ib, _ = run(big, dw=dwb, ws=ws)
+    os_, is_, _ = run(small, dw=dws, ws=ws)
+    check_sampled(big, ob, ib)
+    check_sampled(small, os_, is_)

@@ -116,7 +116,7 @@ class Workload:
     v_pages: Optional[np.ndarray] = None
     block_table: Optional[np.ndarray] = None
     # Bernoulli score stage
-    k_t: Optional[np.ndarray] = None          # feature-major keys [B, Hkv, d, n_max]
+    k_t: Optional[np.ndarray] = None          # feature-major keys [B, Hkv, d, n_pad >= n_max]
     u_q: Optional[np.ndarray] = None          # [B, Hq, d] (mode 0) or [B, Hkv, d] (mode 1)
     B_draws: int = 0
     mode: int = 0
@@ -193,7 +193,8 @@ def make_workload(cfg: int, seed: int = 0, **over) -> Workload:
                                                    endpoint=True).astype(np.int32)
     else:
         ctx = np.full(B, n, dtype=np.int32)
-    n_max = int(max(n, int(ctx.max()) if B else 0))
+    # paged caches are sized by their longest sequence; contiguous ones by n
+    n_max = int(ctx.max()) if paged else int(max(n, int(ctx.max()) if B else 0))
 
     # planted positions: `heavy` distinct positions in [1, L) per (b, kv head)
     nh = int(p.get("heavy", 0))
@@ -263,7 +264,10 @@ def make_workload(cfg: int, seed: int = 0, **over) -> Workload:
     if kind == "bernoulli":
         w.B_draws = int(p.get("B_draws", 1))
         w.mode = int(p.get("mode", 0))
-        w.k_t = np.ascontiguousarray(w.k.transpose(0, 2, 3, 1))   # [B, Hkv, d, n_max]
+        # feature-major keys [B, Hkv, d, n_pad]; rows padded to 64 keys (128 B bf16)
+        n_pad = (n_max + 63) // 64 * 64
+        w.k_t = np.zeros((B, Hkv, d, n_pad), dtype=w.k.dtype)
+        w.k_t[..., :n_max] = w.k.transpose(0, 2, 3, 1)
         rq = _rng(cfg, STREAM_UQ, seed)
         w.u_q = rq.random((B, Hq if w.mode == 0 else Hkv, d), dtype=np.float32)
     return w
