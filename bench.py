@@ -1,0 +1,260 @@
+#!/usr/bin/env python3
+"""Decode-step benchmark of the SANTA / S2ANTA HIP path on one MI355X.
+
+Workload (default): Llama-3.1-8B attention layer at 32k context, batch 1 --
+32 query heads, 8 KV heads, head_dim 128, bf16, n_k = 32768, sink + 32
+planted heavy keys per KV head, stratified sampling with S = 256 (seeded
+synthetic inputs, see workload/gen.py).  One "step" is one call of
+santa_decode_stratified over the whole batch.
+
+Protocol (the paper's decode microbenchmark, adapted): inputs are built and
+uploaded before timing; W untimed warm-up steps; then K timed steps, each
+preceded (outside the timed region) by an in-place update of a 1 GiB buffer
+(the paper's cache-thrash step) and a read-only pass over a second 2 GiB
+buffer, so that neither L2 nor the 256 MB Infinity Cache holds the KV cache and
+no dirty flush lines are left to be written back during the timed call; HIP
+events recorded on the library's stream around each call.  The exact dense
+kernel of the same library is timed the same way on the same inputs.
+
+value = algorithmic bytes / mean step time, where algorithmic bytes = all keys
++ the unique value rows the step gathers (counted from idx_out in an untimed
+call) + q + out + uniforms.  Prints one JSON line.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode-attn µs/step + HBM GB/s (% of peak) at 32k ctx, vs dense decode"
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=40)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--cfg", type=int, default=2, help="workload configuration (1..5)")
+    ap.add_argument("--B", type=int, default=None)
+    ap.add_argument("--S", type=int, default=None)
+    ap.add_argument("--kind", default=None)
+    ap.add_argument("--layout", default="nhd", choices=["nhd", "hnd"])
+    ap.add_argument("--flush-gib", type=float, default=1.0)
+    ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--profile", action="store_true",
+                    help="timed loops only (for rocprofv3 runs); still prints the JSON line")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        sys.stderr.write("bench.py: this build runs on exactly one GPU; --gpus N > 1 is not "
+                         "supported (the decode step has no multi-GPU path here).\n")
+        sys.exit(2)
+
+    import torch
+    from paper_2605_01910_amd import santa as S
+    from workload import make_workload
+
+    S.load()  # fails loudly if the HIP library is missing
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    over = {}
+    if args.B is not None:
+        over["B"] = args.B
+    if args.S is not None:
+        over["S"] = args.S
+    if args.kind is not None:
+        over["kind"] = args.kind
+    t0 = time.time()
+    w = make_workload(args.cfg, seed=0, **over)
+    print(f"[bench] workload cfg={args.cfg} B={w.B} Hq={w.Hq} Hkv={w.Hkv} n={w.n_max} "
+          f"kind={w.kind} S={w.S} built in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+
+    from tests.gpu_util import DeviceWorkload, KIND_CODE
+    dw = DeviceWorkload(w, layout=args.layout)
+    kind = w.kind
+    out = torch.empty_like(dw.q)
+    ws = S.alloc_workspace(dw.shape, dw.kv, max(w.S, 1), KIND_CODE[kind])
+    ws_dense = S.alloc_workspace(dw.shape, dw.kv, 1, S.SANTA_KIND_DENSE)
+    stream = torch.cuda.current_stream()
+    mask = None
+    if kind == "bernoulli":
+        mask = torch.empty((w.B, w.Hkv, w.d), dtype=torch.uint8, device=dev)
+
+    def step(idx_out=None):
+        if kind == "systematic":
+            S.santa_decode_systematic(dw.q, dw.kv, dw.shape, w.scale, w.S, dw.u, idx_out, out, ws,
+                                      stream)
+        elif kind == "stratified":
+            S.santa_decode_stratified(dw.q, dw.kv, dw.shape, w.scale, w.S, dw.u, idx_out, out, ws,
+                                      stream)
+        elif kind == "bernoulli":
+            S.santa_decode_bernoulli_qk(dw.q, dw.kt, dw.kv, dw.shape, w.scale, w.B_draws, w.mode,
+                                        dw.u_q, w.S, dw.u, idx_out, mask, out, ws, stream)
+        else:
+            S.santa_decode_dense(dw.q, dw.kv, dw.shape, w.scale, out, ws, stream)
+
+    def dense_step():
+        S.santa_decode_dense(dw.q, dw.kv, dw.shape, w.scale, out, ws_dense, stream)
+
+    # ---- algorithmic bytes (untimed call with idx_out) ----
+    esz = 2 if w.dtype == "bf16" else 4
+    L = w.ctx_len.astype(np.int64)
+    k_bytes = int(L.sum()) * w.Hkv * w.d * esz
+    uniq_rows = 0
+    feat_frac = 1.0
+    if kind != "dense":
+        idx = torch.empty((w.B, w.Hq, w.S), dtype=torch.int32, device=dev)
+        step(idx)
+        torch.cuda.synchronize()
+        ix = idx.cpu().numpy().reshape(w.B, w.Hkv, w.G * w.S)
+        uniq_rows = int(sum(len(np.unique(ix[b, k])) for b in range(w.B) for k in range(w.Hkv)))
+        if kind == "bernoulli":
+            m = mask.cpu().numpy()
+            feat_frac = float(m.mean())
+            k_bytes = int(sum(int(m[b].sum()) * int(L[b]) for b in range(w.B))) * esz
+    v_bytes = (uniq_rows if kind != "dense" else int(L.sum()) * w.Hkv) * w.d * esz
+    io_bytes = 2 * w.B * w.Hq * w.d * esz + (w.u.nbytes if w.u is not None else 0)
+    if kind == "bernoulli":
+        io_bytes += w.u_q.nbytes
+    alg_bytes = k_bytes + v_bytes + io_bytes
+    dense_bytes = 2 * int(L.sum()) * w.Hkv * w.d * esz + 2 * w.B * w.Hq * w.d * esz
+
+    # ---- timing ----
+    flush = torch.empty(int(args.flush_gib * (1 << 30)) // 4, dtype=torch.float32, device=dev)
+    flush.zero_()
+    flush_ro = torch.zeros(2 * flush.numel(), dtype=torch.float32, device=dev)
+
+    def cold_cache():
+        flush.add_(1.0)        # evicts L2 / Infinity Cache / TLB (paper's in-place update)
+        flush_ro.sum()         # clean lines: the update's dirty lines are written back now
+
+    def timed(fn, steps, warmup, cold=True):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(steps)]
+        for a, b in evs:
+            if cold:
+                cold_cache()
+            a.record(stream)
+            fn()
+            b.record(stream)
+        torch.cuda.synchronize()
+        us = np.array([a.elapsed_time(b) * 1e3 for a, b in evs])
+        return us
+
+    torch.cuda.synchronize()
+    wall0 = time.time()
+    us = timed(step, args.steps, args.warmup)
+    wall = time.time() - wall0
+    print(f"[bench] {kind}: mean {us.mean():.2f} us  median {np.median(us):.2f}  min {us.min():.2f}",
+          file=sys.stderr, flush=True)
+    res = {}
+    if not args.no_dense and kind != "dense":
+        dus = timed(dense_step, args.steps, args.warmup)
+        res["dense_us_per_step"] = round(float(dus.mean()), 3)
+        res["dense_gbs"] = round(dense_bytes / (dus.mean() * 1e-6) / 1e9, 1)
+        res["speedup_vs_dense"] = round(float(dus.mean() / us.mean()), 3)
+        print(f"[bench] dense: mean {dus.mean():.2f} us", file=sys.stderr, flush=True)
+    if not args.profile:
+        warm = timed(step, args.steps, 2, cold=False)
+        res["warm_us_per_step"] = round(float(warm.mean()), 3)
+
+    gbs = alg_bytes / (us.mean() * 1e-6) / 1e9
+    line = {
+        "metric": METRIC,
+        "value": round(gbs, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(float(us.mean()) / 1e3, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": (f"cfg{args.cfg}: {w.kind} S={w.S}, B={w.B}, Hq={w.Hq}, Hkv={w.Hkv}, d={w.d}, "
+                         f"n_k={w.n_max}, {w.dtype}, {args.layout} cache, cold cache "
+                         f"({args.flush_gib:g} GiB update + {2 * args.flush_gib:g} GiB read per step)"),
+            "variant": os.environ.get("SANTA_VARIANT", "fused"),
+            "batch": w.B, "n_k": w.n_max, "S": w.S, "kind": w.kind,
+        },
+        "us_per_step": round(float(us.mean()), 3),
+        "us_median": round(float(np.median(us)), 3),
+        "us_min": round(float(us.min()), 3),
+        "hbm_frac_of_peak": round(gbs / PEAK_HBM_GBS, 4),
+        "bytes_touched": alg_bytes,
+        "bytes_breakdown": {"k": k_bytes, "v_unique_rows": v_bytes, "q_out_u": io_bytes},
+        "unique_v_rows": uniq_rows,
+        "k_feature_fraction": round(feat_frac, 4),
+        **res,
+        "roofline": {
+            "bound": "hbm",
+            "kernel": ("k_fused_" + ("dense" if kind == "dense" else "sampled")
+                       if os.environ.get("SANTA_VARIANT", "fused") != "multi" and kind != "bernoulli"
+                       else "all kernels of one santa_decode_* call"),
+            "timing": "HIP events around the single library call (includes launch latency)",
+            "achieved": round(gbs, 1),
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": round(gbs / PEAK_HBM_GBS, 4),
+            "traffic": None,
+        },
+        "timed_wall_s": round(wall, 3),
+    }
+
+    if not args.no_cpu and not args.profile:
+        line["cpu_baseline"] = cpu_baseline(w, kind, alg_bytes, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(w, kind, alg_bytes, seconds):
+    """The CPU oracle (float64 C, OpenMP over rows) timed on this host on full
+    decode steps of the same workload, repeated for about `seconds`."""
+    from oracle import oracle as O
+
+    O.lib()
+    reps, total, threads = 0, 0.0, 1
+    t_end = time.time() + seconds
+    while True:
+        t0 = time.perf_counter()
+        r = O.decode_workload(w, kind)
+        total += time.perf_counter() - t0
+        threads = r.threads
+        reps += 1
+        if time.time() >= t_end or reps >= 2000:
+            break
+    per = total / reps
+    return {
+        "value": round(alg_bytes / per / 1e9, 3),
+        "unit": "GB/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"{reps} full decode step(s) of the same workload (all {w.B * w.Hq} rows), "
+                   f"{per * 1e3:.1f} ms per step, float64, {threads} OpenMP threads, "
+                   f"host nproc={os.cpu_count()}"),
+        "ms_per_step": round(per * 1e3, 3),
+    }
+
+
+if __name__ == "__main__":
+    main()

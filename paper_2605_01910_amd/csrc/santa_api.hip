@@ -3,7 +3,9 @@
 // here allocates device memory or synchronises.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
+#include <cstdlib>
 #include <string>
 
 #include "santa.h"
@@ -37,6 +39,34 @@ int choose_split(int64_t rows, int64_t n_k) {
   int p = 256;
   while (p < santa::kSplitMax && p * 2 <= ls) p *= 2;
   return p;
+}
+
+// Tuning knobs read from the environment on every call (measurement sweeps and
+// tests of both paths; a workspace must be sized under the same settings):
+//   SANTA_VARIANT=multi  use the multi-kernel path instead of the fused launch
+//   SANTA_SPLITS=T       splits per row of the fused path
+//   SANTA_XCD=0          do not place a row's splits on one XCD
+struct Tuning {
+  int fused, splits, xcd;
+};
+
+Tuning tuning() {
+  Tuning r{1, 0, 1};
+  if (const char *v = std::getenv("SANTA_VARIANT")) r.fused = std::string(v) != "multi";
+  if (const char *v = std::getenv("SANTA_SPLITS")) r.splits = std::atoi(v);
+  if (const char *v = std::getenv("SANTA_XCD")) r.xcd = std::atoi(v) != 0;
+  return r;
+}
+
+// Splits per row of the fused path: enough that the whole batch of rows fills
+// about 1024 workgroups (4 per CU), at least ceil(n_k / kSplitMax).
+int fused_splits(int64_t rows_kv, int64_t n_k) {
+  const int tmin = (int)((n_k + santa::kSplitMax - 1) / santa::kSplitMax);
+  int fill = 128;
+  while (fill > 1 && (int64_t)fill * rows_kv > 512) fill >>= 1;
+  int T = std::max(tmin, fill);
+  if (tuning().splits > 0) T = std::max(tmin, tuning().splits);
+  return T;
 }
 
 santa_status_t check_shape(const santa_shape_t *sh) {
@@ -96,6 +126,23 @@ santa::Plan make_plan(const santa_shape_t *sh, const santa_kv_t *kv, int S, int 
     off = align256(off + bytes);
     return o;
   };
+  const Tuning tune = tuning();
+  const int Tf = fused_splits((int64_t)p.B * p.Hkv, p.n_k);
+  if (kind != SANTA_KIND_BERNOULLI && tune.fused && Tf <= santa::kMaxSplits) {
+    // fused layout: counters first (they must start at zero: santa_workspace_init)
+    p.fused = 1;
+    p.xcd = tune.xcd;
+    p.T = Tf;
+    // rows use ceil(L_b / T) keys per split rounded up to 16; Ls is the longest
+    p.Ls = (int)(((p.n_k + p.T - 1) / p.T + 15) & ~15);
+    p.off_err = take(4);
+    p.off_sync = take((size_t)p.B * p.Hkv * santa::kSyncStride * 4);
+    p.off_stats = take(rows * p.T * 8);
+    p.off_part = take((size_t)p.B * p.Hkv * p.T * p.G * D * 4);
+    p.off_flag = take((size_t)p.B * p.Hkv * p.T * 4);
+    p.total = off;
+    return p;
+  }
   p.off_stats = take(rows * p.T * 8);
   p.off_part = take((size_t)p.B * p.Hkv * p.T * p.G * D * 4);
   if (kind != SANTA_KIND_DENSE) {
@@ -168,6 +215,10 @@ santa_status_t sampled(const void *q, const santa_kv_t *kv, const santa_shape_t 
   const santa::Plan p = make_plan(sh, kv, S, strat ? SANTA_KIND_STRATIFIED : SANTA_KIND_SYSTEMATIC);
   s = check_ws(p, ws, ws_bytes);
   if (s != SANTA_OK) return s;
+  if (p.fused)
+    return hip_status(santa::launch_fused_sampled(p, make_view(kv), q, log2_scale(scale), strat, u,
+                                                  idx_out, out, static_cast<char *>(ws),
+                                                  static_cast<hipStream_t>(stream)));
   return hip_status(santa::launch_sampled(p, make_view(kv), q, log2_scale(scale), strat, u, idx_out,
                                           out, static_cast<char *>(ws),
                                           static_cast<hipStream_t>(stream)));
@@ -200,6 +251,10 @@ santa_status_t santa_decode_dense(const void *q, const santa_kv_t *kv, const san
   const santa::Plan p = make_plan(shape, kv, 0, SANTA_KIND_DENSE);
   s = check_ws(p, ws, ws_bytes);
   if (s != SANTA_OK) return s;
+  if (p.fused)
+    return hip_status(santa::launch_fused_dense(p, make_view(kv), q, log2_scale(scale), out,
+                                                static_cast<char *>(ws),
+                                                static_cast<hipStream_t>(stream)));
   return hip_status(santa::launch_dense(p, make_view(kv), q, log2_scale(scale), out,
                                         static_cast<char *>(ws), static_cast<hipStream_t>(stream)));
 }

@@ -97,48 +97,64 @@ __device__ __forceinline__ float row16_max(float v) {
   return v;
 }
 
-__device__ __forceinline__ float wave_max(float v) {
-  v = row16_max(v);
-  v = fmaxf(v, __shfl_xor(v, 16, 64));
-  v = fmaxf(v, __shfl_xor(v, 32, 64));
-  return v;
+// Lane-wise combination with the lane 16 (32) apart, on every lane, using the
+// gfx950 lane-swap instructions (VALU, no LDS crossbar).  Both lanes of a pair
+// see the operands in the same order, so they get bitwise-identical results.
+__device__ __forceinline__ float xor16_sum(float v) {
+  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(p[0]) + __uint_as_float(p[1]);
+}
+__device__ __forceinline__ float xor32_sum(float v) {
+  const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(p[0]) + __uint_as_float(p[1]);
+}
+__device__ __forceinline__ float xor16_max(float v) {
+  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1]));
+}
+__device__ __forceinline__ float xor32_max(float v) {
+  const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1]));
 }
 
-__device__ __forceinline__ float wave_sum(float v) {
-  v = row16_sum(v);
-  v += __shfl_xor(v, 16, 64);
-  v += __shfl_xor(v, 32, 64);
-  return v;
+// Wave-wide max / sum; every lane gets the same value.
+__device__ __forceinline__ float wave_max(float v) { return xor32_max(xor16_max(row16_max(v))); }
+__device__ __forceinline__ float wave_sum(float v) { return xor32_sum(xor16_sum(row16_sum(v))); }
+
+// DPP with a fill value for lanes that have no source lane.
+template <int CTRL, int ROWS = 0xf>
+__device__ __forceinline__ float dpp_fill(float fill, float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, fill),
+                                                               __builtin_bit_cast(int, v), CTRL,
+                                                               ROWS, 0xf, false));
 }
 
-// Inclusive prefix sum over the 64 lanes (fixed order of operations).
-__device__ __forceinline__ float wave_incl_scan(float v, int lane) {
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    float t = __shfl_up(v, off, 64);
-    if (lane >= off) v += t;
-  }
+// Inclusive prefix sum over the 64 lanes in a fixed order: row_shr 1/2/4/8
+// within each row of 16, then row_bcast 15 and 31 across rows.
+__device__ __forceinline__ float wave_incl_scan(float v) {
+  v += dpp_fill<0x111>(0.0f, v);
+  v += dpp_fill<0x112>(0.0f, v);
+  v += dpp_fill<0x114>(0.0f, v);
+  v += dpp_fill<0x118>(0.0f, v);
+  v += dpp_fill<0x142, 0xa>(0.0f, v);
+  v += dpp_fill<0x143, 0xc>(0.0f, v);
   return v;
 }
 
 // Inclusive prefix max over the 64 lanes (exact).
-__device__ __forceinline__ float wave_incl_max(float v, int lane) {
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    float t = __shfl_up(v, off, 64);
-    if (lane >= off) v = fmaxf(v, t);
-  }
+__device__ __forceinline__ float wave_incl_max(float v) {
+  const float ninf = -__builtin_huge_valf();
+  v = fmaxf(v, dpp_fill<0x111>(ninf, v));
+  v = fmaxf(v, dpp_fill<0x112>(ninf, v));
+  v = fmaxf(v, dpp_fill<0x114>(ninf, v));
+  v = fmaxf(v, dpp_fill<0x118>(ninf, v));
+  v = fmaxf(v, dpp_fill<0x142, 0xa>(ninf, v));
+  v = fmaxf(v, dpp_fill<0x143, 0xc>(ninf, v));
   return v;
 }
 
-__device__ __forceinline__ int wave_incl_scan_int(int v, int lane) {
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    int t = __shfl_up(v, off, 64);
-    if (lane >= off) v += t;
-  }
-  return v;
-}
+// Value of the previous lane (wave_shr:1); lane 0 gets `fill`.
+__device__ __forceinline__ float wave_prev(float fill, float v) { return dpp_fill<0x138>(fill, v); }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 

@@ -3,6 +3,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "santa_plan.h"
 
 namespace santa {
@@ -20,5 +22,36 @@ hipError_t launch_bernoulli(const Plan &p, const KvView &kv, const KtView &kt, c
                             hipStream_t st);
 
 hipError_t launch_zero(void *ws, size_t bytes, hipStream_t st);
+
+hipError_t launch_fused_dense(const Plan &p, const KvView &kv, const void *q, float scale_log2,
+                              void *out, char *ws, hipStream_t st);
+
+hipError_t launch_fused_sampled(const Plan &p, const KvView &kv, const void *q, float scale_log2,
+                                bool strat, const float *u, int32_t *idx_out, void *out, char *ws,
+                                hipStream_t st);
+
+// Compile-time dispatch over the GQA group size, element type and cache kind.
+template <typename F>
+inline hipError_t with_g(int G, F &&f) {
+  switch (G) {
+    case 1: return f(std::integral_constant<int, 1>{});
+    case 2: return f(std::integral_constant<int, 2>{});
+    case 4: return f(std::integral_constant<int, 4>{});
+    case 8: return f(std::integral_constant<int, 8>{});
+  }
+  return hipErrorInvalidValue;
+}
+
+template <typename F>
+inline hipError_t with_types(const Plan &p, bool paged, F &&f) {
+  return with_g(p.G, [&](auto gc) -> hipError_t {
+    if (p.dtype == 0) {
+      if (paged) return f((uint16_t *)nullptr, gc, std::true_type{});
+      return f((uint16_t *)nullptr, gc, std::false_type{});
+    }
+    if (paged) return f((float *)nullptr, gc, std::true_type{});
+    return f((float *)nullptr, gc, std::false_type{});
+  });
+}
 
 }  // namespace santa

@@ -19,165 +19,10 @@
 // same inputs give bitwise-identical outputs.
 #include <hip/hip_runtime.h>
 
-#include "santa_device.h"
 #include "santa_kernels.h"
+#include "santa_tiles.h"
 
 namespace santa {
-
-// ---------------------------------------------------------------------------
-// shared device pieces
-// ---------------------------------------------------------------------------
-template <typename E, int G>
-struct QRegs {
-  Chunk<E> h[G];
-};
-
-template <typename E, int G>
-__device__ __forceinline__ QRegs<E, G> load_q(const E *q, int b, int Hq, int kvh, int c) {
-  QRegs<E, G> r;
-#pragma unroll
-  for (int h = 0; h < G; ++h)
-    r.h[h] = Chunk<E>::load(q + ((int64_t)b * Hq + kvh * G + h) * kHeadDim + c * 8);
-  return r;
-}
-
-__device__ __forceinline__ float to_f32(uint16_t x) { return __uint_as_float((uint32_t)x << 16); }
-__device__ __forceinline__ float to_f32(float x) { return x; }
-
-__device__ __forceinline__ void store_out(uint16_t *p, float x) {
-  uint32_t u = __float_as_uint(x);
-  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) {
-    *p = 0x7fc0;  // NaN
-    return;
-  }
-  u += 0x7fffu + ((u >> 16) & 1u);  // round to nearest even
-  *p = (uint16_t)(u >> 16);
-}
-__device__ __forceinline__ void store_out(float *p, float x) { *p = x; }
-
-// Score tile (Sec. 2, SDPA equation, the q K^T product):
-// s[h*kSplitMax + j] = scale_log2 * <q_h, K_{start+j}> for j < nrows.
-// Lane c of each 16-lane row holds features 8c..8c+7 of one key; a wave covers
-// 4 keys per 128-bit load and U loads are in flight per lane.
-template <typename E, int G, bool PAGED, int U>
-__device__ __forceinline__ void score_tile(const KvView &kv, int b, int kvh, int start, int nrows,
-                                           const QRegs<E, G> &qr, float scale_log2, float *s) {
-  const int tid = threadIdx.x, slot = tid >> 4, c = tid & 15;
-  const E *K = static_cast<const E *>(kv.k);
-  for (int base = 0; base < nrows; base += 16 * U) {
-    Chunk<E> ch[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int j = base + u * 16 + slot;
-      ch[u] = j < nrows ? Chunk<E>::load(K + row_offset<PAGED>(kv, b, kvh, start + j) + c * 8)
-                        : Chunk<E>::zero();
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int j = base + u * 16 + slot;
-      float acc[G];
-#pragma unroll
-      for (int h = 0; h < G; ++h) acc[h] = row16_sum(ch[u].dot(qr.h[h]));
-      if (c == 0 && j < nrows) {
-#pragma unroll
-        for (int h = 0; h < G; ++h) s[h * kSplitMax + j] = acc[h] * scale_log2;
-      }
-    }
-  }
-}
-
-// Split-local CDF of one head, computed by one wave (Sec. 2.1, "Construction":
-// F is the running sum of the attention weights).  On return s[j] holds
-// P_j = sum_{i<=j} exp2(s_i - m) for j < nrows, where m = max_j s_j is returned.
-// Each lane owns a contiguous run of keys and sums it sequentially; the runs are
-// joined by a wave prefix sum.
-__device__ float wave_split_cdf(float *s, int nrows, int lane) {
-  float m = -kInf;
-  for (int j = lane; j < nrows; j += 64) m = fmaxf(m, s[j]);
-  m = wave_max(m);
-  constexpr int CH = kSplitMax / 64;
-  const int ch = (nrows + 63) >> 6;
-  const int j0 = lane * ch;
-  float loc[CH];
-  float run = 0.0f;
-#pragma unroll
-  for (int i = 0; i < CH; ++i) {
-    if (i < ch) {
-      const int j = j0 + i;
-      run += j < nrows ? fast_exp2(s[j] - m) : 0.0f;
-      loc[i] = run;
-    }
-  }
-  const float incl = wave_incl_scan(run, lane);
-  float base = __shfl_up(incl, 1, 64);
-  if (lane == 0) base = 0.0f;
-#pragma unroll
-  for (int i = 0; i < CH; ++i) {
-    if (i < ch) {
-      const int j = j0 + i;
-      if (j < nrows) s[j] = base + loc[i];
-    }
-  }
-  return m;
-}
-
-// After the split's scores are in s[]: build each head's split CDF and write
-// the split statistics (m_t, l_t = P_last) and the CDF stash.
-template <int G>
-__device__ __forceinline__ void finish_split_cdf(float *s, float *mh, int nrows, int64_t row0,
-                                                 int T, int t, int64_t stash_pitch, int start,
-                                                 float2 *stats, float *stash) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  for (int h = wave; h < G; h += kThreads / 64) {
-    const float m = wave_split_cdf(s + h * kSplitMax, nrows, lane);
-    if (lane == 0) mh[h] = m;
-  }
-  __syncthreads();
-  if (tid < G) stats[(row0 + tid) * T + t] = make_float2(mh[tid], s[tid * kSplitMax + nrows - 1]);
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    float *dst = stash + (row0 + h) * stash_pitch + start;
-    for (int j = tid; j < nrows; j += kThreads) dst[j] = s[h * kSplitMax + j];
-  }
-}
-
-// Sum of acc[G][8] over the 16 row slots of the workgroup (4 per wave, 4 waves)
-// into red[G*128] (fixed order); thread tid then owns outputs tid, tid+256, ...
-template <int G>
-__device__ __forceinline__ void reduce_slots(float (&acc)[G][8], float *red /* [4][G*128] */) {
-  const int tid = threadIdx.x, wave = tid >> 6, c = tid & 15;
-#pragma unroll
-  for (int h = 0; h < G; ++h)
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      float v = acc[h][i];
-      v += __shfl_xor(v, 16, 64);
-      v += __shfl_xor(v, 32, 64);
-      acc[h][i] = v;
-    }
-  if ((tid & 63) < 16) {
-#pragma unroll
-    for (int h = 0; h < G; ++h)
-#pragma unroll
-      for (int i = 0; i < 8; ++i) red[wave * G * kHeadDim + h * kHeadDim + c * 8 + i] = acc[h][i];
-  }
-  __syncthreads();
-}
-
-__device__ __forceinline__ float threshold(int r, float ur, float invS, float Z) {
-  return ((float)r + ur) * invS * Z;
-}
-
-// Number of j < n with a * P[j] <= x (P non-decreasing): branch-free binary lifting.
-__device__ __forceinline__ int cdf_count(const float *P, int n, float a, float x) {
-  int pos = 0;
-#pragma unroll
-  for (int step = kSplitMax; step > 0; step >>= 1) {
-    const int np = pos + step;
-    if (np <= n && a * P[np - 1] <= x) pos = np;
-  }
-  return pos;
-}
 
 // ---------------------------------------------------------------------------
 // dense: split partials and merge
@@ -199,7 +44,8 @@ __global__ __launch_bounds__(kThreads) void k_dense_split(KvView kv, const E *__
   const int64_t row0 = (int64_t)b * Hq + kvh * G;
 
   const QRegs<E, G> qr = load_q<E, G>(q, b, Hq, kvh, c);
-  score_tile<E, G, PAGED, 8>(kv, b, kvh, start, nrows, qr, scale_log2, s);
+  float mx[G];
+  score_tile<E, G, PAGED, kScoreUnroll>(kv, b, kvh, start, nrows, qr, scale_log2, s, kSplitMax, mx);
   __syncthreads();
   // split max and exponentials e_j = exp2(s_j - m_t), l_t = sum_j e_j
   for (int h = wave; h < G; h += kThreads / 64) {
@@ -299,7 +145,8 @@ __global__ __launch_bounds__(kThreads) void k_score_cdf(KvView kv, const E *__re
   __shared__ float s[G * kSplitMax];
   __shared__ float mh[G];
   const QRegs<E, G> qr = load_q<E, G>(q, b, Hq, kvh, threadIdx.x & 15);
-  score_tile<E, G, PAGED, 8>(kv, b, kvh, start, nrows, qr, scale_log2, s);
+  float mx[G];
+  score_tile<E, G, PAGED, kScoreUnroll>(kv, b, kvh, start, nrows, qr, scale_log2, s, kSplitMax, mx);
   __syncthreads();
   finish_split_cdf<G>(s, mh, nrows, (int64_t)b * Hq + kvh * G, T, t, (int64_t)T * Ls, start,
                       stats, stash);
@@ -336,18 +183,15 @@ __global__ __launch_bounds__(64) void k_offsets(KvView kv, int Hq, int Ls, int T
       tot = fmaf(a, st[t].y, tot);
     }
   }
-  const float incl = wave_incl_scan(tot, lane);
-  float base = __shfl_up(incl, 1, 64);
-  if (lane == 0) base = 0.0f;
+  const float base = wave_prev(0.0f, wave_incl_scan(tot));
   // lane runs are non-decreasing; lift each run to the max of all earlier runs' ends
   float run = base;
   for (int i = 0; i < ch; ++i) {
     const int t = t0 + i;
     if (t < Tb) run = fmaf(al[t], st[t].y, run);
   }
-  const float pm = wave_incl_max(run, lane);
-  float floor_v = __shfl_up(pm, 1, 64);
-  if (lane == 0) floor_v = 0.0f;
+  const float pm = wave_incl_max(run);
+  const float floor_v = wave_prev(0.0f, pm);
   run = base;
   for (int i = 0; i < ch; ++i) {
     const int t = t0 + i;
@@ -357,21 +201,15 @@ __global__ __launch_bounds__(64) void k_offsets(KvView kv, int Hq, int Ls, int T
     }
   }
   // Z is the inclusive max over all lanes, i.e. the last offset written
-  const float Z = __shfl(pm, 63, 64);
+  const float Z = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(pm), 63));
   if (lane == 0) {
     off[0] = 0.0f;
     rowst[row] = make_float2(m, Z);
   }
 }
 
-// Threshold claim, inverse-CDF search and gather-add for one split.
-// Threshold m of head h (Sec. 2.1, "Construction"): systematic (m + u)/S or
-// stratified (m + u_m)/S, scaled by Z.  The split claims the thresholds in
-// [Off_t, Off_{t+1}); for each, the key index is #{j : a_t P_j <= tau - Off_t}
-// (the CDF interval containing the threshold, App. A), clamped to the split.
-// Counts c_{h,j} are accumulated in LDS; the union over the group's heads of
-// the chosen keys is compacted in key order and each V row is read once:
-// O_h += c_{h,j} V_j.
+// Threshold claim, inverse-CDF search and gather-add for one split, from the
+// stashed split CDF (see claim_gather).
 template <typename E, int G, bool PAGED, bool STRAT>
 __global__ __launch_bounds__(kThreads) void k_sample(
     KvView kv, int Hq, int Ls, int T, int S, float invS, const float *__restrict__ u,
@@ -384,11 +222,11 @@ __global__ __launch_bounds__(kThreads) void k_sample(
   if (start >= L) return;
   const int nrows = min(Ls, L - start);
   const int Tb = (L + Ls - 1) / Ls;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, slot = tid >> 4, c = tid & 15;
+  const int tid = threadIdx.x;
   const int64_t row0 = (int64_t)b * Hq + kvh * G;
   const int64_t sid = ((int64_t)b * gridDim.y + kvh) * T + t;
 
-  __shared__ float lo_s[G], hi_s[G], z_s[G], a_s[G];
+  __shared__ HeadClaim hc[G];
   __shared__ float P[G * kSplitMax];  // split CDF; reused as the slot-reduction buffer
   __shared__ int cnt[G * kSplitMax];
   __shared__ int list[kSplitMax];
@@ -396,23 +234,11 @@ __global__ __launch_bounds__(kThreads) void k_sample(
 
   if (tid < G) {
     const int64_t r = row0 + tid;
-    lo_s[tid] = offs[r * (T + 1) + t];
-    hi_s[tid] = t == Tb - 1 ? kInf : offs[r * (T + 1) + t + 1];
-    z_s[tid] = rowst[r].y;
-    a_s[tid] = alpha[r * T + t];
+    hc[tid] = HeadClaim{offs[r * (T + 1) + t], t == Tb - 1 ? kInf : offs[r * (T + 1) + t + 1],
+                        rowst[r].y, alpha[r * T + t]};
   }
   __syncthreads();
-  int any = 0;
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    const float lo = lo_s[h], hi = hi_s[h], Z = z_s[h];
-    const float *uh = STRAT ? u + (row0 + h) * S : u + (row0 + h);
-    for (int r = tid; r < S; r += kThreads) {
-      const float tau = threshold(r, STRAT ? uh[r] : uh[0], invS, Z);
-      any |= (tau >= lo) & (tau < hi);
-    }
-  }
-  if (!__syncthreads_or(any)) {
+  if (!any_claims<G, STRAT>(hc, row0, S, invS, u)) {
     if (tid == 0) flags[sid] = 0;
     return;
   }
@@ -426,87 +252,10 @@ __global__ __launch_bounds__(kThreads) void k_sample(
     }
   }
   __syncthreads();
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    const float lo = lo_s[h], hi = hi_s[h], Z = z_s[h], a = a_s[h];
-    const float *uh = STRAT ? u + (row0 + h) * S : u + (row0 + h);
-    for (int r = tid; r < S; r += kThreads) {
-      const float tau = threshold(r, STRAT ? uh[r] : uh[0], invS, Z);
-      if (tau >= lo && tau < hi) {
-        int j = cdf_count(P + h * kSplitMax, nrows, a, tau - lo);
-        j = j < nrows ? j : nrows - 1;
-        atomicAdd(&cnt[h * kSplitMax + j], 1);
-        if (idx_out) idx_out[(row0 + h) * S + r] = start + j;
-      }
-    }
-  }
-  __syncthreads();
-  // compact the union of chosen keys in key order (each wave a contiguous range)
-  const int per_wave = ((nrows + 255) >> 8) << 6;
-  const int jb = wave * per_wave, je = min(nrows, jb + per_wave);
-  int wcount = 0;
-  for (int j0 = jb; j0 < je; j0 += 64) {
-    const int j = j0 + lane;
-    bool need = false;
-    if (j < je)
-#pragma unroll
-      for (int h = 0; h < G; ++h) need |= cnt[h * kSplitMax + j] != 0;
-    wcount += __popcll(__ballot(need));
-  }
-  if (lane == 0) wave_cnt[wave] = wcount;
-  __syncthreads();
-  int pos = 0;
-  for (int w = 0; w < wave; ++w) pos += wave_cnt[w];
-  const int nlist = wave_cnt[0] + wave_cnt[1] + wave_cnt[2] + wave_cnt[3];
-  for (int j0 = jb; j0 < je; j0 += 64) {
-    const int j = j0 + lane;
-    bool need = false;
-    if (j < je)
-#pragma unroll
-      for (int h = 0; h < G; ++h) need |= cnt[h * kSplitMax + j] != 0;
-    const uint64_t mask = __ballot(need);
-    if (need) list[pos + __popcll(mask & ((1ull << lane) - 1ull))] = j;
-    pos += __popcll(mask);
-  }
-  __syncthreads();
-  // gather-add: slot takes list entries slot, slot+16, ...; 4 rows in flight
-  const E *V = static_cast<const E *>(kv.v);
-  float acc[G][8];
-#pragma unroll
-  for (int h = 0; h < G; ++h)
-#pragma unroll
-    for (int i = 0; i < 8; ++i) acc[h][i] = 0.0f;
-  constexpr int U = 4;
-  for (int e0 = slot; e0 < nlist; e0 += 16 * U) {
-    Chunk<E> ch[U];
-    int jj[U];
-#pragma unroll
-    for (int uu = 0; uu < U; ++uu) {
-      const int e = e0 + uu * 16;
-      jj[uu] = e < nlist ? list[e] : -1;
-      ch[uu] = jj[uu] >= 0 ? Chunk<E>::load(V + row_offset<PAGED>(kv, b, kvh, start + jj[uu]) + c * 8)
-                           : Chunk<E>::zero();
-    }
-#pragma unroll
-    for (int uu = 0; uu < U; ++uu) {
-      if (jj[uu] < 0) continue;
-      float f[8];
-      ch[uu].to_float(f);
-#pragma unroll
-      for (int h = 0; h < G; ++h) {
-        const float w = (float)cnt[h * kSplitMax + jj[uu]];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) acc[h][i] = fmaf(w, f[i], acc[h][i]);
-      }
-    }
-  }
-  reduce_slots<G>(acc, P);
-  for (int o = tid; o < G * kHeadDim; o += kThreads) {
-    float v = 0.0f;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) v += P[w * G * kHeadDim + o];
-    part[sid * G * kHeadDim + o] = v;
-  }
+  claim_search<G, STRAT>(start, nrows, row0, S, invS, STRAT ? u + row0 * S : u + row0,
+                         STRAT ? S : 1, hc, P, kSplitMax, cnt, idx_out);
+  gather_union<E, G, PAGED, false>(kv, b, kvh, start, nrows, P, kSplitMax, cnt, list, wave_cnt,
+                                   part + sid * G * kHeadDim);
   if (tid == 0) flags[sid] = 1;
 }
 
@@ -687,29 +436,6 @@ __global__ __launch_bounds__(kThreads) void k_bern_score(KvView kv, KtView kt, i
 // ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
-template <typename F>
-static hipError_t with_g(int G, F &&f) {
-  switch (G) {
-    case 1: return f(std::integral_constant<int, 1>{});
-    case 2: return f(std::integral_constant<int, 2>{});
-    case 4: return f(std::integral_constant<int, 4>{});
-    case 8: return f(std::integral_constant<int, 8>{});
-  }
-  return hipErrorInvalidValue;
-}
-
-template <typename F>
-static hipError_t with_types(const Plan &p, bool paged, F &&f) {
-  return with_g(p.G, [&](auto gc) -> hipError_t {
-    if (p.dtype == 0) {
-      if (paged) return f((uint16_t *)nullptr, gc, std::true_type{});
-      return f((uint16_t *)nullptr, gc, std::false_type{});
-    }
-    if (paged) return f((float *)nullptr, gc, std::true_type{});
-    return f((float *)nullptr, gc, std::false_type{});
-  });
-}
-
 template <typename T>
 static T *ws_at(char *ws, size_t off) {
   return reinterpret_cast<T *>(ws + off);

@@ -11,6 +11,8 @@ namespace santa {
 constexpr int kHeadDim = 128;   // supported head dimension
 constexpr int kThreads = 256;   // threads per workgroup (4 waves of 64)
 constexpr int kSplitMax = 1024; // largest KV split (keys) handled by one workgroup
+constexpr int kMaxSplits = 256; // largest number of splits per row in the fused kernels
+constexpr int kSyncStride = 64; // ints per row of fused-path counters (256 B apart)
 
 // Per-call launch plan.  The KV sequence of every (batch, kv head) row is cut
 // into T splits of Ls keys; each split is one workgroup.  All sizes below are
@@ -23,6 +25,8 @@ struct Plan {
   int T;        // splits per row for n_k keys
   int S;        // samples per row (0 for dense)
   int kind;     // santa_kind_t
+  int fused;    // 1: single persistent launch (per-row split lengths), 0: multi-kernel
+  int xcd;      // fused: place each row's splits on one XCD
   // workspace carve-up (byte offsets, 256-aligned)
   size_t off_stats;  // float2 [B*Hq*T]     per-split (max, sum) in log2 units
   size_t off_stash;  // float  [B*Hq*T*Ls]  split-local CDF of each row
@@ -34,6 +38,8 @@ struct Plan {
   size_t off_bw;     // float  [B*Hq*128]   Bernoulli query weights
   size_t off_blist;  // int    [B*Hkv*128]  Bernoulli feature list
   size_t off_bn;     // int    [B*Hkv]      Bernoulli feature count
+  size_t off_err;    // int    [1]          fused: barrier wait gave up
+  size_t off_sync;   // int    [B*Hkv*2]    fused: per-row arrival / completion counters
   size_t total;
 };
 

@@ -124,3 +124,50 @@ def test_workspace_reuse_across_shapes():
     os_, is_, _ = run(small, dw=dws, ws=ws)
     check_sampled(big, ob, ib)
     check_sampled(small, os_, is_)
+
+
+MULTI_CASES = {
+    "dense_cfg2": (2, "dense", dict(B=2, n=3000, ctx_len=[3000, 1234])),
+    "strat_cfg2": (2, "stratified", dict(B=2, n=2500, ctx_len=[2500, 777])),
+    "sys_paged": (4, "systematic", dict(B=3, len_lo=700, len_hi=3000)),
+    "sys_f32": (1, "systematic", {}),
+}
+
+
+@pytest.mark.parametrize("case", sorted(MULTI_CASES))
+def test_multi_kernel_variant_parity(case, monkeypatch):
+    """The multi-kernel path (score/CDF stash, offsets, sample, merge launches)."""
+    monkeypatch.setenv("SANTA_VARIANT", "multi")
+    cfg, kind, over = MULTI_CASES[case]
+    log(f"[multi/{kind}] {case} cfg={cfg} {over}")
+    w = make_workload(cfg, seed=51, kind=kind if kind != "dense" else "systematic", **over)
+    out, idx, _ = run(w, kind)
+    if kind == "dense":
+        check_dense(w, out)
+    else:
+        log(f"  {check_sampled(w, out, idx, kind)}")
+
+
+@pytest.mark.parametrize("splits,xcd", [(16, "1"), (64, "0"), (200, "1")])
+def test_fused_split_counts(splits, xcd, monkeypatch):
+    """Fused path at other split counts, with and without XCD placement."""
+    monkeypatch.setenv("SANTA_SPLITS", str(splits))
+    monkeypatch.setenv("SANTA_XCD", xcd)
+    w = make_workload(2, B=3, n=5000, kind="stratified", S=128, ctx_len=[5000, 2222, 17], seed=52)
+    log(f"[fused splits={splits} xcd={xcd}]")
+    out, idx, _ = run(w)
+    check_sampled(w, out, idx)
+    d, _, _ = run(w, "dense")
+    check_dense(w, d)
+
+
+def test_fused_barrier_flag_stays_clear():
+    """The fused path's bounded barrier wait never gives up on these inputs."""
+    from paper_2605_01910_amd import santa as S
+    w = make_workload(2, B=16, n=1024, kind="systematic", S=64, seed=53)
+    dw = DeviceWorkload(w)
+    ws = S.alloc_workspace(dw.shape, dw.kv, w.S, S.SANTA_KIND_SYSTEMATIC)
+    for _ in range(3):
+        out, idx, _ = run(w, dw=dw, ws=ws)
+    check_sampled(w, out, idx)
+    assert int(ws[:4].view(torch.int32).item()) == 0
