@@ -168,6 +168,18 @@ santa_status_t santa_decode_bernoulli_qk(const void *q, const santa_kt_t *kt,
                                          int32_t *idx_out, uint8_t *feat_mask_out, void *out,
                                          void *ws, size_t ws_bytes, void *stream);
 
+/* Profiling hook (not part of the method).  start_event and stop_event are
+ * hipEvent_t handles created by the caller with timing enabled.  The next
+ * santa_decode_* call made on the calling thread attaches them to its own
+ * kernels: the GPU records start_event when the call's first kernel is
+ * dispatched and stop_event when its last kernel completes, so
+ * hipEventElapsedTime(start, stop) is the call's execution time on the device
+ * without host launch latency.  One-shot: that call consumes the request even
+ * if it fails validation.  (NULL, NULL) cancels a pending request; exactly one
+ * NULL is SANTA_ERR_INVALID_ARG.  The events stay owned by the caller and must
+ * outlive the call's kernels. */
+santa_status_t santa_time_next_call(void *start_event, void *stop_event);
+
 /* Human-readable name of a status code. */
 const char *santa_status_string(santa_status_t status);
 

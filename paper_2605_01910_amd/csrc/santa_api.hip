@@ -15,6 +15,12 @@
 namespace {
 
 thread_local std::string g_last_error;
+thread_local santa::CallTimer g_timer;
+
+// Consumes the pending call timer when a decode entry point returns.
+struct TimerScope {
+  ~TimerScope() { g_timer = santa::CallTimer{}; }
+};
 
 santa_status_t fail(santa_status_t s, const std::string &msg) {
   g_last_error = msg;
@@ -48,18 +54,23 @@ int choose_split(int64_t rows, int64_t n_k) {
 //   SANTA_XCD=0          do not place a row's splits on one XCD
 struct Tuning {
   int fused, splits, xcd;
+  int sampled_path;  // 0: by size, 1: one persistent launch, 2: two launches
 };
 
 Tuning tuning() {
-  Tuning r{1, 0, 1};
+  Tuning r{1, 0, 1, 0};
   if (const char *v = std::getenv("SANTA_VARIANT")) r.fused = std::string(v) != "multi";
   if (const char *v = std::getenv("SANTA_SPLITS")) r.splits = std::atoi(v);
   if (const char *v = std::getenv("SANTA_XCD")) r.xcd = std::atoi(v) != 0;
+  if (const char *v = std::getenv("SANTA_SAMPLED")) {
+    const std::string s(v);
+    r.sampled_path = s == "fused" ? 1 : s == "split" ? 2 : 0;
+  }
   return r;
 }
 
 // Splits per row of the fused path: enough that the whole batch of rows fills
-// about 1024 workgroups (4 per CU), at least ceil(n_k / kSplitMax).
+// about 512 workgroups (2 per CU), at least ceil(n_k / kSplitMax).
 int fused_splits(int64_t rows_kv, int64_t n_k) {
   const int tmin = (int)((n_k + santa::kSplitMax - 1) / santa::kSplitMax);
   int fill = 128;
@@ -133,13 +144,24 @@ santa::Plan make_plan(const santa_shape_t *sh, const santa_kv_t *kv, int S, int 
     p.fused = 1;
     p.xcd = tune.xcd;
     p.T = Tf;
-    // rows use ceil(L_b / T) keys per split rounded up to 16; Ls is the longest
-    p.Ls = (int)(((p.n_k + p.T - 1) / p.T + 15) & ~15);
-    p.off_err = take(4);
-    p.off_sync = take((size_t)p.B * p.Hkv * santa::kSyncStride * 4);
-    p.off_stats = take(rows * p.T * 8);
-    p.off_part = take((size_t)p.B * p.Hkv * p.T * p.G * D * 4);
-    p.off_flag = take((size_t)p.B * p.Hkv * p.T * 4);
+    // rows use ceil(L_b / T) keys per split rounded up to 64; Ls is the longest
+    p.Ls = (int)(((p.n_k + p.T - 1) / p.T + 63) & ~63);
+    const bool sampled = kind != SANTA_KIND_DENSE;
+    // sampled steps whose rows do not fit in one resident round of about 1024
+    // workgroups take the two-launch path
+    p.split2 = sampled && (tune.sampled_path == 2 ||
+                           (tune.sampled_path == 0 && (int64_t)p.B * p.Hkv * p.T > 1024));
+    if (p.split2) {
+      p.npitch = ((int64_t)p.n_k + 63) & ~int64_t(63);
+      p.off_stats = take(rows * p.T * 8);
+      p.off_stash = take(rows * (size_t)p.npitch * 4);
+      p.off_coarse = take(rows * (size_t)(p.npitch / 32) * 4);
+    } else {
+      p.off_err = take(4);
+      p.off_sync = take((size_t)p.B * p.Hkv * santa::kSyncStride * 4);
+      p.off_stats = take(rows * p.T * 8);
+      p.off_part = take((size_t)p.B * p.Hkv * p.T * p.G * D * 4);
+    }
     p.total = off;
     return p;
   }
@@ -208,6 +230,7 @@ santa_status_t common_checks(const void *q, const santa_kv_t *kv, const santa_sh
 santa_status_t sampled(const void *q, const santa_kv_t *kv, const santa_shape_t *sh, float scale,
                        int32_t S, const float *u, int32_t *idx_out, void *out, void *ws,
                        size_t ws_bytes, void *stream, bool strat) {
+  TimerScope timer_scope;
   santa_status_t s = common_checks(q, kv, sh, scale, out, true);
   if (s != SANTA_OK) return s;
   if (S < 1 || S > (1 << 24)) return fail(SANTA_ERR_INVALID_ARG, "S must be in [1, 2^24]");
@@ -225,6 +248,8 @@ santa_status_t sampled(const void *q, const santa_kv_t *kv, const santa_shape_t 
 }
 
 }  // namespace
+
+santa::CallTimer &santa::call_timer() { return g_timer; }
 
 extern "C" {
 
@@ -246,6 +271,7 @@ santa_status_t santa_workspace_init(void *ws, size_t ws_bytes, void *stream) {
 santa_status_t santa_decode_dense(const void *q, const santa_kv_t *kv, const santa_shape_t *shape,
                                   float scale, void *out, void *ws, size_t ws_bytes,
                                   void *stream) {
+  TimerScope timer_scope;
   santa_status_t s = common_checks(q, kv, shape, scale, out, true);
   if (s != SANTA_OK) return s;
   const santa::Plan p = make_plan(shape, kv, 0, SANTA_KIND_DENSE);
@@ -279,6 +305,7 @@ santa_status_t santa_decode_bernoulli_qk(const void *q, const santa_kt_t *kt,
                                          const float *u_q, int32_t S, const float *u,
                                          int32_t *idx_out, uint8_t *feat_mask_out, void *out,
                                          void *ws, size_t ws_bytes, void *stream) {
+  TimerScope timer_scope;
   santa_status_t s = common_checks(q, kv, shape, scale, out, false);
   if (s != SANTA_OK) return s;
   if (kv->block_table) return fail(SANTA_ERR_UNSUPPORTED, "Bernoulli scores need a contiguous cache");
@@ -301,6 +328,15 @@ santa_status_t santa_decode_bernoulli_qk(const void *q, const santa_kt_t *kt,
                                             mode, u_q, u, idx_out, feat_mask_out, out,
                                             static_cast<char *>(ws),
                                             static_cast<hipStream_t>(stream)));
+}
+
+santa_status_t santa_time_next_call(void *start_event, void *stop_event) {
+  g_last_error.clear();
+  if ((start_event == nullptr) != (stop_event == nullptr))
+    return fail(SANTA_ERR_INVALID_ARG, "start_event and stop_event must both be set or both NULL");
+  g_timer.start = static_cast<hipEvent_t>(start_event);
+  g_timer.stop = static_cast<hipEvent_t>(stop_event);
+  return SANTA_OK;
 }
 
 const char *santa_status_string(santa_status_t status) {

@@ -1,35 +1,46 @@
-// santa_fused.hip -- single-launch decode kernels (persistent).
+// santa_fused.hip -- the default decode kernels.
 //
-// Every (batch b, KV head k) row is cut into T splits; split t of a row is one
-// work item and one 256-thread workgroup.  The grid holds R whole rows per
-// round (R*T workgroups, no more than fit on the GPU at once, so all of them
-// are resident), and loops over rounds for larger batches.  Split lengths are per row (ceil(L_b/T) rounded
-// to 16 keys), so ragged batches keep T splits of similar length per row.
+// Every (batch b, KV head k) row is cut into Tb <= T splits of Ls keys (Ls =
+// ceil(L_b / T) rounded up to 64); split t of a row is one work item of one
+// 256-thread workgroup.
 //
-// Sampled step, per work item:
-//   1. stream the split's keys, scores for the G heads into LDS, split-local
-//      CDF in LDS (Sec. 2.1: F is the running sum of the attention weights);
-//   2. publish (m_t, l_t) and wait until every split of the row has (per-row
-//      barrier, see row_arrive_wait; bounded spin);
-//   3. every workgroup of the row computes the same global offsets
-//      Off_t = sum_{t'<t} exp2(m_t' - m*) l_t' and Z, so threshold tau falls
-//      in exactly one split; the split claims its thresholds, inverts its own
-//      LDS CDF and gathers the chosen V rows (claim_gather);
-//   4. after a second barrier every workgroup of the row sums its own slice of
-//      the row's outputs over the split partials in split order, scales by 1/S
-//      and writes it.
-// Dense step: 1 and the exact V stream per split, one barrier, then the same
-// distributed merge with the max/sum-exp rescaling.
+// Sampled step, small batches (one persistent launch, k_fused_sampled).  The
+// grid holds R whole rows per round (R*T workgroups, all resident) and loops
+// over rounds.  Per work item:
+//   1. stream the split's keys; scores of the G heads in LDS; split-local CDF
+//      P_j = sum_{i<=j} exp2(s_i - m_t) in LDS (Sec. 2.1: F is the running sum
+//      of the attention weights); publish (m_t, l_t = P_last);
+//   2. wait until every split of the row has published (row counter);
+//   3. global offsets Off_t = sum_{t'<t} a_t' l_t' with a_t = exp2(m_t - m*)
+//      and the total Z, identical in every split; threshold tau_r = ((r + u)/S) Z
+//      (u per row, or u_r) is claimed by the split with Off_t <= tau_r <
+//      Off_{t+1}; tau_r is non-decreasing in r, so the claimed r form one range,
+//      found by binary search; each claimed tau_r maps to the key
+//      #{j : a_t P_j <= tau_r - Off_t} (the CDF interval holding it, App. A),
+//      clamped to the split; the union of chosen keys over the group's heads
+//      is gathered once per key and the G x 128 partial sums are published;
+//   4. take an arrival rank; the last G arrivals each merge one head:
+//      O_h = (1/S) sum_t o_t in split order.
+// Sampled step, large batches (two launches): k_stream_cdf streams every work
+// item and writes the split-local CDF of every key (the stash), the CDF at
+// every 32-key block end and the split statistics; then k_value_heads, one
+// workgroup per query head, finds each threshold's split from the offsets,
+// its 32-key block from the block ends and the key inside the block from the
+// stash, and gathers the chosen V rows once per distinct key.
+// Dense step (k_fused_dense): the split's exact softmax-weighted V sum o_t with
+// (m_t, l_t); the last G arrivals merge O = sum_t a_t o_t / sum_t a_t l_t.
 //
-// Cross-workgroup data (split statistics, partial sums, flags, counters) is
-// written and read with relaxed agent-scope atomics, which are coherent per
-// access across the XCDs' L2s; a writer waits for its stores to complete
-// before it arrives at a barrier.  No cache-wide write-back or invalidation is
-// issued.
+// Inside one launch, cross-workgroup data (statistics, partial sums,
+// counters) is written and read with relaxed agent-scope atomics, which are
+// coherent per access across the XCDs' L2s; a writer waits for its stores to
+// complete before it arrives.  No cache-wide write-back or invalidation is
+// issued.  Between the two launches of the large-batch path the kernel
+// boundary orders the accesses and plain loads and stores are used.
 //
 // Each row's workgroups are placed on one XCD when the round holds a multiple
 // of 8 rows (workgroups are dispatched round-robin over the 8 XCDs), so the
-// row's barrier and merge traffic stays in one L2.
+// row's counter and exchange traffic stays in one L2.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -46,37 +57,59 @@ struct FusedArgs {
   void *out;
   const float *u;
   int32_t *idx_out;
-  float2 *stats;  // [B*Hq][T]        (m_t, l_t) per head and split
-  float *part;    // [B*Hkv][T][G*128] split partial outputs
-  int *flags;     // [B*Hkv][T]        sampled: split holds samples
+  float2 *stats;  // [B*Hq][T]          (m_t, l_t) per head and split
+  float *part;    // [B*Hkv][T][G*128]  split partial outputs
+  float *stash;   // [B*Hq][npitch]     two-launch path: split-local CDF of every key
+  float *coarse;  // [B*Hq][npitch/32]  two-launch path: the CDF at every 32-key block end
   unsigned long long *sync;  // [B*Hkv][kSyncStride/2] arrival counter, counter base
-  int *err;       // [1]               set if a barrier wait gave up
+  int *err;       // [1]                set if a wait gave up
   int B, Hq, Hkv, T, S;
-  int Lsmax;  // longest split (keys) of any row: LDS arrays are sized by it
-  int ustage; // stratified uniforms of the group staged in LDS (G*S floats) if 1
+  int Lsmax;      // longest split (keys) of any row: LDS arrays are sized by it
+  int ustage;     // stratified uniforms of the group staged in LDS (G*S floats) if 1
+  int64_t npitch; // stash floats per head row (n_k rounded up to 64)
   float invS, scale_log2;
   int xcd;
 };
 
 constexpr int kSpinLimit = 1 << 22;
+constexpr int kAlign = 64;         // split lengths and stash rows are multiples of this many keys
+constexpr int kBlock = 32;         // keys per block of the two-level CDF search
+constexpr int kGatherUnroll = 8;   // V rows in flight per row slot in k_value_heads
 
-// LDS layout of the fused kernels (dynamic shared memory), in floats.  The
-// reduction buffers hold both the slot reduction (4 x G x 128 floats) and the
-// per-thread merge partial sums (kThreads floats).
-__host__ __device__ constexpr int fused_red_floats(int G) {
-  return 4 * G * kHeadDim > kThreads ? 4 * G * kHeadDim : kThreads;
+// ---------------------------------------------------------------------------
+// LDS sizes (dynamic shared memory), in floats
+// ---------------------------------------------------------------------------
+// k_fused_sampled: P [G][Lsmax] (scores, CDF; then the slot reduction and the
+// merge scratch), cnt [G][Lsmax], list [max(Lsmax, 2G(T+1))] (offsets and
+// split factors before the claims, the union list after), ul [G*S] if staged.
+__host__ __device__ constexpr int imax(int x, int y) { return x > y ? x : y; }
+__host__ __device__ constexpr int fused_p_floats(int G, int Lsmax, int T) {
+  return imax(imax(G * Lsmax, 4 * G * kHeadDim), T + kThreads);
 }
-__host__ __device__ constexpr int fused_p_floats(int G, int Lsmax) {
-  return G * Lsmax > fused_red_floats(G) ? G * Lsmax : fused_red_floats(G);
+__host__ __device__ constexpr int fused_list_ints(int G, int Lsmax, int T) {
+  return imax(Lsmax, 2 * G * (T + 1));
+}
+__host__ __device__ constexpr int fused_sampled_floats(int G, int Lsmax, int T, int ustaged) {
+  return fused_p_floats(G, Lsmax, T) + G * Lsmax + fused_list_ints(G, Lsmax, T) + ustaged;
+}
+// k_fused_dense: s [G][Lsmax], red [4][G*128] (also the merge scratch).
+__host__ __device__ constexpr int fused_dense_floats(int G, int Lsmax, int T) {
+  return G * Lsmax + imax(4 * G * kHeadDim, T + kThreads);
+}
+// k_stream_cdf: P [G][Lsmax].
+// k_value_heads: block ends [ncoarse], offsets [T+1], split factors [T], chosen
+// keys and run list [2][kThreads], slot reduction [4][128].
+__host__ __device__ constexpr int value_heads_floats(int T, int ncoarse) {
+  return ncoarse + (T + 1) + T + 2 * kThreads + 4 * kHeadDim;
 }
 
 __device__ __forceinline__ void split_geometry(int L, int T, int &Ls, int &Tb) {
   if (L <= 0) {
-    Ls = 16;
+    Ls = kAlign;
     Tb = 0;
     return;
   }
-  Ls = (((L + T - 1) / T) + 15) & ~15;
+  Ls = (((L + T - 1) / T) + kAlign - 1) & ~(kAlign - 1);
   Tb = (L + Ls - 1) / Ls;
 }
 
@@ -92,46 +125,67 @@ __device__ __forceinline__ void map_item(int w, int T, int R, int xcd, int &rho,
   }
 }
 
-// Per-row barrier.  sync[0] counts arrivals and only ever grows; sync[1] holds
-// its value when the current call started (the base).  The k-th barrier of a
-// call waits until the count reaches base + k*n; the row's first split
-// advances the base for the next call once every split has read it (after the
-// first barrier).  Arrival is a fire-and-forget atomic add, so no workgroup
-// waits on another's read-modify-write, and nothing has to be reset.
-__device__ __forceinline__ void row_arrive_wait(unsigned long long *sync, unsigned long long target,
-                                                int *err) {
-  __hip_atomic_fetch_add(sync, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  int spins = 0;
-  while (__hip_atomic_load(sync, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-    if (++spins > kSpinLimit) {
-      atomicOr(err, 1);
-      break;
-    }
-    __builtin_amdgcn_s_sleep(1);
-  }
+template <bool COHERENT>
+__device__ __forceinline__ float2 ld2(const float2 *p) {
+  if constexpr (COHERENT) return ld_coherent(p);
+  return *p;
 }
 
-// All threads: make this workgroup's shared stores visible, arrive, wait.
-__device__ __forceinline__ void row_sync(unsigned long long *sync, unsigned long long target,
-                                         int *err) {
+// ---------------------------------------------------------------------------
+// Row counter.  sync[0] counts arrivals and only ever grows; sync[1] holds its
+// value when the current call started (the base).  A split reads the base
+// when it starts; the counter passes base + Tb once every split has published
+// its statistics and base + 2 Tb once every split has published its partial
+// sums; the last of those arrivals advances the base by 2 Tb for the next
+// call, when every split has read it.  Nothing is reset between calls.
+// ---------------------------------------------------------------------------
+// All threads: make this workgroup's global stores complete, then take an
+// arrival rank relative to `from` (block-uniform).
+__device__ __forceinline__ int row_arrive(unsigned long long *sync, unsigned long long from,
+                                          int *rank_lds) {
   wait_stores();
   __syncthreads();
-  if (threadIdx.x == 0) row_arrive_wait(sync, target, err);
+  if (threadIdx.x == 0) {
+    const unsigned long long old =
+        __hip_atomic_fetch_add(sync, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    *rank_lds = (int)(old - from);
+  }
+  __syncthreads();
+  return *rank_lds;
+}
+
+// All threads: wait until the counter reaches `target` (bounded spin; on
+// giving up the error flag is set and the caller's results are not valid).
+__device__ __forceinline__ void row_wait(const unsigned long long *sync, unsigned long long target,
+                                         int *err) {
+  if (threadIdx.x == 0) {
+    int spins = 0;
+    while (__hip_atomic_load(const_cast<unsigned long long *>(sync), __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT) < target) {
+      if (++spins > kSpinLimit) {
+        atomicOr(err, 1);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+  }
   __syncthreads();
 }
 
 // One wave: global offsets of one head over the row's Tb splits.  off[0..Tb]
-// receives Off_0 = 0, Off_{t+1} = Off_t + exp2(m_t - m*) l_t, made exactly
-// non-decreasing; returns m*.  Identical in every workgroup of the row.  Lane l
-// owns splits l*ch .. l*ch+ch-1 (ch <= kMaxSplits / 64).
-__device__ __forceinline__ float row_offsets_wave(const float2 *st, int Tb, int lane, float *off) {
+// receives Off_0 = 0, Off_{t+1} = Off_t + a_t l_t with a_t = exp2(m_t - m*),
+// made exactly non-decreasing; al[t] receives a_t.  Returns m*.  Lane l owns
+// splits l*ch .. l*ch+ch-1 (ch <= kMaxSplits / 64).
+template <bool COHERENT>
+__device__ __forceinline__ float head_offsets_wave(const float2 *st, int Tb, int lane, float *off,
+                                                   float *al) {
   constexpr int CHM = kMaxSplits / 64;
   const int ch = (Tb + 63) >> 6;
   const int t0 = lane * ch;
   float2 sv[CHM];
 #pragma unroll
   for (int i = 0; i < CHM; ++i)
-    sv[i] = (i < ch && t0 + i < Tb) ? ld_coherent(st + t0 + i) : make_float2(-kInf, 0.0f);
+    sv[i] = (i < ch && t0 + i < Tb) ? ld2<COHERENT>(st + t0 + i) : make_float2(-kInf, 0.0f);
   float m = -kInf;
 #pragma unroll
   for (int i = 0; i < CHM; ++i) m = fmaxf(m, sv[i].x);
@@ -153,75 +207,128 @@ __device__ __forceinline__ float row_offsets_wave(const float2 *st, int Tb, int 
 #pragma unroll
   for (int i = 0; i < CHM; ++i) {
     run = fmaf(a[i], sv[i].y, run);
-    if (i < ch && t0 + i < Tb) off[t0 + i + 1] = fmaxf(run, floor_v);
+    if (i < ch && t0 + i < Tb) {
+      off[t0 + i + 1] = fmaxf(run, floor_v);
+      al[t0 + i] = a[i];
+    }
   }
   if (lane == 0) off[0] = 0.0f;
   return m;
 }
 
-// This workgroup's slice of the row's G*128 outputs after the partials of all
-// Tb splits are published: out[o] = scale_h * sum_t w_t * part[t][o] with
-// h = o / 128.  Thread (group g, output o) sums splits t = g, g + ng, ... in
-// order; groups are then summed in order.  w == nullptr means weight 1 and
-// scale_h = `scale`; otherwise w is [G][T] in LDS and scale_h = 1 / den[h].
+// out_h = scale * sum_t w_t part[t][h*128 + o] (w_t = 1 if w is null), divided
+// by *den if den is not null.  Two interleaved halves of the splits, each
+// summed in split order with 16 loads in flight, then added.  scratch holds
+// kThreads floats.
 template <typename E, int G>
-__device__ __forceinline__ void merge_slice(const float *part_row, int T, int Tb, int t,
-                                            const float *w, const float *den, float scale,
-                                            float *red, E *out_rows) {
-  constexpr int NOUT = G * kHeadDim;
-  const int tid = threadIdx.x;
-  const int sl = (NOUT + Tb - 1) / Tb;
-  const int o0 = t * sl, o1 = min(NOUT, o0 + sl);
-  if (o0 >= o1) return;  // uniform for the workgroup
-  const int n = o1 - o0;
-  for (int ob = 0; ob < n; ob += kThreads) {
-    const int m = min(kThreads, n - ob);
-    int mp = 1;
-    while (mp < m) mp <<= 1;
-    const int ng = kThreads / mp;
-    const int ol = tid % mp, g = tid / mp;
-    float acc = 0.0f;
-    if (ol < m) {
-      const int o = o0 + ob + ol, h = o / kHeadDim;
-      for (int tt = g; tt < Tb; tt += ng) {
-        const float v = ld_coherent(part_row + (int64_t)tt * NOUT + o);
-        acc = w ? fmaf(w[h * T + tt], v, acc) : acc + v;
-      }
+__device__ __forceinline__ void merge_head(const float *part_row, int h, int Tb, const float *w,
+                                           const float *den, float scale, float *scratch,
+                                           E *out_row) {
+  const int tid = threadIdx.x, o = tid & (kHeadDim - 1), g = tid >> 7;
+  const float *ph = part_row + h * kHeadDim + o;
+  const int nk = (Tb - g + 1) >> 1;  // splits g, g + 2, ...
+  float s = 0.0f;
+  for (int k0 = 0; k0 < nk; k0 += 16) {
+    float v[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int tt = g + 2 * (k0 + i);
+      v[i] = k0 + i < nk ? ld_coherent(ph + (int64_t)tt * G * kHeadDim) : 0.0f;
     }
-    red[tid] = acc;
-    __syncthreads();
-    // pairwise tree over the ng groups (fixed order)
-    for (int half = ng >> 1; half > 0; half >>= 1) {
-      if (g < half) red[tid] += red[tid + half * mp];
-      __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int tt = g + 2 * (k0 + i);
+      if (k0 + i < nk) s = w ? fmaf(w[tt], v[i], s) : s + v[i];
     }
-    if (tid < m) {
-      const int o = o0 + ob + tid, h = o / kHeadDim;
-      store_out(out_rows + o, red[tid] * (w ? 1.0f / den[h] : scale));
-    }
-    __syncthreads();
   }
+  scratch[tid] = s;
+  __syncthreads();
+  if (tid < kHeadDim) {
+    const float r = (scratch[tid] + scratch[tid + kHeadDim]) * scale;
+    store_out(out_row + tid, den ? r / *den : r);
+  }
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------------------
+// Small-batch sampled step
+// ---------------------------------------------------------------------------
+// Threshold r of head h is claimed iff lo <= tau_r < hi.  tau_r is
+// non-decreasing in r (fp32 rounding is monotone), so the claimed r form the
+// range [#{r : tau_r < lo}, #{r : tau_r < hi}); threads 2h and 2h+1 count the
+// two ends by binary search.
+template <int G, bool STRAT>
+__device__ __forceinline__ void claim_ranges(const HeadClaim *hc, const float *us, int64_t ustride,
+                                             int S, float invS, int *rng /* [G][2] */) {
+  const int tid = threadIdx.x;
+  if (tid < 2 * G) {
+    const int h = tid >> 1;
+    const HeadClaim c = hc[h];
+    const float bound = (tid & 1) ? c.hi : c.lo;
+    const float *uh = us + h * ustride;
+    int pos = 0;
+    for (int step = 1 << (31 - __clz(S)); step > 0; step >>= 1) {
+      const int np = pos + step;
+      if (np <= S && threshold(np - 1, STRAT ? uh[np - 1] : uh[0], invS, c.Z) < bound) pos = np;
+    }
+    rng[tid] = pos;
+  }
+  __syncthreads();
+}
+
+// Inverse CDF of the claimed thresholds of every head (LDS CDF P of the
+// split): key #{j : a P_j <= tau - lo}, clamped to the split.  Counts per key
+// go to cnt (LDS), indices to idx_out.  Returns (block-uniform) whether the
+// split holds any sample.
+template <int G, bool STRAT>
+__device__ __forceinline__ bool claim_keys(const HeadClaim *hc, const int *rng, const float *us,
+                                           int64_t ustride, int S, float invS, const float *P,
+                                           int pitch, int start, int nrows, int64_t row0, int *cnt,
+                                           int32_t *__restrict__ idx_out) {
+  const int tid = threadIdx.x;
+  int first[G + 1];
+  first[0] = 0;
+#pragma unroll
+  for (int h = 0; h < G; ++h) first[h + 1] = first[h] + max(0, rng[2 * h + 1] - rng[2 * h]);
+  const int total = first[G];
+  const int step0 = 1 << (31 - __clz(nrows));
+  for (int i = tid; i < total; i += kThreads) {
+    int h = 0;
+#pragma unroll
+    for (int k = 1; k < G; ++k) h += (i >= first[k]) ? 1 : 0;
+    const int r = rng[2 * h] + (i - first[h]);
+    const HeadClaim c = hc[h];
+    const float tau = threshold(r, STRAT ? us[h * ustride + r] : us[h * ustride], invS, c.Z);
+    const float x = tau - c.lo;
+    const float *Ph = P + h * pitch;
+    int pos = 0;
+    for (int step = step0; step > 0; step >>= 1) {
+      const int np = pos + step;
+      pos = (np <= nrows && c.a * Ph[np - 1] <= x) ? np : pos;
+    }
+    const int j = pos < nrows ? pos : nrows - 1;
+    atomicAdd(&cnt[h * pitch + j], 1);
+    if (idx_out) idx_out[(row0 + h) * S + r] = start + j;
+  }
+  return total > 0;
 }
 
 template <typename E, int G, bool PAGED, bool STRAT>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(G <= 4 ? 4 : 2))) void k_fused_sampled(FusedArgs a) {
-  // dynamic LDS: P [G][pitch] split CDF (reused as reduction buffer), cnt
-  // [G][pitch] sample counts, then the compaction list, which is also the
-  // offsets table [G][T+1] before the claims and the split flags [T] in the
-  // merge, then (stratified, if staged) the group's uniforms [G][S].
   extern __shared__ float dyn[];
-  const int pitch = a.Lsmax;
+  const int pitch = a.Lsmax, T = a.T;
   float *P = dyn;
-  int *cnt = reinterpret_cast<int *>(dyn + fused_p_floats(G, a.Lsmax));
+  int *cnt = reinterpret_cast<int *>(dyn + fused_p_floats(G, pitch, T));
   int *list = cnt + G * pitch;
-  float *offl = reinterpret_cast<float *>(list);
-  float *ul = reinterpret_cast<float *>(list + (pitch > G * (a.T + 1) ? pitch : G * (a.T + 1)));
+  float *offl = reinterpret_cast<float *>(list);  // [G][T+1], then al [G][T]
+  float *all = offl + G * (T + 1);
+  float *ul = reinterpret_cast<float *>(list + fused_list_ints(G, pitch, T));
   __shared__ HeadClaim hc[G];
   __shared__ float mh[G], mtmp[4 * G];
-  __shared__ int wave_cnt[4];
+  __shared__ int wave_cnt[4], rank_lds, rng[2 * G];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int nrk = a.B * a.Hkv, T = a.T;
+  const int nrk = a.B * a.Hkv;
   const int R = gridDim.x / T;
   int rho, t;
   map_item(blockIdx.x, T, R, a.xcd, rho, t);
@@ -251,13 +358,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(G <= 4
 
     // uniforms of the group (read while the keys stream)
     const float *us = STRAT ? a.u + row0 * a.S : a.u + row0;
-    int64_t ustride = STRAT ? a.S : 1;
+    const int64_t ustride = STRAT ? a.S : 1;
     if (STRAT && a.ustage) {
       for (int i = tid; i < G * a.S; i += kThreads) ul[i] = us[i];
       us = ul;
     }
 
-    // 1. scores and split-local CDF
+    // 1. scores and split-local CDF; publish (m_t, l_t)
     const QRegs<E, G> qr = load_q<E, G>(static_cast<const E *>(a.q), b, a.Hq, kvh, tid & 15);
     float mx[G];
     score_tile<E, G, PAGED, kScoreUnroll>(a.kv, b, kvh, start, nrows, qr, a.scale_log2, P, pitch, mx);
@@ -269,20 +376,20 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(G <= 4
     for (int i = tid; i < G * pitch; i += kThreads) cnt[i] = 0;
 
     // 2. every split of the row has published its statistics
-    row_sync(sync, base + (unsigned long long)Tb, a.err);
-    if (t == 0 && tid == 0)
-      __hip_atomic_store(sync + 1, base + 2ull * Tb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    row_arrive(sync, base, &rank_lds);
+    row_wait(sync, base + (unsigned long long)Tb, a.err);
 
-    // 3. global offsets (one wave per head), claims, inverse CDF, gather
+    // 3. offsets, claimed ranges, inverse CDF, union gather, partial sums
     for (int h = wave; h < G; h += kThreads / 64) {
-      float *oh = offl + h * (T + 1);
-      const float mstar = row_offsets_wave(a.stats + (row0 + h) * T, Tb, lane, oh);
-      if (lane == 0)
-        hc[h] = HeadClaim{oh[t], t == Tb - 1 ? kInf : oh[t + 1], oh[Tb], fast_exp2(mh[h] - mstar)};
+      float *oh = offl + h * (T + 1), *ah = all + h * T;
+      head_offsets_wave<true>(a.stats + (row0 + h) * T, Tb, lane, oh, ah);
+      if (lane == 0) hc[h] = HeadClaim{oh[t], t == Tb - 1 ? kInf : oh[t + 1], oh[Tb], ah[t]};
     }
     __syncthreads();
-    const bool has = claim_search<G, STRAT>(start, nrows, row0, a.S, a.invS, us, ustride, hc, P,
-                                            pitch, cnt, a.idx_out);
+    claim_ranges<G, STRAT>(hc, us, ustride, a.S, a.invS, rng);
+    const bool has = claim_keys<G, STRAT>(hc, rng, us, ustride, a.S, a.invS, P, pitch, start, nrows,
+                                          row0, cnt, a.idx_out);
+    __syncthreads();  // counts complete; offl/all are no longer needed
     if (has) {
       gather_union<E, G, PAGED, true>(a.kv, b, kvh, start, nrows, P, pitch, cnt, list, wave_cnt,
                                       part_row + (int64_t)t * G * kHeadDim);
@@ -291,22 +398,33 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(G <= 4
       for (int o2 = tid; o2 < G * kHeadDim / 2; o2 += kThreads) st_coherent(pz + o2, make_float2(0.f, 0.f));
     }
 
-    // 4. every split has published its partial sums; merge this split's slice
-    row_sync(sync, base + 2ull * Tb, a.err);
-    merge_slice<E, G>(part_row, T, Tb, t, nullptr, nullptr, a.invS, P, out + row0 * kHeadDim);
-    __syncthreads();
+    // 4. arrive; the last min(G, Tb) arrivals merge one or more heads each
+    const int W = min(G, Tb);
+    const int rank = row_arrive(sync, base + (unsigned long long)Tb, &rank_lds);
+    if (rank < Tb - W) continue;
+    if (rank == Tb - 1) {
+      if (tid == 0)
+        __hip_atomic_store(sync + 1, base + 2ull * Tb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    } else {
+      row_wait(sync, base + 2ull * Tb, a.err);
+    }
+    for (int h = rank - (Tb - W); h < G; h += W)
+      merge_head<E, G>(part_row, h, Tb, nullptr, nullptr, a.invS, P, out + (row0 + h) * kHeadDim);
   }
 }
 
+// ---------------------------------------------------------------------------
+// Dense step
+// ---------------------------------------------------------------------------
 template <typename E, int G, bool PAGED>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(G <= 4 ? 4 : 2))) void k_fused_dense(FusedArgs a) {
-  // dynamic LDS: s [G][pitch] scores / weights, red [fused_red_floats(G)], al [G][T]
+  // dynamic LDS: s [G][pitch] scores / weights, red [4][G*128] (also the merge scratch)
   extern __shared__ float dyn[];
   const int pitch = a.Lsmax;
   float *s = dyn;
   float *red = s + G * pitch;
-  float *al = red + fused_red_floats(G);
-  __shared__ float mh[G], lh[G], den[G], mtmp[4 * G];
+  __shared__ float mh[G], lh[G], mtmp[4 * G], den;
+  __shared__ int rank_lds;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, slot = tid >> 4, c = tid & 15;
   const int nrk = a.B * a.Hkv, T = a.T;
@@ -392,30 +510,240 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(G <= 4
     }
     if (tid < G) st_coherent(a.stats + (row0 + tid) * T + t, make_float2(mh[tid], lh[tid]));
 
-    // all splits of the row have published (m_t, l_t, o_t)
-    row_sync(sync, base + (unsigned long long)Tb, a.err);
-    if (t == 0 && tid == 0)
-      __hip_atomic_store(sync + 1, base + (unsigned long long)Tb, __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
-    // rescale factors a_t = exp2(m_t - m*) and denominators sum_t a_t l_t
-    for (int h = wave; h < G; h += kThreads / 64) {
-      const float2 *st = a.stats + (row0 + h) * T;
-      float m = -kInf;
-      for (int tt = lane; tt < Tb; tt += 64) m = fmaxf(m, ld_coherent(st + tt).x);
-      m = wave_max(m);
-      float d = 0.0f;
-      for (int tt = lane; tt < Tb; tt += 64) {
-        const float2 v = ld_coherent(st + tt);
-        const float aa = fast_exp2(v.x - m);
-        al[h * T + tt] = aa;
-        d = fmaf(aa, v.y, d);
+    // arrive; the last min(G, Tb) arrivals merge one or more heads each
+    const int W = min(G, Tb);
+    const int rank = row_arrive(sync, base, &rank_lds);
+    if (rank < Tb - W) continue;
+    if (rank == Tb - 1) {
+      if (tid == 0)
+        __hip_atomic_store(sync + 1, base + (unsigned long long)Tb, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+    } else {
+      row_wait(sync, base + (unsigned long long)Tb, a.err);
+    }
+    for (int h = rank - (Tb - W); h < G; h += W) {
+      // a_t = exp2(m_t - m*) and the denominator sum_t a_t l_t
+      float *al = red + kThreads;
+      if (wave == 0) {
+        const float2 *st = a.stats + (row0 + h) * T;
+        float m = -kInf;
+        for (int tt = lane; tt < Tb; tt += 64) m = fmaxf(m, ld_coherent(st + tt).x);
+        m = wave_max(m);
+        float d = 0.0f;
+        for (int tt = lane; tt < Tb; tt += 64) {
+          const float2 v = ld_coherent(st + tt);
+          const float aa = fast_exp2(v.x - m);
+          al[tt] = aa;
+          d = fmaf(aa, v.y, d);
+        }
+        d = wave_sum(d);
+        if (lane == 0) den = d;
       }
-      d = wave_sum(d);
-      if (lane == 0) den[h] = d;
+      __syncthreads();
+      merge_head<E, G>(part_row, h, Tb, al, &den, 1.0f, red, out + (row0 + h) * kHeadDim);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Large-batch sampled step: two launches
+// ---------------------------------------------------------------------------
+// One work item per workgroup, items row-major; the hardware dispatcher
+// balances them.  Writes the stash, the block ends and the statistics.
+template <typename E, int G, bool PAGED>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(G <= 4 ? 4 : 2))) void k_stream_cdf(FusedArgs a) {
+  extern __shared__ float dyn[];
+  const int pitch = a.Lsmax, T = a.T;
+  float *P = dyn;
+  __shared__ float mh[G], mtmp[4 * G];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int rowkv = blockIdx.x / T, t = blockIdx.x % T;
+  const int b = rowkv / a.Hkv, kvh = rowkv % a.Hkv;
+  const int64_t row0 = (int64_t)b * a.Hq + kvh * G;
+  const int L = seq_len(a.kv, b);
+  int Ls, Tb;
+  split_geometry(L, T, Ls, Tb);
+  if (t >= Tb) return;
+  const int start = t * Ls, nrows = min(Ls, L - start);
+
+  const QRegs<E, G> qr = load_q<E, G>(static_cast<const E *>(a.q), b, a.Hq, kvh, tid & 15);
+  float mx[G];
+  score_tile<E, G, PAGED, kScoreUnroll>(a.kv, b, kvh, start, nrows, qr, a.scale_log2, P, pitch, mx);
+  block_max_heads<G>(mx, mtmp, mh);
+  for (int h = wave; h < G; h += kThreads / 64) wave_split_cdf_m(P + h * pitch, nrows, lane, mh[h]);
+  __syncthreads();
+  if (tid < G) a.stats[(row0 + tid) * T + t] = make_float2(mh[tid], P[tid * pitch + nrows - 1]);
+  // stash, in pairs of keys; an odd last split also writes the (unused) slot at L
+  const int half = (nrows + 1) >> 1;
+  for (int i = tid; i < G * half; i += kThreads) {
+    const int h = i / half, j = 2 * (i - h * half);
+    const float *ph = P + h * pitch;
+    *reinterpret_cast<float2 *>(a.stash + (row0 + h) * a.npitch + start + j) =
+        make_float2(ph[j], j + 1 < nrows ? ph[j + 1] : ph[j]);
+  }
+  // block ends, in pairs (start / 32 is even); an odd last count also writes
+  // the (unused) slot after the row's last block
+  const int ncoarse = (int)(a.npitch / kBlock);
+  const int nbh = ((nrows + kBlock - 1) / kBlock + 1) >> 1;
+  for (int i = tid; i < G * nbh; i += kThreads) {
+    const int h = i / nbh, k = 2 * (i - h * nbh);
+    const float *ph = P + h * pitch;
+    *reinterpret_cast<float2 *>(a.coarse + (row0 + h) * ncoarse + start / kBlock + k) =
+        make_float2(ph[min(k * kBlock + kBlock - 1, nrows - 1)],
+                    ph[min(k * kBlock + 2 * kBlock - 1, nrows - 1)]);
+  }
+}
+
+// Inverse CDF of one threshold (global units) for one query head: split
+// t = #{t' in [1,Tb) : off[t'] <= tau}; inside it the key #{j : al_t P_j <=
+// tau - off[t]} over the split's CDF, clamped to the split.  Two levels: the
+// number of whole 32-key blocks below the threshold, from the block-end values
+// cl[] in LDS, then the count inside the next block, from the stash row Pst.
+// Both are exact counts over a non-decreasing sequence, so they add up to the
+// plain count.  Returns the logical key position.
+__device__ __forceinline__ int invert_threshold(const float *Pst, const float *cl, const float *off,
+                                                const float *al, int Tb, int Ls, int L, float tau) {
+  int t = 0;
+  for (int step = 1 << (31 - __clz(Tb)); step > 0; step >>= 1) {
+    const int nt = t + step;
+    t = (nt < Tb && off[nt] <= tau) ? nt : t;
+  }
+  const float x = tau - off[t], a = al[t];
+  const int st = t * Ls, nr = min(Ls, L - st);
+  const int nb = (nr + kBlock - 1) / kBlock;
+  const float *ce = cl + st / kBlock;
+  int kb = 0;
+#pragma unroll
+  for (int step = kSplitMax / kBlock / 2; step > 0; step >>= 1) {
+    const int nk = kb + step;
+    kb = (nk <= nb && a * ce[nk - 1] <= x) ? nk : kb;
+  }
+  int pos;
+  if (kb >= nb) {
+    pos = nr;
+  } else {
+    const int j0 = kb * kBlock, nin = min(kBlock, nr - j0);
+    const float4 *Pb = reinterpret_cast<const float4 *>(Pst + st + j0);
+    float4 v[kBlock / 4];
+#pragma unroll
+    for (int i = 0; i < kBlock / 4; ++i) v[i] = Pb[i];
+    int c = 0;
+#pragma unroll
+    for (int i = 0; i < kBlock / 4; ++i) {
+      c += (4 * i < nin && a * v[i].x <= x) ? 1 : 0;
+      c += (4 * i + 1 < nin && a * v[i].y <= x) ? 1 : 0;
+      c += (4 * i + 2 < nin && a * v[i].z <= x) ? 1 : 0;
+      c += (4 * i + 3 < nin && a * v[i].w <= x) ? 1 : 0;
+    }
+    pos = j0 + c;
+  }
+  return st + min(pos, nr - 1);
+}
+
+// One workgroup per query head.  Thresholds are taken kThreads at a time; the
+// chosen keys of a chunk are non-decreasing, so equal keys form runs, and each
+// run's V row is read once and added with its length: O = (1/S) sum_r
+// V_{idx_r} (Sec. 2, the stochastic add-only attention).
+template <typename E, bool PAGED, bool STRAT>
+__global__ __launch_bounds__(kThreads) void k_value_heads(FusedArgs a, int G) {
+  extern __shared__ float dyn[];
+  __shared__ int wave_cnt[4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, slot = tid >> 4, c = tid & 15;
+  const int64_t rowq = blockIdx.x;
+  const int b = (int)(rowq / a.Hq), kvh = (int)(rowq % a.Hq) / G;
+  E *out = static_cast<E *>(a.out) + rowq * kHeadDim;
+  const int L = seq_len(a.kv, b);
+  if (L <= 0) {
+    if (tid < kHeadDim) store_out(out + tid, 0.0f);
+    if (a.idx_out)
+      for (int r = tid; r < a.S; r += kThreads) a.idx_out[rowq * a.S + r] = -1;
+    return;
+  }
+  int Ls, Tb;
+  split_geometry(L, a.T, Ls, Tb);
+  const int ncoarse = (int)(a.npitch / kBlock);
+  float *cl = dyn;                   // [ncoarse]
+  float *off = cl + ncoarse;         // [T+1]
+  float *al = off + (a.T + 1);       // [T]
+  int *keys = reinterpret_cast<int *>(al + a.T);            // [kThreads]
+  int *runs = keys + kThreads;                               // [kThreads]
+  float *red = reinterpret_cast<float *>(runs + kThreads);  // [4][128]
+  {
+    // the head's block ends, in pairs (ncoarse is even)
+    const float2 *src = reinterpret_cast<const float2 *>(a.coarse + rowq * ncoarse);
+    const int nc2 = ((L + kBlock - 1) / kBlock + 1) >> 1;
+    for (int i = tid; i < nc2; i += kThreads) reinterpret_cast<float2 *>(cl)[i] = src[i];
+  }
+  if (wave == 0) head_offsets_wave<false>(a.stats + rowq * a.T, Tb, lane, off, al);
+  __syncthreads();
+  const float Z = off[Tb];
+  const float *Pst = a.stash + rowq * a.npitch;
+  const E *V = static_cast<const E *>(a.kv.v);
+
+  float acc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = 0.0f;
+  const float u0 = STRAT ? 0.0f : a.u[rowq];
+  for (int r0 = 0; r0 < a.S; r0 += kThreads) {
+    const int n = min(kThreads, a.S - r0);
+    const int r = r0 + tid;
+    int key = 0;
+    if (tid < n) {
+      const float ur = STRAT ? a.u[rowq * a.S + r] : u0;
+      key = invert_threshold(Pst, cl, off, al, Tb, Ls, L, threshold(r, ur, a.invS, Z));
+      keys[tid] = key;
+      if (a.idx_out) a.idx_out[rowq * a.S + r] = key;
     }
     __syncthreads();
-    merge_slice<E, G>(part_row, T, Tb, t, al, den, 1.0f, red, out + row0 * kHeadDim);
+    // run starts in threshold order (ballot per wave, waves in order)
+    const bool start = tid < n && (tid == 0 || keys[tid - 1] != key);
+    const unsigned long long mask = __ballot(start);
+    if (lane == 0) wave_cnt[wave] = __popcll(mask);
     __syncthreads();
+    int before = 0;
+    for (int w = 0; w < wave; ++w) before += wave_cnt[w];
+    const int nruns = wave_cnt[0] + wave_cnt[1] + wave_cnt[2] + wave_cnt[3];
+    if (start) runs[before + __popcll(mask & ((1ull << lane) - 1))] = tid;
+    __syncthreads();
+    // gather: 16 row slots, U rows in flight per slot
+    constexpr int U = kGatherUnroll;
+    for (int g0 = 0; g0 < nruns; g0 += 16 * U) {
+      Chunk<E> ch[U];
+      float w[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int i = g0 + u * 16 + slot;
+        if (i < nruns) {
+          const int j = runs[i];
+          const int len = (i + 1 < nruns ? runs[i + 1] : n) - j;
+          ch[u] = Chunk<E>::load(V + row_offset<PAGED>(a.kv, b, kvh, keys[j]) + c * 8);
+          w[u] = (float)len;
+        } else {
+          ch[u] = Chunk<E>::zero();
+          w[u] = 0.0f;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        float f[8];
+        ch[u].to_float(f);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i] = fmaf(w[u], f[i], acc[i]);
+      }
+    }
+    __syncthreads();  // keys / runs are rewritten by the next chunk
+  }
+  // sum the 16 slots (4 per wave, then the 4 waves in order), scale, store
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = xor32_sum(xor16_sum(acc[i]));
+  if (lane < 16) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) red[wave * kHeadDim + c * 8 + i] = acc[i];
+  }
+  __syncthreads();
+  if (tid < kHeadDim) {
+    const float s = ((red[tid] + red[kHeadDim + tid]) + red[2 * kHeadDim + tid]) + red[3 * kHeadDim + tid];
+    store_out(out + tid, s * a.invS);
   }
 }
 
@@ -454,7 +782,8 @@ int capacity_of(const void *fn, size_t lds) {
 }
 
 // Launch R*T workgroups with R whole rows per round, R limited so that every
-// workgroup of the grid is resident at once (the per-row barrier needs it).
+// workgroup of the grid is resident at once: a waiting split only waits for
+// splits of its own row, which the same round holds.
 hipError_t launch_resident(const void *fn, const Plan &p, FusedArgs &args, size_t lds,
                            hipStream_t st) {
   const int nrk = p.B * p.Hkv;
@@ -462,7 +791,9 @@ hipError_t launch_resident(const void *fn, const Plan &p, FusedArgs &args, size_
   if (cap < p.T) return hipErrorInvalidConfiguration;
   const int R = std::min(nrk, cap / p.T);
   void *params[] = {&args};
-  return hipLaunchKernel(fn, dim3(R * p.T), dim3(kThreads), params, lds, st);
+  const CallTimer tm = call_timer();
+  return hipExtLaunchKernel(fn, dim3(R * p.T), dim3(kThreads), params, lds, st, tm.start, tm.stop,
+                            0);
 }
 
 FusedArgs make_args(const Plan &p, const KvView &kv, const void *q, void *out, float scale_log2,
@@ -472,9 +803,10 @@ FusedArgs make_args(const Plan &p, const KvView &kv, const void *q, void *out, f
   a.q = q;
   a.out = out;
   a.stats = reinterpret_cast<float2 *>(ws + p.off_stats);
-  a.part = reinterpret_cast<float *>(ws + p.off_part);
-  a.flags = reinterpret_cast<int *>(ws + p.off_flag);
-  a.sync = reinterpret_cast<unsigned long long *>(ws + p.off_sync);
+  a.part = p.off_part ? reinterpret_cast<float *>(ws + p.off_part) : nullptr;
+  a.stash = p.off_stash ? reinterpret_cast<float *>(ws + p.off_stash) : nullptr;
+  a.coarse = p.off_coarse ? reinterpret_cast<float *>(ws + p.off_coarse) : nullptr;
+  a.sync = p.off_sync ? reinterpret_cast<unsigned long long *>(ws + p.off_sync) : nullptr;
   a.err = reinterpret_cast<int *>(ws + p.off_err);
   a.B = p.B;
   a.Hq = p.Hq;
@@ -482,6 +814,7 @@ FusedArgs make_args(const Plan &p, const KvView &kv, const void *q, void *out, f
   a.T = p.T;
   a.S = p.S;
   a.Lsmax = p.Ls;
+  a.npitch = p.npitch;
   a.invS = p.S ? 1.0f / (float)p.S : 0.0f;
   a.scale_log2 = scale_log2;
   a.xcd = p.xcd;
@@ -497,7 +830,7 @@ hipError_t launch_fused_dense(const Plan &p, const KvView &kv, const void *q, fl
     using E = std::remove_pointer_t<decltype(eptr)>;
     constexpr int G = decltype(gc)::value;
     constexpr bool PG = decltype(paged)::value;
-    const size_t lds = ((size_t)G * p.Ls + fused_red_floats(G) + (size_t)G * p.T) * 4;
+    const size_t lds = (size_t)fused_dense_floats(G, p.Ls, p.T) * 4;
     return launch_resident(reinterpret_cast<const void *>(&k_fused_dense<E, G, PG>), p, args, lds,
                            st);
   });
@@ -513,13 +846,27 @@ hipError_t launch_fused_sampled(const Plan &p, const KvView &kv, const void *q, 
     using E = std::remove_pointer_t<decltype(eptr)>;
     constexpr int G = decltype(gc)::value;
     constexpr bool PG = decltype(paged)::value;
+    if (p.split2) {
+      const CallTimer tm = call_timer();
+      void *params[] = {&args};
+      const size_t lds1 = (size_t)G * p.Ls * 4;
+      hipError_t e = hipExtLaunchKernel(reinterpret_cast<const void *>(&k_stream_cdf<E, G, PG>),
+                                        dim3(p.B * p.Hkv * p.T), dim3(kThreads), params, lds1, st,
+                                        tm.start, nullptr, 0);
+      if (e != hipSuccess) return e;
+      int g = G;
+      void *params2[] = {&args, &g};
+      const size_t lds2 = (size_t)value_heads_floats(p.T, (int)(p.npitch / kBlock)) * 4;
+      const void *fn2 = strat ? reinterpret_cast<const void *>(&k_value_heads<E, PG, true>)
+                              : reinterpret_cast<const void *>(&k_value_heads<E, PG, false>);
+      return hipExtLaunchKernel(fn2, dim3(p.B * p.Hq), dim3(kThreads), params2, lds2, st, nullptr,
+                                tm.stop, 0);
+    }
     const void *fn = strat ? reinterpret_cast<const void *>(&k_fused_sampled<E, G, PG, true>)
                            : reinterpret_cast<const void *>(&k_fused_sampled<E, G, PG, false>);
     // stage the group's stratified uniforms in LDS when they are small
     args.ustage = strat && (size_t)G * p.S <= 4096;
-    const size_t lds = ((size_t)fused_p_floats(G, p.Ls) + (size_t)G * p.Ls +
-                        std::max<size_t>((size_t)p.Ls, (size_t)G * (p.T + 1)) +
-                        (args.ustage ? (size_t)G * p.S : 0)) * 4;
+    const size_t lds = (size_t)fused_sampled_floats(G, p.Ls, p.T, args.ustage ? G * p.S : 0) * 4;
     return launch_resident(fn, p, args, lds, st);
   });
 }

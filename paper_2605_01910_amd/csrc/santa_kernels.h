@@ -9,6 +9,16 @@
 
 namespace santa {
 
+// Events the GPU records around the kernels of one call (santa_time_next_call):
+// `start` when the call's first kernel is dispatched, `stop` when its last
+// kernel completes.  Null events launch normally.  Thread-local, consumed by
+// the next santa_decode_* call on the thread.
+struct CallTimer {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
+CallTimer &call_timer();
+
 hipError_t launch_dense(const Plan &p, const KvView &kv, const void *q, float scale_log2,
                         void *out, char *ws, hipStream_t st);
 

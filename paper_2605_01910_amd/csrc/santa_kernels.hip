@@ -17,6 +17,7 @@
 // Scores are kept in log2 units (s * scale * log2 e) so exponentials are one
 // v_exp_f32 each.  Every reduction has a fixed order, so repeated calls on the
 // same inputs give bitwise-identical outputs.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include "santa_kernels.h"
@@ -450,10 +451,13 @@ hipError_t launch_dense(const Plan &p, const KvView &kv, const void *q, float sc
     using E = std::remove_pointer_t<decltype(eptr)>;
     constexpr int G = decltype(gc)::value;
     constexpr bool PG = decltype(paged)::value;
-    k_dense_split<E, G, PG><<<grid, kThreads, 0, st>>>(kv, static_cast<const E *>(q), p.Hq, p.Ls,
-                                                        p.T, scale_log2, stats, part);
-    k_merge_dense<E, G><<<p.B * p.Hq, kHeadDim, 0, st>>>(kv, p.Hq, p.Hkv, p.Ls, p.T, stats, part,
-                                                         static_cast<E *>(out));
+    const CallTimer tm = call_timer();
+    hipExtLaunchKernelGGL(k_dense_split<E, G, PG>, grid, dim3(kThreads), 0, st, tm.start, nullptr,
+                          0, kv, static_cast<const E *>(q), p.Hq, p.Ls, p.T, scale_log2, stats,
+                          part);
+    hipExtLaunchKernelGGL(k_merge_dense<E, G>, dim3(p.B * p.Hq), dim3(kHeadDim), 0, st, nullptr,
+                          tm.stop, 0, kv, p.Hq, p.Hkv, p.Ls, p.T, stats, part,
+                          static_cast<E *>(out));
     return hipGetLastError();
   });
 }
@@ -477,9 +481,9 @@ static hipError_t launch_value_stage(const Plan &p, const KvView &kv, bool strat
   else
     k_sample<E, G, PG, false><<<grid, kThreads, 0, st>>>(kv, p.Hq, p.Ls, p.T, p.S, invS, u, stash,
                                                          offs, alpha, rowst, flags, part, idx_out);
-  k_merge_sampled<E, G><<<p.B * p.Hq, kHeadDim, 0, st>>>(kv, p.Hq, p.Hkv, p.Ls, p.T, p.S, invS,
-                                                         flags, part, static_cast<E *>(out),
-                                                         idx_out);
+  hipExtLaunchKernelGGL(k_merge_sampled<E, G>, dim3(p.B * p.Hq), dim3(kHeadDim), 0, st, nullptr,
+                        call_timer().stop, 0, kv, p.Hq, p.Hkv, p.Ls, p.T, p.S, invS, flags, part,
+                        static_cast<E *>(out), idx_out);
   return hipGetLastError();
 }
 
@@ -493,8 +497,9 @@ hipError_t launch_sampled(const Plan &p, const KvView &kv, const void *q, float 
     using E = std::remove_pointer_t<decltype(eptr)>;
     constexpr int G = decltype(gc)::value;
     constexpr bool PG = decltype(paged)::value;
-    k_score_cdf<E, G, PG><<<grid, kThreads, 0, st>>>(kv, static_cast<const E *>(q), p.Hq, p.Ls,
-                                                      p.T, scale_log2, stats, stash);
+    hipExtLaunchKernelGGL(k_score_cdf<E, G, PG>, grid, dim3(kThreads), 0, st, call_timer().start,
+                          nullptr, 0, kv, static_cast<const E *>(q), p.Hq, p.Ls, p.T, scale_log2,
+                          stats, stash);
     return launch_value_stage<E, G, PG>(p, kv, strat, u, idx_out, out, ws, st);
   });
 }
@@ -512,8 +517,9 @@ hipError_t launch_bernoulli(const Plan &p, const KvView &kv, const KtView &kt, c
   return with_types(p, false, [&](auto eptr, auto gc, auto) -> hipError_t {
     using E = std::remove_pointer_t<decltype(eptr)>;
     constexpr int G = decltype(gc)::value;
-    k_bern_prep<E, G><<<p.B * p.Hkv, kHeadDim, 0, st>>>(static_cast<const E *>(q), p.Hq, p.Hkv,
-                                                        Bd, mode, u_q, bw, blist, bn, mask_out);
+    hipExtLaunchKernelGGL(k_bern_prep<E, G>, dim3(p.B * p.Hkv), dim3(kHeadDim), 0, st,
+                          call_timer().start, nullptr, 0, static_cast<const E *>(q), p.Hq, p.Hkv,
+                          Bd, mode, u_q, bw, blist, bn, mask_out);
     k_bern_score<E, G><<<grid, kThreads, 0, st>>>(kv, kt, p.Hq, p.Ls, p.T, scale_log2, bw, blist,
                                                   bn, stats, stash);
     return launch_value_stage<E, G, false>(p, kv, false, u, idx_out, out, ws, st);

@@ -21,15 +21,20 @@ constexpr int kSyncStride = 64; // ints per row of fused-path counters (256 B ap
 struct Plan {
   int B, Hq, Hkv, G, dtype;
   int n_k;      // max context length
-  int Ls;       // keys per split (multiple of 16, <= kSplitMax)
+  int Ls;       // keys per split (multi-kernel: multiple of 16; fused: longest split of
+                // any row, multiple of 64; <= kSplitMax)
   int T;        // splits per row for n_k keys
   int S;        // samples per row (0 for dense)
   int kind;     // santa_kind_t
   int fused;    // 1: single persistent launch (per-row split lengths), 0: multi-kernel
   int xcd;      // fused: place each row's splits on one XCD
+  int split2;   // fused sampled: 1 = two launches (stream + CDF stash, then one
+                // workgroup per query head), 0 = one persistent launch
+  int64_t npitch;  // two-launch sampled: stash floats per query head (n_k rounded up to 64)
   // workspace carve-up (byte offsets, 256-aligned)
   size_t off_stats;  // float2 [B*Hq*T]     per-split (max, sum) in log2 units
-  size_t off_stash;  // float  [B*Hq*T*Ls]  split-local CDF of each row
+  size_t off_stash;  // float  [B*Hq*T*Ls] (fused: [B*Hq*npitch]) split-local CDF of each row
+  size_t off_coarse; // float  [B*Hq*npitch/32] fused: CDF at every 32-key block end
   size_t off_offs;   // float  [B*Hq*(T+1)] global split offsets of the CDF
   size_t off_alpha;  // float  [B*Hq*T]     per-split rescale exp2(m_t - m*)
   size_t off_rowst;  // float2 [B*Hq]       (m*, Z) per row
@@ -38,8 +43,8 @@ struct Plan {
   size_t off_bw;     // float  [B*Hq*128]   Bernoulli query weights
   size_t off_blist;  // int    [B*Hkv*128]  Bernoulli feature list
   size_t off_bn;     // int    [B*Hkv]      Bernoulli feature count
-  size_t off_err;    // int    [1]          fused: barrier wait gave up
-  size_t off_sync;   // int    [B*Hkv*2]    fused: per-row arrival / completion counters
+  size_t off_err;    // int    [1]          fused: a wait gave up
+  size_t off_sync;   // u64    [B*Hkv*kSyncStride/2] fused: per-row arrival counter and base
   size_t total;
 };
 

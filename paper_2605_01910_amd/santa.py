@@ -25,7 +25,7 @@ SANTA_KIND_DENSE, SANTA_KIND_SYSTEMATIC, SANTA_KIND_STRATIFIED, SANTA_KIND_BERNO
 # every symbol include/santa.h declares
 EXPORTS = ("santa_workspace_size", "santa_workspace_init", "santa_decode_dense",
            "santa_decode_systematic", "santa_decode_stratified", "santa_decode_bernoulli_qk",
-           "santa_status_string", "santa_last_error")
+           "santa_time_next_call", "santa_status_string", "santa_last_error")
 
 
 class SantaError(RuntimeError):
@@ -76,11 +76,12 @@ def load() -> ctypes.CDLL:
     L.santa_decode_stratified.argtypes = [P, KP, SP, ctypes.c_float, I32, P, P, P, P, SZ, P]
     L.santa_decode_bernoulli_qk.argtypes = [P, TP, KP, SP, ctypes.c_float, I32, I32, P, I32, P,
                                             P, P, P, P, SZ, P]
+    L.santa_time_next_call.argtypes = [P, P]
     L.santa_status_string.argtypes = [ctypes.c_int]
     L.santa_status_string.restype = ctypes.c_char_p
     L.santa_last_error.restype = ctypes.c_char_p
     for name in ("santa_workspace_init", "santa_decode_dense", "santa_decode_systematic",
-                 "santa_decode_stratified", "santa_decode_bernoulli_qk"):
+                 "santa_decode_stratified", "santa_decode_bernoulli_qk", "santa_time_next_call"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -219,3 +220,18 @@ def santa_decode_bernoulli_qk(q: torch.Tensor, kt: santa_kt_t, kv: santa_kv_t,
                                             int(mode), _ptr(u_q), int(S), _ptr(u), _ptr(idx_out),
                                             _ptr(feat_mask_out), _ptr(out), _ptr(ws),
                                             ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def santa_time_next_call(start, stop) -> None:
+    """Attach two timing events to the kernels of the next santa_decode_* call on
+    this thread (start: first kernel dispatched, stop: last kernel done).
+    `start`/`stop` are torch.cuda.Event objects that have been recorded at least
+    once (so their HIP event exists), raw hipEvent_t handles, or both None."""
+    def handle(e):
+        if e is None:
+            return None
+        h = e.cuda_event if hasattr(e, "cuda_event") else int(e)
+        if not h:
+            raise ValueError("event has no HIP handle yet: record it once first")
+        return ctypes.c_void_p(h)
+    _check(load().santa_time_next_call(handle(start), handle(stop)))

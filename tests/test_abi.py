@@ -107,3 +107,12 @@ def test_status_strings():
     lib = S.load()
     assert lib.santa_status_string(0) == b"SANTA_OK"
     assert lib.santa_status_string(3) == b"SANTA_ERR_WORKSPACE"
+
+
+def test_time_next_call_needs_both_events_or_neither():
+    lib = S.load()
+    assert lib.santa_time_next_call(None, None) == S.SANTA_OK
+    st = lib.santa_time_next_call(ctypes.c_void_p(0x1000), None)
+    assert st == S.SANTA_ERR_INVALID_ARG
+    assert b"both" in lib.santa_last_error()
+    assert lib.santa_time_next_call(None, None) == S.SANTA_OK

@@ -171,3 +171,26 @@ def test_fused_barrier_flag_stays_clear():
         out, idx, _ = run(w, dw=dw, ws=ws)
     check_sampled(w, out, idx)
     assert int(ws[:4].view(torch.int32).item()) == 0
+
+
+@pytest.mark.parametrize("case", sorted(SAMPLED_CASES))
+def test_two_launch_sampled_parity(case, monkeypatch):
+    """The large-batch sampled path (stream + CDF stash launch, then one
+    workgroup per query head) on every sampled case."""
+    monkeypatch.setenv("SANTA_SAMPLED", "split")
+    cfg, kind, over = SAMPLED_CASES[case]
+    log(f"[two-launch/{kind}] {case} cfg={cfg} {over}")
+    w = make_workload(cfg, seed=23, kind=kind, **over)
+    out, idx, _ = run(w, kind)
+    log(f"  {check_sampled(w, out, idx, kind)}")
+
+
+@pytest.mark.parametrize("case", sorted(SAMPLED_CASES))
+def test_one_launch_sampled_parity(case, monkeypatch):
+    """The small-batch sampled path forced on every sampled case."""
+    monkeypatch.setenv("SANTA_SAMPLED", "fused")
+    cfg, kind, over = SAMPLED_CASES[case]
+    log(f"[one-launch/{kind}] {case} cfg={cfg} {over}")
+    w = make_workload(cfg, seed=24, kind=kind, **over)
+    out, idx, _ = run(w, kind)
+    log(f"  {check_sampled(w, out, idx, kind)}")
