@@ -7,10 +7,15 @@
 // Sampled step, small batches (one persistent launch, k_fused_sampled).  The
 // grid holds R whole rows per round (R*T workgroups, all resident) and loops
 // over rounds.  Per work item:
-//   1. stream the split's keys; scores of the G heads in LDS; split-local CDF
-//      P_j = sum_{i<=j} exp2(s_i - m_t) in LDS (Sec. 2.1: F is the running sum
-//      of the attention weights); publish (m_t, l_t = P_last);
-//   2. wait until every split of the row has published (row counter);
+//   1. stream the split's keys; scores of the G heads in LDS; each lane keeps a
+//      running (max, sum of exp2) per head, so the split's (m_t, l_t) is
+//      published as soon as the keys are in;
+//   2. while the other splits arrive, the split-local CDF
+//      P_j = sum_{i<=j} exp2(s_i - m_t) is built in LDS (Sec. 2.1: F is the
+//      running sum of the attention weights); then wait until every split of
+//      the row has published (row counter).  P_last equals l_t up to rounding;
+//      a threshold that falls between a_t P_last and Off_{t+1} - Off_t maps to
+//      the split's last key (the clamp below);
 //   3. global offsets Off_t = sum_{t'<t} a_t' l_t' with a_t = exp2(m_t - m*)
 //      and the total Z, identical in every split; threshold tau_r = ((r + u)/S) Z
 //      (u per row, or u_r) is claimed by the split with Off_t <= tau_r <
@@ -313,6 +318,63 @@ __device__ __forceinline__ bool claim_keys(const HeadClaim *hc, const int *rng, 
   return total > 0;
 }
 
+// Value stage of one split with one query head per wave (G >= 4): after the
+// union of chosen keys is compacted, wave w accumulates heads w, w + 4, ...
+// over the whole list (4 rows per wave instruction, 4 rows in flight per row
+// slot), sums its 4 row slots with lane swaps and writes the heads' 128
+// partial sums directly: O_h += c_{h,j} V_j (Sec. 2, the stochastic add-only
+// attention).
+template <typename E, int G, bool PAGED>
+__device__ __forceinline__ void gather_heads_waves(const KvView &kv, int b, int kvh, int start,
+                                                   int nrows, const int *cnt, int pitch, int *list,
+                                                   float *__restrict__ part_out) {
+  static_assert(G % 4 == 0, "one head per wave needs G >= 4");
+  constexpr int HW = G / 4, U = 4;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, rs = lane >> 4, c = lane & 15;
+  const int nlist = compact_union<G>(cnt, pitch, nrows, list);
+  const E *V = static_cast<const E *>(kv.v);
+  float acc[HW][8];
+#pragma unroll
+  for (int hw = 0; hw < HW; ++hw)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[hw][i] = 0.0f;
+  for (int e0 = rs; e0 < nlist; e0 += 4 * U) {
+    Chunk<E> ch[U];
+    int jj[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int e = e0 + 4 * u;
+      jj[u] = e < nlist ? list[e] : -1;
+      ch[u] = jj[u] >= 0 ? Chunk<E>::load(V + row_offset<PAGED>(kv, b, kvh, start + jj[u]) + c * 8)
+                         : Chunk<E>::zero();
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (jj[u] < 0) continue;
+      float f[8];
+      ch[u].to_float(f);
+#pragma unroll
+      for (int hw = 0; hw < HW; ++hw) {
+        const float w = (float)cnt[(wave + 4 * hw) * pitch + jj[u]];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[hw][i] = fmaf(w, f[i], acc[hw][i]);
+      }
+    }
+  }
+#pragma unroll
+  for (int hw = 0; hw < HW; ++hw)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[hw][i] = xor32_sum(xor16_sum(acc[hw][i]));
+  if (lane < 16) {
+#pragma unroll
+    for (int hw = 0; hw < HW; ++hw) {
+      float2 *dst = reinterpret_cast<float2 *>(part_out + (wave + 4 * hw) * kHeadDim + c * 8);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) st_coherent(dst + i, make_float2(acc[hw][2 * i], acc[hw][2 * i + 1]));
+    }
+  }
+}
+
 template <typename E, int G, bool PAGED, bool STRAT>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(G <= 4 ? 4 : 2))) void k_fused_sampled(FusedArgs a) {
   extern __shared__ float dyn[];
@@ -324,7 +386,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(G <= 4
   float *all = offl + G * (T + 1);
   float *ul = reinterpret_cast<float *>(list + fused_list_ints(G, pitch, T));
   __shared__ HeadClaim hc[G];
-  __shared__ float mh[G], mtmp[4 * G];
+  __shared__ float mh[G], lh[G], mtmp[8 * G];
   __shared__ int wave_cnt[4], rank_lds, rng[2 * G];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -364,19 +426,20 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(G <= 4
       us = ul;
     }
 
-    // 1. scores and split-local CDF; publish (m_t, l_t)
+    // 1. scores with running (max, sum of exp2) per lane; publish the split's
+    //    (m_t, l_t) as soon as the keys are in
     const QRegs<E, G> qr = load_q<E, G>(static_cast<const E *>(a.q), b, a.Hq, kvh, tid & 15);
-    float mx[G];
-    score_tile<E, G, PAGED, kScoreUnroll>(a.kv, b, kvh, start, nrows, qr, a.scale_log2, P, pitch, mx);
-    block_max_heads<G>(mx, mtmp, mh);
-    for (int h = wave; h < G; h += kThreads / 64) wave_split_cdf_m(P + h * pitch, nrows, lane, mh[h]);
-    __syncthreads();
-    if (tid < G)
-      st_coherent(a.stats + (row0 + tid) * T + t, make_float2(mh[tid], P[tid * pitch + nrows - 1]));
-    for (int i = tid; i < G * pitch; i += kThreads) cnt[i] = 0;
-
-    // 2. every split of the row has published its statistics
+    float mx[G], ls[G];
+    score_tile<E, G, PAGED, kScoreUnroll, true>(a.kv, b, kvh, start, nrows, qr, a.scale_log2, P,
+                                                pitch, mx, ls);
+    block_stats_heads<G>(mx, ls, mtmp, mh, lh);
+    if (tid < G) st_coherent(a.stats + (row0 + tid) * T + t, make_float2(mh[tid], lh[tid]));
     row_arrive(sync, base, &rank_lds);
+
+    // 2. split-local CDF and zero counts while the other splits arrive, then
+    //    wait until every split of the row has published its statistics
+    for (int h = wave; h < G; h += kThreads / 64) wave_split_cdf_m(P + h * pitch, nrows, lane, mh[h]);
+    for (int i = tid; i < G * pitch; i += kThreads) cnt[i] = 0;
     row_wait(sync, base + (unsigned long long)Tb, a.err);
 
     // 3. offsets, claimed ranges, inverse CDF, union gather, partial sums
@@ -391,8 +454,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(G <= 4
                                           row0, cnt, a.idx_out);
     __syncthreads();  // counts complete; offl/all are no longer needed
     if (has) {
-      gather_union<E, G, PAGED, true>(a.kv, b, kvh, start, nrows, P, pitch, cnt, list, wave_cnt,
-                                      part_row + (int64_t)t * G * kHeadDim);
+      if constexpr (G >= 4)
+        gather_heads_waves<E, G, PAGED>(a.kv, b, kvh, start, nrows, cnt, pitch, list,
+                                        part_row + (int64_t)t * G * kHeadDim);
+      else
+        gather_union<E, G, PAGED, true>(a.kv, b, kvh, start, nrows, P, pitch, cnt, list, wave_cnt,
+                                        part_row + (int64_t)t * G * kHeadDim);
     } else {  // a split without samples contributes zeros
       float2 *pz = reinterpret_cast<float2 *>(part_row + (int64_t)t * G * kHeadDim);
       for (int o2 = tid; o2 < G * kHeadDim / 2; o2 += kThreads) st_coherent(pz + o2, make_float2(0.f, 0.f));

@@ -55,18 +55,41 @@ __device__ __forceinline__ void store_out(float *p, float x) { *p = x; }
 #endif
 constexpr int kScoreUnroll = SANTA_SCORE_UNROLL;
 
+// Running (max, sum of exp2(s - max)) of a stream of scores: adds y with one
+// exp2 (the smaller of the two terms is rescaled).
+__device__ __forceinline__ void stat_push(float &m, float &l, float y) {
+  const float d = y - m;  // +inf while the stream is empty (m = -inf)
+  const float e = fast_exp2(-fabsf(d));
+  l = d > 0.0f ? fmaf(l, e, 1.0f) : l + e;
+  m = fmaxf(m, y);
+}
+// Combination of two partial (max, sum) pairs.
+__device__ __forceinline__ void stat_merge(float &m, float &l, float m2, float l2) {
+  const float M = fmaxf(m, m2);
+  const float e1 = m == M ? 1.0f : fast_exp2(m - M);
+  const float e2 = m2 == M ? 1.0f : fast_exp2(m2 - M);
+  l = l * e1 + l2 * e2;
+  m = M;
+}
+
 // Score tile (Sec. 2, SDPA equation, the q K^T product):
 // s[h*pitch + j] = scale_log2 * <q_h, K_{start+j}> for j < nrows.
 // Lane c of each 16-lane row holds features 8c..8c+7 of one key; a wave covers
-// 4 keys per 128-bit load and U loads are in flight per lane.
-template <typename E, int G, bool PAGED, int U>
+// 4 keys per 128-bit load and U loads are in flight per lane.  mx[h] receives
+// this lane's running max of head h's scores and, if STATS, ls[h] the running
+// sum of exp2(s - mx[h]) (G = 4: only the lane's own head, others -inf / 0).
+template <typename E, int G, bool PAGED, int U, bool STATS = false>
 __device__ __forceinline__ void score_tile(const KvView &kv, int b, int kvh, int start, int nrows,
                                            const QRegs<E, G> &qr, float scale_log2, float *s,
-                                           int pitch, float (&mx)[G]) {
+                                           int pitch, float (&mx)[G], float (&ls)[G]) {
   const int tid = threadIdx.x, slot = tid >> 4, c = tid & 15;
   const E *K = static_cast<const E *>(kv.k);
+  float m1 = -kInf, l1 = 0.0f;  // G == 4: the lane's own head
 #pragma unroll
-  for (int h = 0; h < G; ++h) mx[h] = -kInf;
+  for (int h = 0; h < G; ++h) {
+    mx[h] = -kInf;
+    ls[h] = 0.0f;
+  }
   for (int base = 0; base < nrows; base += 16 * U) {
     Chunk<E> ch[U];
 #pragma unroll
@@ -89,10 +112,10 @@ __device__ __forceinline__ void score_tile(const KvView &kv, int b, int kvh, int
         y += dpp<0xB1>(y);
         y += dpp<0x4E>(y);
         y *= scale_log2;
-        const int hq = quarter_gray(c);
         if (j < nrows) {
-          mx[hq] = fmaxf(mx[hq], y);
-          if ((c & 3) == 0) s[hq * pitch + j] = y;
+          if (STATS) stat_push(m1, l1, y);
+          else m1 = fmaxf(m1, y);
+          if ((c & 3) == 0) s[quarter_gray(c) * pitch + j] = y;
         }
       } else {
         float acc[G];
@@ -100,7 +123,10 @@ __device__ __forceinline__ void score_tile(const KvView &kv, int b, int kvh, int
         for (int h = 0; h < G; ++h) acc[h] = row16_sum(ch[u].dot(qr.h[h])) * scale_log2;
         if (j < nrows) {
 #pragma unroll
-          for (int h = 0; h < G; ++h) mx[h] = fmaxf(mx[h], acc[h]);
+          for (int h = 0; h < G; ++h) {
+            if (STATS) stat_push(mx[h], ls[h], acc[h]);
+            else mx[h] = fmaxf(mx[h], acc[h]);
+          }
           if (c == 0) {
 #pragma unroll
             for (int h = 0; h < G; ++h) s[h * pitch + j] = acc[h];
@@ -109,6 +135,89 @@ __device__ __forceinline__ void score_tile(const KvView &kv, int b, int kvh, int
       }
     }
   }
+  if constexpr (G == 4) {
+    const int hq = quarter_gray(c);
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      mx[h] = h == hq ? m1 : -kInf;
+      ls[h] = h == hq ? l1 : 0.0f;
+    }
+  }
+}
+
+// Without the running sums.
+template <typename E, int G, bool PAGED, int U>
+__device__ __forceinline__ void score_tile(const KvView &kv, int b, int kvh, int start, int nrows,
+                                           const QRegs<E, G> &qr, float scale_log2, float *s,
+                                           int pitch, float (&mx)[G]) {
+  float ls[G];
+  score_tile<E, G, PAGED, U, false>(kv, b, kvh, start, nrows, qr, scale_log2, s, pitch, mx, ls);
+}
+
+// Split (max, sum of exp2(s - max)) of every head from the score tile's
+// per-lane running pairs (all threads get them in mh[h], lh[h]); tmp holds
+// 8*G floats.
+template <int G>
+__device__ __forceinline__ void block_stats_heads(float (&mx)[G], float (&ls)[G], float *tmp,
+                                                  float *mh, float *lh) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if constexpr (G == 4) {
+    // the four lanes of a quarter hold the same pair; combine the 4 rows
+    const int hq = quarter_gray(lane & 15);
+    float m = mx[0], l = ls[0];
+#pragma unroll
+    for (int h = 1; h < G; ++h) {
+      m = h == hq ? mx[h] : m;
+      l = h == hq ? ls[h] : l;
+    }
+    {
+      const auto pm = __builtin_amdgcn_permlane16_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+      const auto pl = __builtin_amdgcn_permlane16_swap(__float_as_uint(l), __float_as_uint(l), false, false);
+      m = __uint_as_float(pm[0]); l = __uint_as_float(pl[0]);
+      stat_merge(m, l, __uint_as_float(pm[1]), __uint_as_float(pl[1]));
+    }
+    {
+      const auto pm = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+      const auto pl = __builtin_amdgcn_permlane32_swap(__float_as_uint(l), __float_as_uint(l), false, false);
+      m = __uint_as_float(pm[0]); l = __uint_as_float(pl[0]);
+      stat_merge(m, l, __uint_as_float(pm[1]), __uint_as_float(pl[1]));
+    }
+    if (lane < 16 && (lane & 3) == 0) {
+      tmp[(wave * G + hq) * 2] = m;
+      tmp[(wave * G + hq) * 2 + 1] = l;
+    }
+  } else {
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      // lanes of a 16-lane row hold the same pair; combine the 4 rows
+      float m = mx[h], l = ls[h];
+      {
+        const auto pm = __builtin_amdgcn_permlane16_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+        const auto pl = __builtin_amdgcn_permlane16_swap(__float_as_uint(l), __float_as_uint(l), false, false);
+        m = __uint_as_float(pm[0]); l = __uint_as_float(pl[0]);
+        stat_merge(m, l, __uint_as_float(pm[1]), __uint_as_float(pl[1]));
+      }
+      {
+        const auto pm = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+        const auto pl = __builtin_amdgcn_permlane32_swap(__float_as_uint(l), __float_as_uint(l), false, false);
+        m = __uint_as_float(pm[0]); l = __uint_as_float(pl[0]);
+        stat_merge(m, l, __uint_as_float(pm[1]), __uint_as_float(pl[1]));
+      }
+      if (lane == 0) {
+        tmp[(wave * G + h) * 2] = m;
+        tmp[(wave * G + h) * 2 + 1] = l;
+      }
+    }
+  }
+  __syncthreads();
+  if (tid < G) {
+    float m = tmp[tid * 2], l = tmp[tid * 2 + 1];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) stat_merge(m, l, tmp[(w * G + tid) * 2], tmp[(w * G + tid) * 2 + 1]);
+    mh[tid] = m;
+    lh[tid] = l;
+  }
+  __syncthreads();
 }
 
 // Split max of every head from the score tile's per-lane maxima (all threads
@@ -319,28 +428,20 @@ __device__ __forceinline__ bool claim_search(int start, int nrows, int64_t row0,
   return __syncthreads_or(any) != 0;
 }
 
-// Value stage of one split after claim_search: the union over the group's
-// heads of the chosen keys is compacted in key order and each chosen V row is
-// read once: O_h += c_{h,j} V_j (Sec. 2, Eq. "stochastic-add-only-attn").  The
-// G x 128 partial sums are written to part_out (global; coherent stores if
-// COHERENT).  P is reused as the reduction buffer.
-template <typename E, int G, bool PAGED, bool COHERENT>
-__device__ __forceinline__ void gather_union(const KvView &kv, int b, int kvh, int start, int nrows,
-                                             float *P, int pitch, const int *cnt, int *list,
-                                             int *wave_cnt, float *__restrict__ part_out) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, slot = tid >> 4, c = tid & 15;
-  // compact the union of chosen keys in key order: one ballot mask per 64 keys
+// Union over the group's heads of the keys with a nonzero count (cnt[h*pitch
+// + j], j < nrows), compacted in key order into list[]; returns its length
+// (block-uniform).  One ballot mask per 64 keys, then an exclusive prefix.
+template <int G>
+__device__ __forceinline__ int compact_union(const int *cnt, int pitch, int nrows, int *list) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   __shared__ unsigned long long masks[kSplitMax / 64];
   const int nch = (nrows + 63) >> 6;
   for (int ch = wave; ch < nch; ch += kThreads / 64) {
     const int j = ch * 64 + lane;
     const int jc = min(j, nrows - 1);
-    int c4[G];
-#pragma unroll
-    for (int h = 0; h < G; ++h) c4[h] = cnt[h * pitch + jc];
     bool need = false;
 #pragma unroll
-    for (int h = 0; h < G; ++h) need |= c4[h] != 0;
+    for (int h = 0; h < G; ++h) need |= cnt[h * pitch + jc] != 0;
     const unsigned long long m = __ballot(need && j < nrows);
     if (lane == 0) masks[ch] = m;
   }
@@ -355,8 +456,22 @@ __device__ __forceinline__ void gather_union(const KvView &kv, int b, int kvh, i
     const int off = __builtin_amdgcn_readlane(excl, ch);
     if ((m >> lane) & 1ull) list[off + __popcll(m & ((1ull << lane) - 1ull))] = ch * 64 + lane;
   }
-  (void)wave_cnt;
   __syncthreads();
+  return nlist;
+}
+
+// Value stage of one split after claim_search: the union over the group's
+// heads of the chosen keys is compacted in key order and each chosen V row is
+// read once: O_h += c_{h,j} V_j (Sec. 2, Eq. "stochastic-add-only-attn").  The
+// G x 128 partial sums are written to part_out (global; coherent stores if
+// COHERENT).  P is reused as the reduction buffer.
+template <typename E, int G, bool PAGED, bool COHERENT>
+__device__ __forceinline__ void gather_union(const KvView &kv, int b, int kvh, int start, int nrows,
+                                             float *P, int pitch, const int *cnt, int *list,
+                                             int *wave_cnt, float *__restrict__ part_out) {
+  const int tid = threadIdx.x, slot = tid >> 4, c = tid & 15;
+  (void)wave_cnt;
+  const int nlist = compact_union<G>(cnt, pitch, nrows, list);
   // gather-add: slot takes list entries slot, slot+16, ...; 4 rows in flight
   const E *V = static_cast<const E *>(kv.v);
   float acc[G][8];
