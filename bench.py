@@ -239,9 +239,7 @@ def main():
         **res,
         "roofline": {
             "bound": "hbm",
-            "kernel": ("k_fused_" + ("dense" if kind == "dense" else "sampled")
-                       if os.environ.get("SANTA_VARIANT", "fused") != "multi" and kind != "bernoulli"
-                       else "all kernels of one santa_decode_* call"),
+            "kernel": kernel_label(w, kind),
             "timing": ("HIP events the library attaches to its kernel dispatch "
                        "(santa_time_next_call), mean over the timed cold-cache steps"),
             "kernel_us": round(float(kus.mean()), 3),
@@ -254,9 +252,62 @@ def main():
         "timed_wall_s": round(wall, 3),
     }
 
+    # counter-based traffic exists for the default workload only
+    if (args.cfg == 2 and args.B is None and args.S is None and args.kind is None
+            and args.layout == "nhd" and line["roofline"]["kernel"].startswith("k_fused_")):
+        line["roofline"]["traffic"] = measured_traffic(line["roofline"]["kernel"],
+                                                       "traffic_llama8b_32k_b1.json")
     if not args.no_cpu and not args.profile:
         line["cpu_baseline"] = cpu_baseline(w, kind, alg_bytes, args.cpu_seconds)
     print(json.dumps(line), flush=True)
+
+
+def kernel_label(w, kind: str) -> str:
+    """Name of the kernel(s) one call launches, following the library's path
+    choice: the sampled step takes two launches when its rows exceed one
+    resident round of ~1024 workgroups (splits per row: at least n_k / 1024,
+    and 128 halved while splits x rows > 512)."""
+    if os.environ.get("SANTA_VARIANT", "fused") == "multi" or kind == "bernoulli":
+        return "all kernels of one santa_decode_* call"
+    if kind == "dense":
+        return "k_fused_dense"
+    rows = w.B * w.Hkv
+    fill = 128
+    while fill > 1 and fill * rows > 512:
+        fill //= 2
+    T = max((w.n_max + 1023) // 1024, fill)
+    forced = os.environ.get("SANTA_SAMPLED", "")
+    two = forced == "split" or (forced != "fused" and rows * T > 1024)
+    return "k_stream_cdf + k_value_heads" if two else "k_fused_sampled"
+
+
+def kernel_source_hash() -> str:
+    """Hash of the HIP sources (file names and contents), as recorded with the
+    counter runs under profiles/."""
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2605_01910_amd", "csrc")
+    for f in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.h"))):
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel: str, workload_file: str):
+    """HBM bytes per launch of `kernel` from the committed FETCH_SIZE /
+    WRITE_SIZE runs, or None if there are none for this workload or the
+    kernel sources changed since they were taken."""
+    path = os.path.join(ROOT, "profiles", workload_file)
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        rec = json.load(fh)
+    if rec.get("source_hash") != kernel_source_hash():
+        return None
+    k = rec.get("kernels", {}).get(kernel)
+    return None if k is None else int(k["bytes"])
 
 
 def cpu_baseline(w, kind, alg_bytes, seconds):

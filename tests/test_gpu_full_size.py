@@ -1,0 +1,62 @@
+"""GPU parity at the full benchmark shapes, in the launch configuration the
+benchmark times (default split counts and path choice, seed 0 as in bench.py).
+
+Configurations 2, 3 and 5 are checked on every row: the oracle finishes a
+full 32k-context step in milliseconds.  Configuration 4 (paged, 64 sequences
+of up to 64k keys) is checked on a sample of rows that includes the shortest
+and the longest sequence and rows of every KV head."""
+
+import numpy as np
+import pytest
+
+from tests.gpu_util import check_dense, check_sampled, log, run
+from workload import make_workload
+
+pytestmark = pytest.mark.gpu
+
+
+def test_cfg2_full_every_row():
+    w = make_workload(2, seed=0)
+    log(f"[full cfg2] B={w.B} n={w.n_max} {w.kind} S={w.S}")
+    out, idx, _ = run(w)
+    log(f"  sampled {check_sampled(w, out, idx)}")
+    d, _, _ = run(w, "dense")
+    log(f"  dense {check_dense(w, d)}")
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("S", [128, 256, 512])
+def test_cfg3_full_every_row(S):
+    w = make_workload(3, seed=0, S=S)
+    log(f"[full cfg3] B={w.B} n={w.n_max} {w.kind} S={w.S}")
+    out, idx, _ = run(w)
+    log(f"  sampled {check_sampled(w, out, idx)}")
+    if S == 256:
+        d, _, _ = run(w, "dense")
+        log(f"  dense {check_dense(w, d)}")
+
+
+@pytest.mark.timeout(600)
+def test_cfg4_paged_full_sampled_rows():
+    w = make_workload(4, seed=0)
+    order = np.argsort(w.ctx_len)
+    bs = sorted({int(order[0]), int(order[-1]), int(order[len(order) // 2]), 5, 37})
+    rows = [b * w.Hq + h for b in bs for h in range(0, w.Hq, 3)]
+    log(f"[full cfg4] B={w.B} n_max={w.n_max} ctx {w.ctx_len.min()}..{w.ctx_len.max()} "
+        f"rows={len(rows)} of {w.B * w.Hq}")
+    out, idx, _ = run(w)
+    log(f"  sampled {check_sampled(w, out, idx, rows=rows)}")
+    d, _, _ = run(w, "dense")
+    log(f"  dense {check_dense(w, d, rows=rows)}")
+
+
+@pytest.mark.timeout(300)
+def test_cfg5_bernoulli_full_every_row():
+    from oracle import oracle as O
+    w = make_workload(5, seed=0)
+    log(f"[full cfg5] B={w.B} n={w.n_max} bernoulli mode={w.mode} S={w.S}")
+    out, idx, mask = run(w, want_mask=True)
+    log(f"  sampled {check_sampled(w, out, idx, 'bernoulli')}")
+    res = O.decode_workload(w, "bernoulli", rows=[b * w.Hq + kv * w.G for b in range(w.B)
+                                                  for kv in range(w.Hkv)], want_weights=True)
+    assert np.array_equal(mask, res.mask.reshape(w.B, w.Hkv, w.d)), "feature mask differs"
