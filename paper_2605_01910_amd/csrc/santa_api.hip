@@ -105,6 +105,9 @@ santa_status_t check_kv(const santa_kv_t *kv, const santa_shape_t *sh, bool need
     return fail(SANTA_ERR_INVALID_ARG, "strides must be non-negative");
   if (kv->stride_b % a || kv->stride_n % a || kv->stride_h % a)
     return fail(SANTA_ERR_UNSUPPORTED, "strides must keep every row 16-byte aligned");
+  // a lane's byte offset inside a 16-row batch of keys is 32 bits
+  if ((15 * kv->stride_n + santa::kHeadDim) * esz >= (int64_t(1) << 31))
+    return fail(SANTA_ERR_UNSUPPORTED, "stride_n too large");
   if ((need_k && (reinterpret_cast<uintptr_t>(kv->k) & 15)) ||
       (reinterpret_cast<uintptr_t>(kv->v) & 15))
     return fail(SANTA_ERR_UNSUPPORTED, "k and v must be 16-byte aligned");

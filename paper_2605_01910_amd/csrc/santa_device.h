@@ -41,6 +41,9 @@ struct Chunk<uint16_t> {
     f[0] = bf16_lo(w.x); f[1] = bf16_hi(w.x); f[2] = bf16_lo(w.y); f[3] = bf16_hi(w.y);
     f[4] = bf16_lo(w.z); f[5] = bf16_hi(w.z); f[6] = bf16_lo(w.w); f[7] = bf16_hi(w.w);
   }
+  __device__ __forceinline__ void require() const {
+    asm volatile("" ::"v"(w.x), "v"(w.y), "v"(w.z), "v"(w.w));
+  }
   // <this, q> over the 8 features
   __device__ __forceinline__ float dot(const Chunk &q) const {
     float a = dot2_bf16(w.x, q.w.x, 0.0f);
@@ -61,6 +64,10 @@ struct Chunk<float> {
   }
   __device__ __forceinline__ void to_float(float (&f)[8]) const {
     f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w; f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
+  }
+  __device__ __forceinline__ void require() const {
+    asm volatile("" ::"v"(a.x), "v"(a.y), "v"(a.z), "v"(a.w));
+    asm volatile("" ::"v"(b.x), "v"(b.y), "v"(b.z), "v"(b.w));
   }
   __device__ __forceinline__ float dot(const Chunk &q) const {
     float s = a.x * q.a.x;

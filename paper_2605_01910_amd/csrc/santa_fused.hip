@@ -69,8 +69,7 @@ struct FusedArgs {
   unsigned long long *sync;  // [B*Hkv][kSyncStride/2] arrival counter, counter base
   int *err;       // [1]                set if a wait gave up
   int B, Hq, Hkv, T, S;
-  int Lsmax;      // longest split (keys) of any row: LDS arrays are sized by it
-  int ustage;     // stratified uniforms of the group staged in LDS (G*S floats) if 1
+  int ustage;     // the group's uniforms (G*S stratified, G systematic) staged in LDS if 1
   int64_t npitch; // stash floats per head row (n_k rounded up to 64)
   float invS, scale_log2;
   int xcd;
@@ -80,13 +79,17 @@ constexpr int kSpinLimit = 1 << 22;
 constexpr int kAlign = 64;         // split lengths and stash rows are multiples of this many keys
 constexpr int kBlock = 32;         // keys per block of the two-level CDF search
 constexpr int kGatherUnroll = 8;   // V rows in flight per row slot in k_value_heads
+constexpr int kUReg = 4;           // uniforms per thread fetched into registers before the stream
+constexpr int kUStageMax = 4096;   // largest uniform set (floats per KV group) staged in LDS
 
 // ---------------------------------------------------------------------------
 // LDS sizes (dynamic shared memory), in floats
 // ---------------------------------------------------------------------------
+// LDS arrays of a split have a row pitch of kSplitMax keys (a compile-time
+// constant, so per-key LDS offsets are immediates).
 // k_fused_sampled: P [G][Lsmax] (scores, CDF; then the slot reduction and the
 // merge scratch), cnt [G][Lsmax], list [max(Lsmax, 2G(T+1))] (offsets and
-// split factors before the claims, the union list after), ul [G*S] if staged.
+// split factors before the claims, the union list after), ul [G*S or G] if staged.
 __host__ __device__ constexpr int imax(int x, int y) { return x > y ? x : y; }
 __host__ __device__ constexpr int fused_p_floats(int G, int Lsmax, int T) {
   return imax(imax(G * Lsmax, 4 * G * kHeadDim), T + kThreads);
@@ -98,10 +101,11 @@ __host__ __device__ constexpr int fused_sampled_floats(int G, int Lsmax, int T, 
   return fused_p_floats(G, Lsmax, T) + G * Lsmax + fused_list_ints(G, Lsmax, T) + ustaged;
 }
 // k_fused_dense: s [G][Lsmax], red [4][G*128] (also the merge scratch).
+// (Lsmax = kSplitMax in every launch.)
 __host__ __device__ constexpr int fused_dense_floats(int G, int Lsmax, int T) {
   return G * Lsmax + imax(4 * G * kHeadDim, T + kThreads);
 }
-// k_stream_cdf: P [G][Lsmax].
+// k_stream_cdf: P [G][kSplitMax].
 // k_value_heads: block ends [ncoarse], offsets [T+1], split factors [T], chosen
 // keys and run list [2][kThreads], slot reduction [4][128].
 __host__ __device__ constexpr int value_heads_floats(int T, int ncoarse) {
@@ -177,6 +181,26 @@ __device__ __forceinline__ void row_wait(const unsigned long long *sync, unsigne
   __syncthreads();
 }
 
+// row_wait for a workgroup that has already arrived: thread 0 holds in
+// `arrived` the counter value its own arrival produced and skips the poll when
+// that value already reaches `target` (the last arrival).
+__device__ __forceinline__ void row_wait_unless(const unsigned long long *sync,
+                                                unsigned long long target,
+                                                unsigned long long arrived, int *err) {
+  if (threadIdx.x == 0 && arrived < target) {
+    int spins = 0;
+    while (__hip_atomic_load(const_cast<unsigned long long *>(sync), __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT) < target) {
+      if (++spins > kSpinLimit) {
+        atomicOr(err, 1);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+  }
+  __syncthreads();
+}
+
 // One wave: global offsets of one head over the row's Tb splits.  off[0..Tb]
 // receives Off_0 = 0, Off_{t+1} = Off_t + a_t l_t with a_t = exp2(m_t - m*),
 // made exactly non-decreasing; al[t] receives a_t.  Returns m*.  Lane l owns
@@ -223,7 +247,7 @@ __device__ __forceinline__ float head_offsets_wave(const float2 *st, int Tb, int
 
 // out_h = scale * sum_t w_t part[t][h*128 + o] (w_t = 1 if w is null), divided
 // by *den if den is not null.  Two interleaved halves of the splits, each
-// summed in split order with 16 loads in flight, then added.  scratch holds
+// summed in split order with 32 loads in flight, then added.  scratch holds
 // kThreads floats.
 template <typename E, int G>
 __device__ __forceinline__ void merge_head(const float *part_row, int h, int Tb, const float *w,
@@ -233,15 +257,15 @@ __device__ __forceinline__ void merge_head(const float *part_row, int h, int Tb,
   const float *ph = part_row + h * kHeadDim + o;
   const int nk = (Tb - g + 1) >> 1;  // splits g, g + 2, ...
   float s = 0.0f;
-  for (int k0 = 0; k0 < nk; k0 += 16) {
-    float v[16];
+  for (int k0 = 0; k0 < nk; k0 += 32) {
+    float v[32];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
+    for (int i = 0; i < 32; ++i) {
       const int tt = g + 2 * (k0 + i);
       v[i] = k0 + i < nk ? ld_coherent(ph + (int64_t)tt * G * kHeadDim) : 0.0f;
     }
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
+    for (int i = 0; i < 32; ++i) {
       const int tt = g + 2 * (k0 + i);
       if (k0 + i < nk) s = w ? fmaf(w[tt], v[i], s) : s + v[i];
     }
@@ -258,6 +282,53 @@ __device__ __forceinline__ void merge_head(const float *part_row, int h, int Tb,
 // ---------------------------------------------------------------------------
 // Small-batch sampled step
 // ---------------------------------------------------------------------------
+// #{j < nrows : a P_j <= x} over a non-decreasing LDS CDF P (nrows <=
+// kSplitMax): branch-free binary lifting in a rolled loop (a handful of
+// instructions; one LDS read per step).
+__device__ __forceinline__ int lds_cdf_count(const float *Ph, int nrows, float a, float x) {
+  int pos = 0;
+#pragma unroll 1
+  for (int step = 1 << (31 - __clz(nrows)); step > 0; step >>= 1) {
+    const int np = pos + step;
+    const float v = Ph[min(np, nrows) - 1];
+    pos = (np <= nrows && a * v <= x) ? np : pos;
+  }
+  return pos;
+}
+
+// Claims and inverse CDF of one split when the group's uniforms are few
+// (G*S <= kUStageMax): the G*S thresholds tau = ((r + u)/S) Z are numbered
+// n = r*G + h (the G heads of one r on neighbouring lanes) and thread i
+// evaluates n = i, i + kThreads, ...; those with lo <= tau < hi belong to this
+// split and map to the key #{j : a P_j <= tau - lo} (the CDF interval holding
+// tau, App. A), clamped to the split.  A split's claims form one range of r per
+// head, so a wave usually searches once.  Counts per key go to cnt (LDS),
+// indices to idx_out.  Returns (block-uniform) whether the split holds any
+// sample.
+template <int G, bool STRAT>
+__device__ __forceinline__ bool claim_scan(const HeadClaim *hc, const float *ul, int S, float invS,
+                                           const float *P, int pitch, int start, int nrows,
+                                           int64_t row0, int *cnt, int32_t *__restrict__ idx_out) {
+  const int tid = threadIdx.x;
+  const int h = tid % G;  // the same head on every pass (kThreads is a multiple of G)
+  const HeadClaim c = hc[h];
+  const float *Ph = P + h * pitch;
+  bool any = false;
+#pragma unroll 1
+  for (int n = tid; n < G * S; n += kThreads) {
+    const int r = n / G;
+    const float tau = threshold(r, STRAT ? ul[h * S + r] : ul[h], invS, c.Z);
+    if ((tau >= c.lo) & (tau < c.hi)) {
+      const int pos = lds_cdf_count(Ph, nrows, c.a, tau - c.lo);
+      const int j = pos < nrows ? pos : nrows - 1;
+      atomicAdd(&cnt[h * pitch + j], 1);
+      if (idx_out) idx_out[(row0 + h) * S + r] = start + j;
+      any = true;
+    }
+  }
+  return __syncthreads_or(any) != 0;
+}
+
 // Threshold r of head h is claimed iff lo <= tau_r < hi.  tau_r is
 // non-decreasing in r (fp32 rounding is monotone), so the claimed r form the
 // range [#{r : tau_r < lo}, #{r : tau_r < hi}); threads 2h and 2h+1 count the
@@ -296,7 +367,6 @@ __device__ __forceinline__ bool claim_keys(const HeadClaim *hc, const int *rng, 
 #pragma unroll
   for (int h = 0; h < G; ++h) first[h + 1] = first[h] + max(0, rng[2 * h + 1] - rng[2 * h]);
   const int total = first[G];
-  const int step0 = 1 << (31 - __clz(nrows));
   for (int i = tid; i < total; i += kThreads) {
     int h = 0;
 #pragma unroll
@@ -304,13 +374,7 @@ __device__ __forceinline__ bool claim_keys(const HeadClaim *hc, const int *rng, 
     const int r = rng[2 * h] + (i - first[h]);
     const HeadClaim c = hc[h];
     const float tau = threshold(r, STRAT ? us[h * ustride + r] : us[h * ustride], invS, c.Z);
-    const float x = tau - c.lo;
-    const float *Ph = P + h * pitch;
-    int pos = 0;
-    for (int step = step0; step > 0; step >>= 1) {
-      const int np = pos + step;
-      pos = (np <= nrows && c.a * Ph[np - 1] <= x) ? np : pos;
-    }
+    const int pos = lds_cdf_count(P + h * pitch, nrows, c.a, tau - c.lo);
     const int j = pos < nrows ? pos : nrows - 1;
     atomicAdd(&cnt[h * pitch + j], 1);
     if (idx_out) idx_out[(row0 + h) * S + r] = start + j;
@@ -376,9 +440,10 @@ __device__ __forceinline__ void gather_heads_waves(const KvView &kv, int b, int 
 }
 
 template <typename E, int G, bool PAGED, bool STRAT>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(G <= 4 ? 4 : 2))) void k_fused_sampled(FusedArgs a) {
-  extern __shared__ float dyn[];
-  const int pitch = a.Lsmax, T = a.T;
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void k_fused_sampled(FusedArgs a) {
+  extern __shared__ __attribute__((aligned(16))) float dyn[];
+  constexpr int pitch = kSplitMax;
+  const int T = a.T;
   float *P = dyn;
   int *cnt = reinterpret_cast<int *>(dyn + fused_p_floats(G, pitch, T));
   int *list = cnt + G * pitch;
@@ -418,40 +483,71 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(G <= 4
         __hip_atomic_load(sync + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     float *part_row = a.part + (int64_t)rowkv * T * G * kHeadDim;
 
-    // uniforms of the group (read while the keys stream)
+    // uniforms of the group: G*S (stratified) or G (systematic) consecutive
+    // floats, staged in LDS when there are few of them; the first
+    // kUReg*kThreads are fetched into registers before the keys stream
     const float *us = STRAT ? a.u + row0 * a.S : a.u + row0;
     const int64_t ustride = STRAT ? a.S : 1;
-    if (STRAT && a.ustage) {
-      for (int i = tid; i < G * a.S; i += kThreads) ul[i] = us[i];
-      us = ul;
+    const int nu = STRAT ? G * a.S : G;
+    float ureg[kUReg];
+    if (a.ustage) {
+#pragma unroll
+      for (int k = 0; k < kUReg; ++k) {
+        const int i = tid + k * kThreads;
+        ureg[k] = i < nu ? us[i] : 0.0f;
+      }
     }
 
-    // 1. scores with running (max, sum of exp2) per lane; publish the split's
-    //    (m_t, l_t) as soon as the keys are in
+    // 1. scores of the G heads into LDS; split max m_t per head
     const QRegs<E, G> qr = load_q<E, G>(static_cast<const E *>(a.q), b, a.Hq, kvh, tid & 15);
-    float mx[G], ls[G];
-    score_tile<E, G, PAGED, kScoreUnroll, true>(a.kv, b, kvh, start, nrows, qr, a.scale_log2, P,
-                                                pitch, mx, ls);
-    block_stats_heads<G>(mx, ls, mtmp, mh, lh);
-    if (tid < G) st_coherent(a.stats + (row0 + tid) * T + t, make_float2(mh[tid], lh[tid]));
-    row_arrive(sync, base, &rank_lds);
+    float mx[G];
+    score_tile<E, G, PAGED, score_unroll<E, G>()>(a.kv, b, kvh, start, nrows, qr, a.scale_log2, P,
+                                                  pitch, mx);
+    block_max_heads<G>(mx, mtmp, mh);
 
-    // 2. split-local CDF and zero counts while the other splits arrive, then
-    //    wait until every split of the row has published its statistics
-    for (int h = wave; h < G; h += kThreads / 64) wave_split_cdf_m(P + h * pitch, nrows, lane, mh[h]);
+    // 2. split-local CDF of head h by wave h; the split's (m_t, l_t = P_last)
+    //    is published as soon as its CDF is built, then the workgroup arrives
+    for (int h = wave; h < G; h += kThreads / 64) {
+      float *Ph = P + h * pitch;
+      wave_split_cdf_m(Ph, nrows, lane, mh[h]);
+      if (lane == 0) st_coherent(a.stats + (row0 + h) * T + t, make_float2(mh[h], Ph[nrows - 1]));
+    }
+    wait_stores();
+    __syncthreads();
+    unsigned long long arrived = 0;
+    if (tid == 0)
+      arrived = __hip_atomic_fetch_add(sync, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1;
+
+    // zero counts and stage the uniforms while the other splits arrive, then
+    // wait until every split of the row has published (the last arrival does
+    // not wait)
     for (int i = tid; i < G * pitch; i += kThreads) cnt[i] = 0;
-    row_wait(sync, base + (unsigned long long)Tb, a.err);
+    if (a.ustage) {
+#pragma unroll
+      for (int k = 0; k < kUReg; ++k) {
+        const int i = tid + k * kThreads;
+        if (i < nu) ul[i] = ureg[k];
+      }
+      for (int i = tid + kUReg * kThreads; i < nu; i += kThreads) ul[i] = us[i];
+    }
+    row_wait_unless(sync, base + (unsigned long long)Tb, arrived, a.err);
 
-    // 3. offsets, claimed ranges, inverse CDF, union gather, partial sums
+    // 3. offsets, claims, inverse CDF, union gather, partial sums
     for (int h = wave; h < G; h += kThreads / 64) {
       float *oh = offl + h * (T + 1), *ah = all + h * T;
       head_offsets_wave<true>(a.stats + (row0 + h) * T, Tb, lane, oh, ah);
       if (lane == 0) hc[h] = HeadClaim{oh[t], t == Tb - 1 ? kInf : oh[t + 1], oh[Tb], ah[t]};
     }
     __syncthreads();
-    claim_ranges<G, STRAT>(hc, us, ustride, a.S, a.invS, rng);
-    const bool has = claim_keys<G, STRAT>(hc, rng, us, ustride, a.S, a.invS, P, pitch, start, nrows,
-                                          row0, cnt, a.idx_out);
+    bool has;
+    if (a.ustage) {
+      has = claim_scan<G, STRAT>(hc, ul, a.S, a.invS, P, pitch, start, nrows, row0, cnt,
+                                 a.idx_out);
+    } else {
+      claim_ranges<G, STRAT>(hc, us, ustride, a.S, a.invS, rng);
+      has = claim_keys<G, STRAT>(hc, rng, us, ustride, a.S, a.invS, P, pitch, start, nrows, row0,
+                                 cnt, a.idx_out);
+    }
     __syncthreads();  // counts complete; offl/all are no longer needed
     if (has) {
       if constexpr (G >= 4)
@@ -484,10 +580,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(G <= 4
 // Dense step
 // ---------------------------------------------------------------------------
 template <typename E, int G, bool PAGED>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(G <= 4 ? 4 : 2))) void k_fused_dense(FusedArgs a) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void k_fused_dense(FusedArgs a) {
   // dynamic LDS: s [G][pitch] scores / weights, red [4][G*128] (also the merge scratch)
-  extern __shared__ float dyn[];
-  const int pitch = a.Lsmax;
+  extern __shared__ __attribute__((aligned(16))) float dyn[];
+  constexpr int pitch = kSplitMax;
   float *s = dyn;
   float *red = s + G * pitch;
   __shared__ float mh[G], lh[G], mtmp[4 * G], den;
@@ -522,7 +618,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(G <= 4
 
     const QRegs<E, G> qr = load_q<E, G>(static_cast<const E *>(a.q), b, a.Hq, kvh, c);
     float mx[G];
-    score_tile<E, G, PAGED, kScoreUnroll>(a.kv, b, kvh, start, nrows, qr, a.scale_log2, s, pitch, mx);
+    score_tile<E, G, PAGED, score_unroll<E, G>()>(a.kv, b, kvh, start, nrows, qr, a.scale_log2, s,
+                                                  pitch, mx);
     block_max_heads<G>(mx, mtmp, mh);
     for (int h = wave; h < G; h += kThreads / 64) {
       float *sh = s + h * pitch;
@@ -538,32 +635,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(G <= 4
     }
     __syncthreads();
     float acc[G][8];
-#pragma unroll
-    for (int h = 0; h < G; ++h)
-#pragma unroll
-      for (int i = 0; i < 8; ++i) acc[h][i] = 0.0f;
-    constexpr int U = 4;
-    for (int base_j = 0; base_j < nrows; base_j += 16 * U) {
-      Chunk<E> ch[U];
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int j = base_j + u * 16 + slot;
-        ch[u] = j < nrows ? Chunk<E>::load(V + row_offset<PAGED>(a.kv, b, kvh, start + j) + c * 8)
-                          : Chunk<E>::zero();
-      }
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int j = base_j + u * 16 + slot;
-        float f[8];
-        ch[u].to_float(f);
-#pragma unroll
-        for (int h = 0; h < G; ++h) {
-          const float w = j < nrows ? s[h * pitch + j] : 0.0f;
-#pragma unroll
-          for (int i = 0; i < 8; ++i) acc[h][i] = fmaf(w, f[i], acc[h][i]);
-        }
-      }
-    }
+    value_tile<E, G, PAGED, score_unroll<E, G>()>(a.kv, b, kvh, start, nrows, s, pitch, acc);
     reduce_slots<G>(acc, red);
     float2 *mypart = reinterpret_cast<float2 *>(part_row + (int64_t)t * G * kHeadDim);
     for (int o2 = tid; o2 < G * kHeadDim / 2; o2 += kThreads) {
@@ -618,9 +690,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(G <= 4
 // One work item per workgroup, items row-major; the hardware dispatcher
 // balances them.  Writes the stash, the block ends and the statistics.
 template <typename E, int G, bool PAGED>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(G <= 4 ? 4 : 2))) void k_stream_cdf(FusedArgs a) {
-  extern __shared__ float dyn[];
-  const int pitch = a.Lsmax, T = a.T;
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(sizeof(E) == 2 && G <= 4 && !PAGED ? 8 : (G <= 4 ? 4 : 2)))) void k_stream_cdf(FusedArgs a) {
+  extern __shared__ __attribute__((aligned(16))) float dyn[];
+  constexpr int pitch = kSplitMax;
+  const int T = a.T;
   float *P = dyn;
   __shared__ float mh[G], mtmp[4 * G];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -635,7 +708,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(G <= 4
 
   const QRegs<E, G> qr = load_q<E, G>(static_cast<const E *>(a.q), b, a.Hq, kvh, tid & 15);
   float mx[G];
-  score_tile<E, G, PAGED, kScoreUnroll>(a.kv, b, kvh, start, nrows, qr, a.scale_log2, P, pitch, mx);
+  // 4 rows per lane and batch: this kernel relies on many resident waves
+  // (64 VGPRs) rather than on deep per-wave buffering
+  score_tile<E, G, PAGED, 4>(a.kv, b, kvh, start, nrows, qr, a.scale_log2, P, pitch, mx);
   block_max_heads<G>(mx, mtmp, mh);
   for (int h = wave; h < G; h += kThreads / 64) wave_split_cdf_m(P + h * pitch, nrows, lane, mh[h]);
   __syncthreads();
@@ -713,7 +788,7 @@ __device__ __forceinline__ int invert_threshold(const float *Pst, const float *c
 // V_{idx_r} (Sec. 2, the stochastic add-only attention).
 template <typename E, bool PAGED, bool STRAT>
 __global__ __launch_bounds__(kThreads) void k_value_heads(FusedArgs a, int G) {
-  extern __shared__ float dyn[];
+  extern __shared__ __attribute__((aligned(16))) float dyn[];
   __shared__ int wave_cnt[4];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, slot = tid >> 4, c = tid & 15;
   const int64_t rowq = blockIdx.x;
@@ -880,7 +955,6 @@ FusedArgs make_args(const Plan &p, const KvView &kv, const void *q, void *out, f
   a.Hkv = p.Hkv;
   a.T = p.T;
   a.S = p.S;
-  a.Lsmax = p.Ls;
   a.npitch = p.npitch;
   a.invS = p.S ? 1.0f / (float)p.S : 0.0f;
   a.scale_log2 = scale_log2;
@@ -897,7 +971,7 @@ hipError_t launch_fused_dense(const Plan &p, const KvView &kv, const void *q, fl
     using E = std::remove_pointer_t<decltype(eptr)>;
     constexpr int G = decltype(gc)::value;
     constexpr bool PG = decltype(paged)::value;
-    const size_t lds = (size_t)fused_dense_floats(G, p.Ls, p.T) * 4;
+    const size_t lds = (size_t)fused_dense_floats(G, kSplitMax, p.T) * 4;
     return launch_resident(reinterpret_cast<const void *>(&k_fused_dense<E, G, PG>), p, args, lds,
                            st);
   });
@@ -916,7 +990,7 @@ hipError_t launch_fused_sampled(const Plan &p, const KvView &kv, const void *q, 
     if (p.split2) {
       const CallTimer tm = call_timer();
       void *params[] = {&args};
-      const size_t lds1 = (size_t)G * p.Ls * 4;
+      const size_t lds1 = (size_t)G * kSplitMax * 4;
       hipError_t e = hipExtLaunchKernel(reinterpret_cast<const void *>(&k_stream_cdf<E, G, PG>),
                                         dim3(p.B * p.Hkv * p.T), dim3(kThreads), params, lds1, st,
                                         tm.start, nullptr, 0);
@@ -931,9 +1005,10 @@ hipError_t launch_fused_sampled(const Plan &p, const KvView &kv, const void *q, 
     }
     const void *fn = strat ? reinterpret_cast<const void *>(&k_fused_sampled<E, G, PG, true>)
                            : reinterpret_cast<const void *>(&k_fused_sampled<E, G, PG, false>);
-    // stage the group's stratified uniforms in LDS when they are small
-    args.ustage = strat && (size_t)G * p.S <= 4096;
-    const size_t lds = (size_t)fused_sampled_floats(G, p.Ls, p.T, args.ustage ? G * p.S : 0) * 4;
+    // stage the group's uniforms in LDS when they are few
+    const size_t nu = strat ? (size_t)G * p.S : (size_t)G;
+    args.ustage = nu <= (size_t)kUStageMax;
+    const size_t lds = (size_t)fused_sampled_floats(G, kSplitMax, p.T, args.ustage ? (int)nu : 0) * 4;
     return launch_resident(fn, p, args, lds, st);
   });
 }

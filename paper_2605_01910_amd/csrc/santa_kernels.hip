@@ -38,7 +38,7 @@ __global__ __launch_bounds__(kThreads) void k_dense_split(KvView kv, const E *__
   const int start = t * Ls;
   if (start >= L) return;
   const int nrows = min(Ls, L - start);
-  __shared__ float s[G * kSplitMax];
+  __shared__ __attribute__((aligned(16))) float s[G * kSplitMax];
   __shared__ float red[4 * G * kHeadDim];
   __shared__ float mh[G], lh[G];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, slot = tid >> 4, c = tid & 15;
@@ -46,7 +46,7 @@ __global__ __launch_bounds__(kThreads) void k_dense_split(KvView kv, const E *__
 
   const QRegs<E, G> qr = load_q<E, G>(q, b, Hq, kvh, c);
   float mx[G];
-  score_tile<E, G, PAGED, kScoreUnroll>(kv, b, kvh, start, nrows, qr, scale_log2, s, kSplitMax, mx);
+  score_tile<E, G, PAGED, score_unroll<E, G>()>(kv, b, kvh, start, nrows, qr, scale_log2, s, kSplitMax, mx);
   __syncthreads();
   // split max and exponentials e_j = exp2(s_j - m_t), l_t = sum_j e_j
   for (int h = wave; h < G; h += kThreads / 64) {
@@ -143,11 +143,11 @@ __global__ __launch_bounds__(kThreads) void k_score_cdf(KvView kv, const E *__re
   const int start = t * Ls;
   if (start >= L) return;
   const int nrows = min(Ls, L - start);
-  __shared__ float s[G * kSplitMax];
+  __shared__ __attribute__((aligned(16))) float s[G * kSplitMax];
   __shared__ float mh[G];
   const QRegs<E, G> qr = load_q<E, G>(q, b, Hq, kvh, threadIdx.x & 15);
   float mx[G];
-  score_tile<E, G, PAGED, kScoreUnroll>(kv, b, kvh, start, nrows, qr, scale_log2, s, kSplitMax, mx);
+  score_tile<E, G, PAGED, score_unroll<E, G>()>(kv, b, kvh, start, nrows, qr, scale_log2, s, kSplitMax, mx);
   __syncthreads();
   finish_split_cdf<G>(s, mh, nrows, (int64_t)b * Hq + kvh * G, T, t, (int64_t)T * Ls, start,
                       stats, stash);
@@ -228,7 +228,7 @@ __global__ __launch_bounds__(kThreads) void k_sample(
   const int64_t sid = ((int64_t)b * gridDim.y + kvh) * T + t;
 
   __shared__ HeadClaim hc[G];
-  __shared__ float P[G * kSplitMax];  // split CDF; reused as the slot-reduction buffer
+  __shared__ __attribute__((aligned(16))) float P[G * kSplitMax];  // split CDF; reused as the slot-reduction buffer
   __shared__ int cnt[G * kSplitMax];
   __shared__ int list[kSplitMax];
   __shared__ int wave_cnt[4];
@@ -373,7 +373,7 @@ __global__ __launch_bounds__(kThreads) void k_bern_score(KvView kv, KtView kt, i
   const int tid = threadIdx.x;
   const int grp = b * gridDim.y + kvh;
   const int64_t row0 = (int64_t)b * Hq + kvh * G;
-  __shared__ float s[G * kSplitMax];
+  __shared__ __attribute__((aligned(16))) float s[G * kSplitMax];
   __shared__ float wl[G * kHeadDim];
   __shared__ int fl[kHeadDim];
   __shared__ float mh[G];

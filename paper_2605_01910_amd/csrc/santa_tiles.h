@@ -15,6 +15,11 @@ namespace santa {
 template <typename E, int G>
 struct QRegs {
   Chunk<E> h[G];
+  // Makes every register available (the compiler waits for their loads here).
+  __device__ __forceinline__ void require() const {
+#pragma unroll
+    for (int i = 0; i < G; ++i) h[i].require();
+  }
 };
 
 // Quarter k (lanes 4k..4k+3) of a 16-lane row: with G = 4 the query registers
@@ -49,175 +54,230 @@ __device__ __forceinline__ void store_out(uint16_t *p, float x) {
 }
 __device__ __forceinline__ void store_out(float *p, float x) { *p = x; }
 
-// Keys in flight per lane in the score tile (U 128-bit loads per lane).
-#ifndef SANTA_SCORE_UNROLL
-#define SANTA_SCORE_UNROLL 8
-#endif
-constexpr int kScoreUnroll = SANTA_SCORE_UNROLL;
-
-// Running (max, sum of exp2(s - max)) of a stream of scores: adds y with one
-// exp2 (the smaller of the two terms is rescaled).
-__device__ __forceinline__ void stat_push(float &m, float &l, float y) {
-  const float d = y - m;  // +inf while the stream is empty (m = -inf)
-  const float e = fast_exp2(-fabsf(d));
-  l = d > 0.0f ? fmaf(l, e, 1.0f) : l + e;
-  m = fmaxf(m, y);
+// Key rows per lane and batch of the score tile (U 16-byte loads per lane in
+// flight, twice that while a batch is scored): 8 for bf16 with G <= 4, 4 for
+// the wider register sets of fp32 rows or G = 8.
+template <typename E, int G>
+constexpr int score_unroll() {
+  return (sizeof(E) == 2 && G <= 4) ? 8 : 4;
 }
-// Combination of two partial (max, sum) pairs.
-__device__ __forceinline__ void stat_merge(float &m, float &l, float m2, float l2) {
-  const float M = fmaxf(m, m2);
-  const float e1 = m == M ? 1.0f : fast_exp2(m - M);
-  const float e2 = m2 == M ? 1.0f : fast_exp2(m2 - M);
-  l = l * e1 + l2 * e2;
-  m = M;
+
+// Byte offset, from the cache base, of key row row0 (feature 0) of sequence
+// b, KV head kvh, for a row0 that is a multiple of 16 (one page-table entry
+// per 16 rows when pages hold at least 16 keys).  Uniform over the workgroup.
+template <bool PAGED>
+__device__ __forceinline__ int64_t row16_offset(const KvView &kv, int b, int kvh, int row0) {
+  if constexpr (PAGED) {
+    const int page = kv.bt[(int64_t)b * kv.max_pages + (row0 >> kv.ps_log2)];
+    return (int64_t)page * kv.sb + (int64_t)(row0 & ((1 << kv.ps_log2) - 1)) * kv.sn +
+           (int64_t)kvh * kv.sh;
+  } else {
+    return (int64_t)b * kv.sb + (int64_t)row0 * kv.sn + (int64_t)kvh * kv.sh;
+  }
+}
+
+// 16 bytes at byte offset lb from p through a buffer resource (uniform base in
+// scalar registers, one 32-bit lane offset; no range limit is used).
+__device__ __forceinline__ uint4 buffer_load16(const void *p, uint32_t lb) {
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), 0, 0x7fffffff, 0x00020000);
+  const auto v = __builtin_amdgcn_raw_buffer_load_b128(rs, lb, 0, 0);
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
+// Features 8c..8c+7 of key row (row0 + slot); lb = (slot*stride_n + 8c) *
+// sizeof(E) is the lane's byte offset (32 bits; the host bounds the stride).
+template <typename E, bool PAGED>
+__device__ __forceinline__ Chunk<E> load_key_row(const E *base, const KvView &kv, int b, int kvh,
+                                                 int row0, int slot, int c, uint32_t lb) {
+  if constexpr (PAGED) {
+    if (kv.ps_log2 < 4) return Chunk<E>::load(base + row_offset<true>(kv, b, kvh, row0 + slot) + c * 8);
+  }
+  const E *p = base + row16_offset<PAGED>(kv, b, kvh, row0);
+  if constexpr (sizeof(E) == 2) {
+    return Chunk<E>{buffer_load16(p, lb)};
+  } else {
+    const uint4 x = buffer_load16(p, lb), y = buffer_load16(p, lb + 16);
+    return Chunk<E>{make_float4(__uint_as_float(x.x), __uint_as_float(x.y), __uint_as_float(x.z),
+                                __uint_as_float(x.w)),
+                    make_float4(__uint_as_float(y.x), __uint_as_float(y.y), __uint_as_float(y.z),
+                                __uint_as_float(y.w))};
+  }
+}
+
+// Scores of key row j for the G heads from the lane's 8 features in ch (Sec.
+// 2, SDPA equation, the q K^T product), written to s[h*pitch + j] and folded
+// into the running maxima when valid.  G = 4: a reduce-scatter over the 16
+// lanes (5 DPP adds instead of 16) leaves quarter k of the row with the full
+// score of head gray(k), kept in m1; other G: full row sums, kept in mx[h].
+template <typename E, int G>
+__device__ __forceinline__ void score_key(const Chunk<E> &ch, const QRegs<E, G> &qr,
+                                          float scale_log2, int c, int j, bool valid, float *s,
+                                          int pitch, float &m1, float (&mx)[G]) {
+  if constexpr (G == 4) {
+    const float v0 = ch.dot(qr.h[0]), v1 = ch.dot(qr.h[1]);
+    const float v2 = ch.dot(qr.h[2]), v3 = ch.dot(qr.h[3]);
+    const float x0 = v0 + dpp<0x140>(v2);  // row_mirror
+    const float x1 = v1 + dpp<0x140>(v3);
+    float y = x0 + dpp<0x141>(x1);         // row_half_mirror
+    y += dpp<0xB1>(y);
+    y += dpp<0x4E>(y);
+    y *= scale_log2;
+    if (valid) {
+      m1 = fmaxf(m1, y);
+      if ((c & 3) == 0) s[quarter_gray(c) * pitch + j] = y;
+    }
+  } else {
+    float acc[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) acc[h] = row16_sum(ch.dot(qr.h[h])) * scale_log2;
+    if (valid) {
+#pragma unroll
+      for (int h = 0; h < G; ++h) mx[h] = fmaxf(mx[h], acc[h]);
+      if (c == 0) {
+#pragma unroll
+        for (int h = 0; h < G; ++h) s[h * pitch + j] = acc[h];
+      }
+    }
+  }
 }
 
 // Score tile (Sec. 2, SDPA equation, the q K^T product):
-// s[h*pitch + j] = scale_log2 * <q_h, K_{start+j}> for j < nrows.
-// Lane c of each 16-lane row holds features 8c..8c+7 of one key; a wave covers
-// 4 keys per 128-bit load and U loads are in flight per lane.  mx[h] receives
-// this lane's running max of head h's scores and, if STATS, ls[h] the running
-// sum of exp2(s - mx[h]) (G = 4: only the lane's own head, others -inf / 0).
-template <typename E, int G, bool PAGED, int U, bool STATS = false>
+// s[h*pitch + j] = scale_log2 * <q_h, K_{start+j}> for j < nrows (start a
+// multiple of 16).  Lane c of each 16-lane row holds features 8c..8c+7 of one
+// key; a wave covers 4 keys per 128-bit load.  Whole batches of 16*U rows are
+// loaded without predicates and double-buffered (the next batch's U loads per
+// lane are in flight while this batch is scored); a ragged tail of fewer rows
+// is loaded with per-row predicates.  mx[h] receives this lane's running max
+// of head h's scores (G = 4: only the lane's own head, others -inf).
+template <typename E, int G, bool PAGED, int U>
 __device__ __forceinline__ void score_tile(const KvView &kv, int b, int kvh, int start, int nrows,
                                            const QRegs<E, G> &qr, float scale_log2, float *s,
-                                           int pitch, float (&mx)[G], float (&ls)[G]) {
+                                           int pitch, float (&mx)[G]) {
   const int tid = threadIdx.x, slot = tid >> 4, c = tid & 15;
   const E *K = static_cast<const E *>(kv.k);
-  float m1 = -kInf, l1 = 0.0f;  // G == 4: the lane's own head
+  const uint32_t lb = (uint32_t)(((int64_t)slot * kv.sn + c * 8) * (int64_t)sizeof(E));
+  float m1 = -kInf;
 #pragma unroll
-  for (int h = 0; h < G; ++h) {
-    mx[h] = -kInf;
-    ls[h] = 0.0f;
+  for (int h = 0; h < G; ++h) mx[h] = -kInf;
+  constexpr int RB = 16 * U;
+  const int nfull = nrows - nrows % RB;
+  auto load = [&](Chunk<E>(&ch)[U], int base) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      ch[u] = load_key_row<E, PAGED>(K, kv, b, kvh, start + base + u * 16, slot, c, lb);
+  };
+  auto score = [&](const Chunk<E>(&ch)[U], int base) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      score_key<E, G>(ch[u], qr, scale_log2, c, base + u * 16 + slot, true, s, pitch, m1, mx);
+  };
+  // two buffers in a rolled loop whose loads are unconditional (so the
+  // compiler's wait counts leave the other buffer's loads in flight), then at
+  // most two more batches; four batch bodies of code in all
+  Chunk<E> A[U], B[U];
+  if (nfull > 0) load(A, 0);
+  // the query registers are complete before the batches (their loads were
+  // issued first), so the waits below count only key loads
+  qr.require();
+  int base = 0;
+#pragma unroll 1
+  for (; base + 2 * RB < nfull; base += 2 * RB) {
+    load(B, base + RB);
+    score(A, base);
+    load(A, base + 2 * RB);
+    score(B, base + RB);
   }
-  for (int base = 0; base < nrows; base += 16 * U) {
-    Chunk<E> ch[U];
+  if (nfull > 0) {
+    const bool two = base + RB < nfull;
+    if (two) load(B, base + RB);
+    score(A, base);
+    if (two) score(B, base + RB);
+  }
+  Chunk<E>(&cur)[U] = A;
+  if (nfull < nrows) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int j = base + u * 16 + slot;
-      ch[u] = j < nrows ? Chunk<E>::load(K + row_offset<PAGED>(kv, b, kvh, start + j) + c * 8)
-                        : Chunk<E>::zero();
+      const int j = nfull + u * 16 + slot;
+      cur[u] = j < nrows ? load_key_row<E, PAGED>(K, kv, b, kvh, start + nfull + u * 16, slot, c, lb)
+                         : Chunk<E>::zero();
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int j = base + u * 16 + slot;
-      if constexpr (G == 4) {
-        // reduce-scatter over the 16 lanes: 5 DPP adds instead of 16; quarter k
-        // ends with the full score of head gray(k)
-        const float v0 = ch[u].dot(qr.h[0]), v1 = ch[u].dot(qr.h[1]);
-        const float v2 = ch[u].dot(qr.h[2]), v3 = ch[u].dot(qr.h[3]);
-        const float x0 = v0 + dpp<0x140>(v2);   // row_mirror
-        const float x1 = v1 + dpp<0x140>(v3);
-        float y = x0 + dpp<0x141>(x1);          // row_half_mirror
-        y += dpp<0xB1>(y);
-        y += dpp<0x4E>(y);
-        y *= scale_log2;
-        if (j < nrows) {
-          if (STATS) stat_push(m1, l1, y);
-          else m1 = fmaxf(m1, y);
-          if ((c & 3) == 0) s[quarter_gray(c) * pitch + j] = y;
-        }
-      } else {
-        float acc[G];
-#pragma unroll
-        for (int h = 0; h < G; ++h) acc[h] = row16_sum(ch[u].dot(qr.h[h])) * scale_log2;
-        if (j < nrows) {
-#pragma unroll
-          for (int h = 0; h < G; ++h) {
-            if (STATS) stat_push(mx[h], ls[h], acc[h]);
-            else mx[h] = fmaxf(mx[h], acc[h]);
-          }
-          if (c == 0) {
-#pragma unroll
-            for (int h = 0; h < G; ++h) s[h * pitch + j] = acc[h];
-          }
-        }
-      }
+      const int j = nfull + u * 16 + slot;
+      score_key<E, G>(cur[u], qr, scale_log2, c, j, j < nrows, s, pitch, m1, mx);
     }
   }
   if constexpr (G == 4) {
     const int hq = quarter_gray(c);
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      mx[h] = h == hq ? m1 : -kInf;
-      ls[h] = h == hq ? l1 : 0.0f;
-    }
+    for (int h = 0; h < G; ++h) mx[h] = h == hq ? m1 : -kInf;
   }
 }
 
-// Without the running sums.
+// Value tile of the exact decode (Sec. 2, SDPA equation, the weighted sum of
+// V): acc[h][i] = sum_j w[h*pitch + j] * V_{start+j}[8c + i] over the rows j
+// < nrows this lane's 16-lane row slot covers (weights in LDS; start a
+// multiple of 16).  Same batching as score_tile: whole batches of 16*U rows
+// without predicates, double-buffered; a ragged tail with per-row masks.
 template <typename E, int G, bool PAGED, int U>
-__device__ __forceinline__ void score_tile(const KvView &kv, int b, int kvh, int start, int nrows,
-                                           const QRegs<E, G> &qr, float scale_log2, float *s,
-                                           int pitch, float (&mx)[G]) {
-  float ls[G];
-  score_tile<E, G, PAGED, U, false>(kv, b, kvh, start, nrows, qr, scale_log2, s, pitch, mx, ls);
-}
-
-// Split (max, sum of exp2(s - max)) of every head from the score tile's
-// per-lane running pairs (all threads get them in mh[h], lh[h]); tmp holds
-// 8*G floats.
-template <int G>
-__device__ __forceinline__ void block_stats_heads(float (&mx)[G], float (&ls)[G], float *tmp,
-                                                  float *mh, float *lh) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  if constexpr (G == 4) {
-    // the four lanes of a quarter hold the same pair; combine the 4 rows
-    const int hq = quarter_gray(lane & 15);
-    float m = mx[0], l = ls[0];
+__device__ __forceinline__ void value_tile(const KvView &kv, int b, int kvh, int start, int nrows,
+                                           const float *w, int pitch, float (&acc)[G][8]) {
+  const int tid = threadIdx.x, slot = tid >> 4, c = tid & 15;
+  const E *V = static_cast<const E *>(kv.v);
+  const uint32_t lb = (uint32_t)(((int64_t)slot * kv.sn + c * 8) * (int64_t)sizeof(E));
 #pragma unroll
-    for (int h = 1; h < G; ++h) {
-      m = h == hq ? mx[h] : m;
-      l = h == hq ? ls[h] : l;
-    }
-    {
-      const auto pm = __builtin_amdgcn_permlane16_swap(__float_as_uint(m), __float_as_uint(m), false, false);
-      const auto pl = __builtin_amdgcn_permlane16_swap(__float_as_uint(l), __float_as_uint(l), false, false);
-      m = __uint_as_float(pm[0]); l = __uint_as_float(pl[0]);
-      stat_merge(m, l, __uint_as_float(pm[1]), __uint_as_float(pl[1]));
-    }
-    {
-      const auto pm = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false, false);
-      const auto pl = __builtin_amdgcn_permlane32_swap(__float_as_uint(l), __float_as_uint(l), false, false);
-      m = __uint_as_float(pm[0]); l = __uint_as_float(pl[0]);
-      stat_merge(m, l, __uint_as_float(pm[1]), __uint_as_float(pl[1]));
-    }
-    if (lane < 16 && (lane & 3) == 0) {
-      tmp[(wave * G + hq) * 2] = m;
-      tmp[(wave * G + hq) * 2 + 1] = l;
-    }
-  } else {
+  for (int h = 0; h < G; ++h)
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      // lanes of a 16-lane row hold the same pair; combine the 4 rows
-      float m = mx[h], l = ls[h];
-      {
-        const auto pm = __builtin_amdgcn_permlane16_swap(__float_as_uint(m), __float_as_uint(m), false, false);
-        const auto pl = __builtin_amdgcn_permlane16_swap(__float_as_uint(l), __float_as_uint(l), false, false);
-        m = __uint_as_float(pm[0]); l = __uint_as_float(pl[0]);
-        stat_merge(m, l, __uint_as_float(pm[1]), __uint_as_float(pl[1]));
-      }
-      {
-        const auto pm = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false, false);
-        const auto pl = __builtin_amdgcn_permlane32_swap(__float_as_uint(l), __float_as_uint(l), false, false);
-        m = __uint_as_float(pm[0]); l = __uint_as_float(pl[0]);
-        stat_merge(m, l, __uint_as_float(pm[1]), __uint_as_float(pl[1]));
-      }
-      if (lane == 0) {
-        tmp[(wave * G + h) * 2] = m;
-        tmp[(wave * G + h) * 2 + 1] = l;
+    for (int i = 0; i < 8; ++i) acc[h][i] = 0.0f;
+  constexpr int RB = 16 * U;
+  const int nfull = nrows - nrows % RB;
+  auto load = [&](Chunk<E>(&ch)[U], int base) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      ch[u] = load_key_row<E, PAGED>(V, kv, b, kvh, start + base + u * 16, slot, c, lb);
+  };
+  auto add = [&](const Chunk<E>(&ch)[U], int base) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = base + u * 16 + slot;
+      float f[8];
+      ch[u].to_float(f);
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        const float wr = w[h * pitch + j];  // j < pitch: in bounds, stale past nrows
+        const float wt = j < nrows ? wr : 0.0f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[h][i] = fmaf(wt, f[i], acc[h][i]);
       }
     }
+  };
+  Chunk<E> A[U], B[U];
+  if (nfull > 0) load(A, 0);
+  int base = 0;
+#pragma unroll 1
+  for (; base + 2 * RB < nfull; base += 2 * RB) {
+    load(B, base + RB);
+    add(A, base);
+    load(A, base + 2 * RB);
+    add(B, base + RB);
   }
-  __syncthreads();
-  if (tid < G) {
-    float m = tmp[tid * 2], l = tmp[tid * 2 + 1];
-#pragma unroll
-    for (int w = 1; w < 4; ++w) stat_merge(m, l, tmp[(w * G + tid) * 2], tmp[(w * G + tid) * 2 + 1]);
-    mh[tid] = m;
-    lh[tid] = l;
+  if (nfull > 0) {
+    const bool two = base + RB < nfull;
+    if (two) load(B, base + RB);
+    add(A, base);
+    if (two) add(B, base + RB);
   }
-  __syncthreads();
+  Chunk<E>(&cur)[U] = A;
+  if (nfull < nrows) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = nfull + u * 16 + slot;
+      cur[u] = j < nrows ? load_key_row<E, PAGED>(V, kv, b, kvh, start + nfull + u * 16, slot, c, lb)
+                         : Chunk<E>::zero();
+    }
+    add(cur, nfull);
+  }
 }
 
 // Split max of every head from the score tile's per-lane maxima (all threads
@@ -237,21 +297,40 @@ __device__ __forceinline__ void block_max_heads(float (&mx)[G], float *tmp, floa
 
 // Split-local CDF of one head, computed by one wave (Sec. 2.1, "Construction":
 // F is the running sum of the attention weights).  On return s[j] holds
-// P_j = sum_{i<=j} exp2(s_i - m) for j < nrows, where m = max_j s_j is returned.
-// Each lane owns a contiguous run of keys and sums it sequentially; the runs are
-// joined by a wave prefix sum.
+// P_j = sum_{i<=j} exp2(s_i - m) for j < nrows (nrows <= kSplitMax; s has room
+// for kSplitMax values).  Lane l owns keys 16l..16l+15 and sums them
+// sequentially (four 16-byte LDS reads, no branches); the 64 run totals are
+// joined by one wave prefix sum, made non-decreasing over the lanes by a prefix
+// max, and every value of a run is capped at its lane's inclusive prefix, so P
+// never decreases.  The summation order is fixed: equal inputs give
+// bitwise-equal CDFs.
 __device__ __forceinline__ void wave_split_cdf_m(float *s, int nrows, int lane, float m) {
-  // rows of 64 keys: lane l holds key 64*i + l of row i; each row is a DPP
-  // prefix sum, offset by the previous row's last value (carried exactly, so
-  // the CDF never decreases from one row to the next)
-  float carry = 0.0f;
-  for (int j0 = 0; j0 < nrows; j0 += 64) {
-    const int j = j0 + lane;
-    const float x = s[min(j, nrows - 1)];
-    const float e = j < nrows ? fast_exp2(x - m) : 0.0f;
-    const float p = carry + wave_incl_scan(e);
-    if (j < nrows) s[j] = p;
-    carry = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(p), 63));
+  constexpr int CH = kSplitMax / 64;
+  const int j0 = lane * CH;
+  float x[CH];
+#pragma unroll
+  for (int i = 0; i < CH / 4; ++i) {
+    const float4 v = reinterpret_cast<const float4 *>(s + j0)[i];
+    x[4 * i] = v.x;
+    x[4 * i + 1] = v.y;
+    x[4 * i + 2] = v.z;
+    x[4 * i + 3] = v.w;
+  }
+  float acc = 0.0f;
+#pragma unroll
+  for (int i = 0; i < CH; ++i) {
+    const float e = fast_exp2(x[i] - m);
+    acc += (j0 + i < nrows) ? e : 0.0f;  // keys past the split hold stale values
+    x[i] = acc;
+  }
+  const float incl = wave_incl_max(wave_incl_scan(acc));
+  const float base = wave_prev(0.0f, incl);
+  if (j0 < nrows) {
+#pragma unroll
+    for (int i = 0; i < CH / 4; ++i)
+      reinterpret_cast<float4 *>(s + j0)[i] =
+          make_float4(fminf(base + x[4 * i], incl), fminf(base + x[4 * i + 1], incl),
+                      fminf(base + x[4 * i + 2], incl), fminf(base + x[4 * i + 3], incl));
   }
 }
 
