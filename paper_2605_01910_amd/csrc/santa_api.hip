@@ -51,17 +51,15 @@ int choose_split(int64_t rows, int64_t n_k) {
 // tests of both paths; a workspace must be sized under the same settings):
 //   SANTA_VARIANT=multi  use the multi-kernel path instead of the fused launch
 //   SANTA_SPLITS=T       splits per row of the fused path
-//   SANTA_XCD=0          do not place a row's splits on one XCD
 struct Tuning {
-  int fused, splits, xcd;
+  int fused, splits;
   int sampled_path;  // 0: by size, 1: one persistent launch, 2: two launches
 };
 
 Tuning tuning() {
-  Tuning r{1, 0, 1, 0};
+  Tuning r{1, 0, 0};
   if (const char *v = std::getenv("SANTA_VARIANT")) r.fused = std::string(v) != "multi";
   if (const char *v = std::getenv("SANTA_SPLITS")) r.splits = std::atoi(v);
-  if (const char *v = std::getenv("SANTA_XCD")) r.xcd = std::atoi(v) != 0;
   if (const char *v = std::getenv("SANTA_SAMPLED")) {
     const std::string s(v);
     r.sampled_path = s == "fused" ? 1 : s == "split" ? 2 : 0;
@@ -143,10 +141,13 @@ santa::Plan make_plan(const santa_shape_t *sh, const santa_kv_t *kv, int S, int 
   const Tuning tune = tuning();
   const int Tf = fused_splits((int64_t)p.B * p.Hkv, p.n_k);
   if (kind != SANTA_KIND_BERNOULLI && tune.fused && Tf <= santa::kMaxSplits) {
-    // fused layout: counters first (they must start at zero: santa_workspace_init)
+    // fused layout: counters first (they must start at zero: santa_workspace_init);
+    // every fused path keeps them at the same offsets, so calls of different
+    // kinds and shapes can share one workspace
     p.fused = 1;
-    p.xcd = tune.xcd;
     p.T = Tf;
+    p.off_err = take(4);
+    p.off_sync = take((size_t)p.B * p.Hkv * santa::kSyncStride * 4);
     // rows use ceil(L_b / T) keys per split rounded up to 64; Ls is the longest
     p.Ls = (int)(((p.n_k + p.T - 1) / p.T + 63) & ~63);
     const bool sampled = kind != SANTA_KIND_DENSE;
@@ -157,11 +158,9 @@ santa::Plan make_plan(const santa_shape_t *sh, const santa_kv_t *kv, int S, int 
     if (p.split2) {
       p.npitch = ((int64_t)p.n_k + 63) & ~int64_t(63);
       p.off_stats = take(rows * p.T * 8);
-      p.off_stash = take(rows * (size_t)p.npitch * 4);
+      p.off_stash = take(rows * (size_t)p.npitch * 2);   // 16-bit in-block CDF
       p.off_coarse = take(rows * (size_t)(p.npitch / 32) * 4);
     } else {
-      p.off_err = take(4);
-      p.off_sync = take((size_t)p.B * p.Hkv * santa::kSyncStride * 4);
       p.off_stats = take(rows * p.T * 8);
       p.off_part = take((size_t)p.B * p.Hkv * p.T * p.G * D * 4);
     }

@@ -2,36 +2,34 @@
 //
 // Every (batch b, KV head k) row is cut into Tb <= T splits of Ls keys (Ls =
 // ceil(L_b / T) rounded up to 64); split t of a row is one work item of one
-// 256-thread workgroup.
+// 256-thread workgroup.  The persistent kernels hold R whole rows per round
+// (R*T workgroups, all resident) and loop over rounds; a row's splits run on
+// one XCD when R is a multiple of 8 (map_item).
 //
-// Sampled step, small batches (one persistent launch, k_fused_sampled).  The
-// grid holds R whole rows per round (R*T workgroups, all resident) and loops
-// over rounds.  Per work item:
-//   1. stream the split's keys; scores of the G heads in LDS; each lane keeps a
-//      running (max, sum of exp2) per head, so the split's (m_t, l_t) is
-//      published as soon as the keys are in;
-//   2. while the other splits arrive, the split-local CDF
-//      P_j = sum_{i<=j} exp2(s_i - m_t) is built in LDS (Sec. 2.1: F is the
-//      running sum of the attention weights); then wait until every split of
-//      the row has published (row counter).  P_last equals l_t up to rounding;
-//      a threshold that falls between a_t P_last and Off_{t+1} - Off_t maps to
-//      the split's last key (the clamp below);
+// Sampled step, small batches (one launch, k_fused_sampled).  Per work item:
+//   1. stream the split's keys (double-buffered 16-byte loads); the scores of
+//      the G heads go to LDS and each lane keeps its running max;
+//   2. the split-local CDF P_j = sum_{i<=j} exp2(s_i - m_t) is built in LDS
+//      (Sec. 2.1: F is the running sum of the attention weights) and the split
+//      publishes (m_t, l_t = P_last); then it arrives on the row counter and
+//      waits until every split of the row has published (the last arrival does
+//      not wait);
 //   3. global offsets Off_t = sum_{t'<t} a_t' l_t' with a_t = exp2(m_t - m*)
 //      and the total Z, identical in every split; threshold tau_r = ((r + u)/S) Z
 //      (u per row, or u_r) is claimed by the split with Off_t <= tau_r <
-//      Off_{t+1}; tau_r is non-decreasing in r, so the claimed r form one range,
-//      found by binary search; each claimed tau_r maps to the key
-//      #{j : a_t P_j <= tau_r - Off_t} (the CDF interval holding it, App. A),
-//      clamped to the split; the union of chosen keys over the group's heads
-//      is gathered once per key and the G x 128 partial sums are published;
+//      Off_{t+1}; each claimed tau_r maps to the key #{j : a_t P_j <= tau_r -
+//      Off_t} (the CDF interval holding it, App. A), clamped to the split; the
+//      union of chosen keys over the group's heads is gathered once per key and
+//      the G x 128 partial sums are published;
 //   4. take an arrival rank; the last G arrivals each merge one head:
 //      O_h = (1/S) sum_t o_t in split order.
 // Sampled step, large batches (two launches): k_stream_cdf streams every work
-// item and writes the split-local CDF of every key (the stash), the CDF at
-// every 32-key block end and the split statistics; then k_value_heads, one
-// workgroup per query head, finds each threshold's split from the offsets,
-// its 32-key block from the block ends and the key inside the block from the
-// stash, and gathers the chosen V rows once per distinct key.
+// item and writes the split-local CDF at every 32-key block end (fp32), each
+// key's CDF within its block as a 16-bit fraction of the block's mass (the
+// stash) and the split statistics; then k_value_heads, one workgroup per
+// query head, finds each threshold's split from the offsets, its 32-key block
+// from the block ends and the key inside the block from the stash, and
+// gathers the chosen V rows once per distinct key.
 // Dense step (k_fused_dense): the split's exact softmax-weighted V sum o_t with
 // (m_t, l_t); the last G arrivals merge O = sum_t a_t o_t / sum_t a_t l_t.
 //
@@ -39,12 +37,8 @@
 // counters) is written and read with relaxed agent-scope atomics, which are
 // coherent per access across the XCDs' L2s; a writer waits for its stores to
 // complete before it arrives.  No cache-wide write-back or invalidation is
-// issued.  Between the two launches of the large-batch path the kernel
+// issued.  Between the two launches of the two-launch path the kernel
 // boundary orders the accesses and plain loads and stores are used.
-//
-// Each row's workgroups are placed on one XCD when the round holds a multiple
-// of 8 rows (workgroups are dispatched round-robin over the 8 XCDs), so the
-// row's counter and exchange traffic stays in one L2.
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
@@ -64,7 +58,8 @@ struct FusedArgs {
   int32_t *idx_out;
   float2 *stats;  // [B*Hq][T]          (m_t, l_t) per head and split
   float *part;    // [B*Hkv][T][G*128]  split partial outputs
-  float *stash;   // [B*Hq][npitch]     two-launch path: split-local CDF of every key
+  uint16_t *qstash;  // [B*Hq][npitch]  two-launch path: every key's CDF within its
+                     //                 32-key block, in units of 2^-16 of the block's mass
   float *coarse;  // [B*Hq][npitch/32]  two-launch path: the CDF at every 32-key block end
   unsigned long long *sync;  // [B*Hkv][kSyncStride/2] arrival counter, counter base
   int *err;       // [1]                set if a wait gave up
@@ -72,7 +67,6 @@ struct FusedArgs {
   int ustage;     // the group's uniforms (G*S stratified, G systematic) staged in LDS if 1
   int64_t npitch; // stash floats per head row (n_k rounded up to 64)
   float invS, scale_log2;
-  int xcd;
 };
 
 constexpr int kSpinLimit = 1 << 22;
@@ -122,9 +116,11 @@ __device__ __forceinline__ void split_geometry(int L, int T, int &Ls, int &Tb) {
   Tb = (L + Ls - 1) / Ls;
 }
 
-// Work item of workgroup w within a round: row rho (0..R-1), split t.
-__device__ __forceinline__ void map_item(int w, int T, int R, int xcd, int &rho, int &t) {
-  if (xcd && (R & 7) == 0) {
+// Work item of workgroup w within a round of R rows: row rho, split t.  When R
+// is a multiple of 8, the splits of a row all run on one XCD (workgroups are
+// dispatched round-robin over the 8 XCDs: w -> XCD w % 8).
+__device__ __forceinline__ void map_item(int w, int T, int R, int &rho, int &t) {
+  if ((R & 7) == 0) {
     const int x = w & 7, l = w >> 3;
     rho = x + 8 * (l / T);
     t = l % T;
@@ -456,12 +452,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nrk = a.B * a.Hkv;
-  const int R = gridDim.x / T;
+  const int R = gridDim.x / T;  // rows per round
   int rho, t;
-  map_item(blockIdx.x, T, R, a.xcd, rho, t);
+  map_item(blockIdx.x, T, R, rho, t);
   E *out = static_cast<E *>(a.out);
 
   for (int rbase = 0; rbase < nrk; rbase += R) {
+    __builtin_amdgcn_s_setprio(0);
     const int rowkv = rbase + rho;
     if (rowkv >= nrk) break;
     const int b = rowkv / a.Hkv, kvh = rowkv % a.Hkv;
@@ -503,6 +500,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     float mx[G];
     score_tile<E, G, PAGED, score_unroll<E, G>()>(a.kv, b, kvh, start, nrows, qr, a.scale_log2, P,
                                                   pitch, mx);
+    // from here on the split is on its row's critical path: its waves issue
+    // ahead of waves that are still streaming keys
+    __builtin_amdgcn_s_setprio(3);
     block_max_heads<G>(mx, mtmp, mh);
 
     // 2. split-local CDF of head h by wave h; the split's (m_t, l_t = P_last)
@@ -589,15 +589,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   __shared__ float mh[G], lh[G], mtmp[4 * G], den;
   __shared__ int rank_lds;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, slot = tid >> 4, c = tid & 15;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, c = tid & 15;
   const int nrk = a.B * a.Hkv, T = a.T;
-  const int R = gridDim.x / T;
+  const int R = gridDim.x / T;  // rows per round
   int rho, t;
-  map_item(blockIdx.x, T, R, a.xcd, rho, t);
+  map_item(blockIdx.x, T, R, rho, t);
   E *out = static_cast<E *>(a.out);
-  const E *V = static_cast<const E *>(a.kv.v);
 
   for (int rbase = 0; rbase < nrk; rbase += R) {
+    __builtin_amdgcn_s_setprio(0);
     const int rowkv = rbase + rho;
     if (rowkv >= nrk) break;
     const int b = rowkv / a.Hkv, kvh = rowkv % a.Hkv;
@@ -636,6 +636,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     __syncthreads();
     float acc[G][8];
     value_tile<E, G, PAGED, score_unroll<E, G>()>(a.kv, b, kvh, start, nrows, s, pitch, acc);
+    __builtin_amdgcn_s_setprio(3);  // the merge chain issues ahead of streaming waves
     reduce_slots<G>(acc, red);
     float2 *mypart = reinterpret_cast<float2 *>(part_row + (int64_t)t * G * kHeadDim);
     for (int o2 = tid; o2 < G * kHeadDim / 2; o2 += kThreads) {
@@ -715,13 +716,28 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(sizeof
   for (int h = wave; h < G; h += kThreads / 64) wave_split_cdf_m(P + h * pitch, nrows, lane, mh[h]);
   __syncthreads();
   if (tid < G) a.stats[(row0 + tid) * T + t] = make_float2(mh[tid], P[tid * pitch + nrows - 1]);
-  // stash, in pairs of keys; an odd last split also writes the (unused) slot at L
-  const int half = (nrows + 1) >> 1;
-  for (int i = tid; i < G * half; i += kThreads) {
-    const int h = i / half, j = 2 * (i - h * half);
+  // stash: 8 keys per 16-byte store; key j of 32-key block k holds
+  // round(65535 (P_j - P_{32k-1}) / (P_{block end} - P_{32k-1})) (P_{-1} = 0),
+  // non-decreasing in j; every block is written whole, keys past the split
+  // holding 65535 (the last split of a row ends within the row's stash pitch)
+  const int q8 = ((nrows + kBlock - 1) / kBlock) * (kBlock / 8);
+  for (int i = tid; i < G * q8; i += kThreads) {
+    const int h = i / q8, j = 8 * (i - h * q8);
     const float *ph = P + h * pitch;
-    *reinterpret_cast<float2 *>(a.stash + (row0 + h) * a.npitch + start + j) =
-        make_float2(ph[j], j + 1 < nrows ? ph[j + 1] : ph[j]);
+    const int k0 = j & ~(kBlock - 1);
+    const float lo = k0 ? ph[k0 - 1] : 0.0f;
+    const float hi = ph[min(k0 + kBlock - 1, nrows - 1)];
+    const float sc = hi > lo ? 65535.0f / (hi - lo) : 0.0f;
+    uint32_t w[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int j0 = j + 2 * e, j1 = j0 + 1;
+      const uint32_t q0 = j0 < nrows ? (uint32_t)fminf(fmaf(ph[j0] - lo, sc, 0.5f), 65535.0f) : 65535u;
+      const uint32_t q1 = j1 < nrows ? (uint32_t)fminf(fmaf(ph[min(j1, nrows - 1)] - lo, sc, 0.5f), 65535.0f) : 65535u;
+      w[e] = q0 | (q1 << 16);
+    }
+    *reinterpret_cast<uint4 *>(a.qstash + (row0 + h) * a.npitch + start + j) =
+        make_uint4(w[0], w[1], w[2], w[3]);
   }
   // block ends, in pairs (start / 32 is even); an odd last count also writes
   // the (unused) slot after the row's last block
@@ -739,12 +755,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(sizeof
 // Inverse CDF of one threshold (global units) for one query head: split
 // t = #{t' in [1,Tb) : off[t'] <= tau}; inside it the key #{j : al_t P_j <=
 // tau - off[t]} over the split's CDF, clamped to the split.  Two levels: the
-// number of whole 32-key blocks below the threshold, from the block-end values
-// cl[] in LDS, then the count inside the next block, from the stash row Pst.
-// Both are exact counts over a non-decreasing sequence, so they add up to the
-// plain count.  Returns the logical key position.
-__device__ __forceinline__ int invert_threshold(const float *Pst, const float *cl, const float *off,
-                                                const float *al, int Tb, int Ls, int L, float tau) {
+// number kb of whole 32-key blocks below the threshold, from the block-end
+// values cl[] in LDS (exact), then the count inside block kb from the 16-bit
+// stash row Qst: the threshold's fraction f of the block's mass against each
+// key's stored fraction.  The second level can differ from the exact count only
+// where the threshold lies within 2^-17 of the block's mass of a key boundary.
+// Returns the logical key position.
+__device__ __forceinline__ int invert_threshold(const uint16_t *Qst, const float *cl,
+                                                const float *off, const float *al, int Tb, int Ls,
+                                                int L, float tau) {
   int t = 0;
   for (int step = 1 << (31 - __clz(Tb)); step > 0; step >>= 1) {
     const int nt = t + step;
@@ -765,19 +784,25 @@ __device__ __forceinline__ int invert_threshold(const float *Pst, const float *c
     pos = nr;
   } else {
     const int j0 = kb * kBlock, nin = min(kBlock, nr - j0);
-    const float4 *Pb = reinterpret_cast<const float4 *>(Pst + st + j0);
-    float4 v[kBlock / 4];
+    const float alo = kb ? a * ce[kb - 1] : 0.0f, ahi = a * ce[kb];
+    const float fq = (x - alo) / (ahi - alo) * 65535.0f;  // a*lo <= x < a*hi
+    const uint4 *Qb = reinterpret_cast<const uint4 *>(Qst + st + j0);
+    uint4 v[kBlock / 8];
 #pragma unroll
-    for (int i = 0; i < kBlock / 4; ++i) v[i] = Pb[i];
+    for (int i = 0; i < kBlock / 8; ++i) v[i] = Qb[i];
     int c = 0;
 #pragma unroll
-    for (int i = 0; i < kBlock / 4; ++i) {
-      c += (4 * i < nin && a * v[i].x <= x) ? 1 : 0;
-      c += (4 * i + 1 < nin && a * v[i].y <= x) ? 1 : 0;
-      c += (4 * i + 2 < nin && a * v[i].z <= x) ? 1 : 0;
-      c += (4 * i + 3 < nin && a * v[i].w <= x) ? 1 : 0;
+    for (int i = 0; i < kBlock / 8; ++i) {
+      const uint32_t w[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        c += (float)(w[e] & 0xffffu) <= fq ? 1 : 0;
+        c += (float)(w[e] >> 16) <= fq ? 1 : 0;
+      }
     }
-    pos = j0 + c;
+    // keys past the split hold 65535 and the block's last key is above the
+    // threshold, so at most nin - 1 keys count
+    pos = j0 + min(c, nin - 1);
   }
   return st + min(pos, nr - 1);
 }
@@ -819,7 +844,7 @@ __global__ __launch_bounds__(kThreads) void k_value_heads(FusedArgs a, int G) {
   if (wave == 0) head_offsets_wave<false>(a.stats + rowq * a.T, Tb, lane, off, al);
   __syncthreads();
   const float Z = off[Tb];
-  const float *Pst = a.stash + rowq * a.npitch;
+  const uint16_t *Qst = a.qstash + rowq * a.npitch;
   const E *V = static_cast<const E *>(a.kv.v);
 
   float acc[8];
@@ -832,7 +857,7 @@ __global__ __launch_bounds__(kThreads) void k_value_heads(FusedArgs a, int G) {
     int key = 0;
     if (tid < n) {
       const float ur = STRAT ? a.u[rowq * a.S + r] : u0;
-      key = invert_threshold(Pst, cl, off, al, Tb, Ls, L, threshold(r, ur, a.invS, Z));
+      key = invert_threshold(Qst, cl, off, al, Tb, Ls, L, threshold(r, ur, a.invS, Z));
       keys[tid] = key;
       if (a.idx_out) a.idx_out[rowq * a.S + r] = key;
     }
@@ -946,7 +971,7 @@ FusedArgs make_args(const Plan &p, const KvView &kv, const void *q, void *out, f
   a.out = out;
   a.stats = reinterpret_cast<float2 *>(ws + p.off_stats);
   a.part = p.off_part ? reinterpret_cast<float *>(ws + p.off_part) : nullptr;
-  a.stash = p.off_stash ? reinterpret_cast<float *>(ws + p.off_stash) : nullptr;
+  a.qstash = p.off_stash ? reinterpret_cast<uint16_t *>(ws + p.off_stash) : nullptr;
   a.coarse = p.off_coarse ? reinterpret_cast<float *>(ws + p.off_coarse) : nullptr;
   a.sync = p.off_sync ? reinterpret_cast<unsigned long long *>(ws + p.off_sync) : nullptr;
   a.err = reinterpret_cast<int *>(ws + p.off_err);
@@ -958,7 +983,6 @@ FusedArgs make_args(const Plan &p, const KvView &kv, const void *q, void *out, f
   a.npitch = p.npitch;
   a.invS = p.S ? 1.0f / (float)p.S : 0.0f;
   a.scale_log2 = scale_log2;
-  a.xcd = p.xcd;
   return a;
 }
 

@@ -27,13 +27,13 @@ struct Plan {
   int S;        // samples per row (0 for dense)
   int kind;     // santa_kind_t
   int fused;    // 1: single persistent launch (per-row split lengths), 0: multi-kernel
-  int xcd;      // fused: place each row's splits on one XCD
   int split2;   // fused sampled: 1 = two launches (stream + CDF stash, then one
                 // workgroup per query head), 0 = one persistent launch
-  int64_t npitch;  // two-launch sampled: stash floats per query head (n_k rounded up to 64)
+  int64_t npitch;  // two-launch sampled: stash entries per query head (n_k rounded up to 64)
   // workspace carve-up (byte offsets, 256-aligned)
   size_t off_stats;  // float2 [B*Hq*T]     per-split (max, sum) in log2 units
-  size_t off_stash;  // float  [B*Hq*T*Ls] (fused: [B*Hq*npitch]) split-local CDF of each row
+  size_t off_stash;  // float  [B*Hq*T*Ls] split-local CDF of each row (multi-kernel);
+                     // uint16 [B*Hq*npitch] in-block CDF fraction of each key (two launches)
   size_t off_coarse; // float  [B*Hq*npitch/32] fused: CDF at every 32-key block end
   size_t off_offs;   // float  [B*Hq*(T+1)] global split offsets of the CDF
   size_t off_alpha;  // float  [B*Hq*T]     per-split rescale exp2(m_t - m*)

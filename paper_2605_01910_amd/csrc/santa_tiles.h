@@ -285,10 +285,21 @@ __device__ __forceinline__ void value_tile(const KvView &kv, int b, int kvh, int
 template <int G>
 __device__ __forceinline__ void block_max_heads(float (&mx)[G], float *tmp, float *mh) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if constexpr (G == 4) {
+    // score_tile leaves only the lane's own head finite: combine the 4 lanes
+    // of a quarter, then the 4 rows of the wave (quarter k of every row holds
+    // head gray(k))
+    float m = fmaxf(fmaxf(mx[0], mx[1]), fmaxf(mx[2], mx[3]));
+    m = fmaxf(m, dpp<0xB1>(m));
+    m = fmaxf(m, dpp<0x4E>(m));
+    m = xor32_max(xor16_max(m));
+    if (lane < 16 && (lane & 3) == 0) tmp[wave * G + quarter_gray(lane)] = m;
+  } else {
 #pragma unroll
-  for (int h = 0; h < G; ++h) {
-    const float m = wave_max(mx[h]);
-    if (lane == 0) tmp[wave * G + h] = m;
+    for (int h = 0; h < G; ++h) {
+      const float m = wave_max(mx[h]);
+      if (lane == 0) tmp[wave * G + h] = m;
+    }
   }
   __syncthreads();
   if (tid < G) mh[tid] = fmaxf(fmaxf(tmp[tid], tmp[G + tid]), fmaxf(tmp[2 * G + tid], tmp[3 * G + tid]));

@@ -148,13 +148,12 @@ def test_multi_kernel_variant_parity(case, monkeypatch):
         log(f"  {check_sampled(w, out, idx, kind)}")
 
 
-@pytest.mark.parametrize("splits,xcd", [(16, "1"), (64, "0"), (200, "1")])
-def test_fused_split_counts(splits, xcd, monkeypatch):
-    """Fused path at other split counts, with and without XCD placement."""
+@pytest.mark.parametrize("splits", [16, 64, 200])
+def test_fused_split_counts(splits, monkeypatch):
+    """Fused path at other split counts."""
     monkeypatch.setenv("SANTA_SPLITS", str(splits))
-    monkeypatch.setenv("SANTA_XCD", xcd)
     w = make_workload(2, B=3, n=5000, kind="stratified", S=128, ctx_len=[5000, 2222, 17], seed=52)
-    log(f"[fused splits={splits} xcd={xcd}]")
+    log(f"[fused splits={splits}]")
     out, idx, _ = run(w)
     check_sampled(w, out, idx)
     d, _, _ = run(w, "dense")
@@ -194,3 +193,47 @@ def test_one_launch_sampled_parity(case, monkeypatch):
     w = make_workload(cfg, seed=24, kind=kind, **over)
     out, idx, _ = run(w, kind)
     log(f"  {check_sampled(w, out, idx, kind)}")
+
+
+def test_one_launch_many_rounds(monkeypatch):
+    """One launch over far more rows than one resident round holds: every
+    workgroup handles a split of several rows, rows have ragged lengths (one
+    empty), and three calls in a row reuse the row counters."""
+    from paper_2605_01910_amd import santa as S
+    monkeypatch.setenv("SANTA_SAMPLED", "fused")
+    lens = [(37 * i * i + 11 * i) % 9000 for i in range(24)]
+    lens[3] = 0
+    lens[7] = 9000
+    w = make_workload(3, B=24, n=9000, kind="systematic", S=64, ctx_len=lens, seed=54)
+    dw = DeviceWorkload(w)
+    ws = S.alloc_workspace(dw.shape, dw.kv, w.S, S.SANTA_KIND_SYSTEMATIC)
+    log(f"[rounds] B={w.B} n={w.n_max} rows={w.B * w.Hkv}")
+    for _ in range(3):
+        out, idx, _ = run(w, dw=dw, ws=ws)
+        check_sampled(w, out, idx)
+        d, _, _ = run(w, "dense", dw=dw, ws=ws)
+        check_dense(w, d)
+    assert int(ws[:4].view(torch.int32).item()) == 0
+
+
+def test_workspace_shared_by_both_sampled_paths(monkeypatch):
+    """The counters keep their place in every fused layout: one workspace
+    serves the one-launch path, the two-launch path and the dense step in any
+    order."""
+    from paper_2605_01910_amd import santa as S
+    w = make_workload(2, B=4, n=3000, kind="stratified", S=128, seed=55)
+    dw = DeviceWorkload(w)
+    spaces = []
+    for path in ("fused", "split"):
+        monkeypatch.setenv("SANTA_SAMPLED", path)
+        spaces.append(S.alloc_workspace(dw.shape, dw.kv, w.S, S.SANTA_KIND_STRATIFIED))
+    ws = max(spaces, key=lambda x: x.numel())
+    log("[workspace] fused, split, dense, fused")
+    for path in ("fused", "split", "dense", "fused"):
+        if path == "dense":
+            d, _, _ = run(w, "dense", dw=dw, ws=ws)
+            check_dense(w, d)
+            continue
+        monkeypatch.setenv("SANTA_SAMPLED", path)
+        out, idx, _ = run(w, dw=dw, ws=ws)
+        check_sampled(w, out, idx)
