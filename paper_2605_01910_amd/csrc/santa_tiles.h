@@ -62,13 +62,39 @@ constexpr int score_unroll() {
   return (sizeof(E) == 2 && G <= 4) ? 8 : 4;
 }
 
+// Block-table entries of the pages one split covers, one per lane: lane l of
+// every wave holds the entry of page p0 + l.  They are loaded once per split,
+// so the key stream does not wait on a table lookup every 16 rows.  A split
+// of at most kSplitMax keys starting at a multiple of 16 spans at most 64
+// pages when pages hold at least 16 keys (smaller pages are addressed per
+// row and use no window).
+struct PageWin {
+  int p0, entry;
+};
+
+template <bool PAGED>
+__device__ __forceinline__ PageWin page_window(const KvView &kv, int b, int start, int nrows) {
+  PageWin w{0, 0};
+  if constexpr (PAGED) {
+    if (kv.ps_log2 >= 4 && nrows > 0) {
+      const int lane = threadIdx.x & 63;
+      w.p0 = start >> kv.ps_log2;
+      const int np = ((start + nrows - 1) >> kv.ps_log2) - w.p0 + 1;
+      w.entry = lane < np ? kv.bt[(int64_t)b * kv.max_pages + w.p0 + lane] : 0;
+    }
+  }
+  return w;
+}
+
 // Byte offset, from the cache base, of key row row0 (feature 0) of sequence
 // b, KV head kvh, for a row0 that is a multiple of 16 (one page-table entry
-// per 16 rows when pages hold at least 16 keys).  Uniform over the workgroup.
+// per 16 rows when pages hold at least 16 keys, taken from the split's page
+// window).  Uniform over the workgroup.
 template <bool PAGED>
-__device__ __forceinline__ int64_t row16_offset(const KvView &kv, int b, int kvh, int row0) {
+__device__ __forceinline__ int64_t row16_offset(const KvView &kv, const PageWin &pw, int b, int kvh,
+                                                int row0) {
   if constexpr (PAGED) {
-    const int page = kv.bt[(int64_t)b * kv.max_pages + (row0 >> kv.ps_log2)];
+    const int page = __builtin_amdgcn_readlane(pw.entry, (row0 >> kv.ps_log2) - pw.p0);
     return (int64_t)page * kv.sb + (int64_t)(row0 & ((1 << kv.ps_log2) - 1)) * kv.sn +
            (int64_t)kvh * kv.sh;
   } else {
@@ -88,12 +114,13 @@ __device__ __forceinline__ uint4 buffer_load16(const void *p, uint32_t lb) {
 // Features 8c..8c+7 of key row (row0 + slot); lb = (slot*stride_n + 8c) *
 // sizeof(E) is the lane's byte offset (32 bits; the host bounds the stride).
 template <typename E, bool PAGED>
-__device__ __forceinline__ Chunk<E> load_key_row(const E *base, const KvView &kv, int b, int kvh,
-                                                 int row0, int slot, int c, uint32_t lb) {
+__device__ __forceinline__ Chunk<E> load_key_row(const E *base, const KvView &kv, const PageWin &pw,
+                                                 int b, int kvh, int row0, int slot, int c,
+                                                 uint32_t lb) {
   if constexpr (PAGED) {
     if (kv.ps_log2 < 4) return Chunk<E>::load(base + row_offset<true>(kv, b, kvh, row0 + slot) + c * 8);
   }
-  const E *p = base + row16_offset<PAGED>(kv, b, kvh, row0);
+  const E *p = base + row16_offset<PAGED>(kv, pw, b, kvh, row0);
   if constexpr (sizeof(E) == 2) {
     return Chunk<E>{buffer_load16(p, lb)};
   } else {
@@ -157,6 +184,7 @@ __device__ __forceinline__ void score_tile(const KvView &kv, int b, int kvh, int
   const int tid = threadIdx.x, slot = tid >> 4, c = tid & 15;
   const E *K = static_cast<const E *>(kv.k);
   const uint32_t lb = (uint32_t)(((int64_t)slot * kv.sn + c * 8) * (int64_t)sizeof(E));
+  const PageWin pw = page_window<PAGED>(kv, b, start, nrows);
   float m1 = -kInf;
 #pragma unroll
   for (int h = 0; h < G; ++h) mx[h] = -kInf;
@@ -165,7 +193,7 @@ __device__ __forceinline__ void score_tile(const KvView &kv, int b, int kvh, int
   auto load = [&](Chunk<E>(&ch)[U], int base) {
 #pragma unroll
     for (int u = 0; u < U; ++u)
-      ch[u] = load_key_row<E, PAGED>(K, kv, b, kvh, start + base + u * 16, slot, c, lb);
+      ch[u] = load_key_row<E, PAGED>(K, kv, pw, b, kvh, start + base + u * 16, slot, c, lb);
   };
   auto score = [&](const Chunk<E>(&ch)[U], int base) {
 #pragma unroll
@@ -199,7 +227,7 @@ __device__ __forceinline__ void score_tile(const KvView &kv, int b, int kvh, int
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int j = nfull + u * 16 + slot;
-      cur[u] = j < nrows ? load_key_row<E, PAGED>(K, kv, b, kvh, start + nfull + u * 16, slot, c, lb)
+      cur[u] = j < nrows ? load_key_row<E, PAGED>(K, kv, pw, b, kvh, start + nfull + u * 16, slot, c, lb)
                          : Chunk<E>::zero();
     }
 #pragma unroll
@@ -226,6 +254,7 @@ __device__ __forceinline__ void value_tile(const KvView &kv, int b, int kvh, int
   const int tid = threadIdx.x, slot = tid >> 4, c = tid & 15;
   const E *V = static_cast<const E *>(kv.v);
   const uint32_t lb = (uint32_t)(((int64_t)slot * kv.sn + c * 8) * (int64_t)sizeof(E));
+  const PageWin pw = page_window<PAGED>(kv, b, start, nrows);
 #pragma unroll
   for (int h = 0; h < G; ++h)
 #pragma unroll
@@ -235,7 +264,7 @@ __device__ __forceinline__ void value_tile(const KvView &kv, int b, int kvh, int
   auto load = [&](Chunk<E>(&ch)[U], int base) {
 #pragma unroll
     for (int u = 0; u < U; ++u)
-      ch[u] = load_key_row<E, PAGED>(V, kv, b, kvh, start + base + u * 16, slot, c, lb);
+      ch[u] = load_key_row<E, PAGED>(V, kv, pw, b, kvh, start + base + u * 16, slot, c, lb);
   };
   auto add = [&](const Chunk<E>(&ch)[U], int base) {
 #pragma unroll
@@ -273,7 +302,7 @@ __device__ __forceinline__ void value_tile(const KvView &kv, int b, int kvh, int
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int j = nfull + u * 16 + slot;
-      cur[u] = j < nrows ? load_key_row<E, PAGED>(V, kv, b, kvh, start + nfull + u * 16, slot, c, lb)
+      cur[u] = j < nrows ? load_key_row<E, PAGED>(V, kv, pw, b, kvh, start + nfull + u * 16, slot, c, lb)
                          : Chunk<E>::zero();
     }
     add(cur, nfull);

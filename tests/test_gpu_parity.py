@@ -206,7 +206,8 @@ def test_one_launch_many_rounds(monkeypatch):
     lens[7] = 9000
     w = make_workload(3, B=24, n=9000, kind="systematic", S=64, ctx_len=lens, seed=54)
     dw = DeviceWorkload(w)
-    ws = S.alloc_workspace(dw.shape, dw.kv, w.S, S.SANTA_KIND_SYSTEMATIC)
+    ws = max((S.alloc_workspace(dw.shape, dw.kv, w.S, k)
+              for k in (S.SANTA_KIND_SYSTEMATIC, S.SANTA_KIND_DENSE)), key=lambda x: x.numel())
     log(f"[rounds] B={w.B} n={w.n_max} rows={w.B * w.Hkv}")
     for _ in range(3):
         out, idx, _ = run(w, dw=dw, ws=ws)
@@ -223,7 +224,7 @@ def test_workspace_shared_by_both_sampled_paths(monkeypatch):
     from paper_2605_01910_amd import santa as S
     w = make_workload(2, B=4, n=3000, kind="stratified", S=128, seed=55)
     dw = DeviceWorkload(w)
-    spaces = []
+    spaces = [S.alloc_workspace(dw.shape, dw.kv, 1, S.SANTA_KIND_DENSE)]
     for path in ("fused", "split"):
         monkeypatch.setenv("SANTA_SAMPLED", path)
         spaces.append(S.alloc_workspace(dw.shape, dw.kv, w.S, S.SANTA_KIND_STRATIFIED))
