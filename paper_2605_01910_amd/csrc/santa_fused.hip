@@ -32,6 +32,8 @@
 // gathers the chosen V rows once per distinct key.
 // Dense step (k_fused_dense): the split's exact softmax-weighted V sum o_t with
 // (m_t, l_t); the last G arrivals merge O = sum_t a_t o_t / sum_t a_t l_t.
+// Batches that need more than one resident round launch one workgroup per
+// split instead, and the last arrival of a row merges all of its heads.
 //
 // Inside one launch, cross-workgroup data (statistics, partial sums,
 // counters) is written and read with relaxed agent-scope atomics, which are
@@ -579,8 +581,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 // ---------------------------------------------------------------------------
 // Dense step
 // ---------------------------------------------------------------------------
-template <typename E, int G, bool PAGED>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void k_fused_dense(FusedArgs a) {
+// PERSIST: a resident grid of R whole rows per round (small batches; the last
+// min(G, Tb) arrivals of a row merge one head each).  Otherwise one work item
+// per workgroup, hardware-scheduled (large batches): the row's last arrival
+// merges every head and nothing waits, so the grid need not be resident.
+template <typename E, int G, bool PAGED, bool PERSIST>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(PERSIST ? 2 : 3))) void k_fused_dense(FusedArgs a) {
   // dynamic LDS: s [G][pitch] scores / weights, red [4][G*128] (also the merge scratch)
   extern __shared__ __attribute__((aligned(16))) float dyn[];
   constexpr int pitch = kSplitMax;
@@ -618,8 +624,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 
     const QRegs<E, G> qr = load_q<E, G>(static_cast<const E *>(a.q), b, a.Hq, kvh, c);
     float mx[G];
-    score_tile<E, G, PAGED, score_unroll<E, G>()>(a.kv, b, kvh, start, nrows, qr, a.scale_log2, s,
-                                                  pitch, mx);
+    constexpr int U = PERSIST ? score_unroll<E, G>() : 4;
+    score_tile<E, G, PAGED, U>(a.kv, b, kvh, start, nrows, qr, a.scale_log2, s, pitch, mx);
     block_max_heads<G>(mx, mtmp, mh);
     for (int h = wave; h < G; h += kThreads / 64) {
       float *sh = s + h * pitch;
@@ -635,7 +641,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     }
     __syncthreads();
     float acc[G][8];
-    value_tile<E, G, PAGED, score_unroll<E, G>()>(a.kv, b, kvh, start, nrows, s, pitch, acc);
+    value_tile<E, G, PAGED, U>(a.kv, b, kvh, start, nrows, s, pitch, acc);
     __builtin_amdgcn_s_setprio(3);  // the merge chain issues ahead of streaming waves
     reduce_slots<G>(acc, red);
     float2 *mypart = reinterpret_cast<float2 *>(part_row + (int64_t)t * G * kHeadDim);
@@ -650,8 +656,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     }
     if (tid < G) st_coherent(a.stats + (row0 + tid) * T + t, make_float2(mh[tid], lh[tid]));
 
-    // arrive; the last min(G, Tb) arrivals merge one or more heads each
-    const int W = min(G, Tb);
+    // arrive; the last W arrivals merge one or more heads each
+    const int W = PERSIST ? min(G, Tb) : 1;
     const int rank = row_arrive(sync, base, &rank_lds);
     if (rank < Tb - W) continue;
     if (rank == Tb - 1) {
@@ -996,8 +1002,15 @@ hipError_t launch_fused_dense(const Plan &p, const KvView &kv, const void *q, fl
     constexpr int G = decltype(gc)::value;
     constexpr bool PG = decltype(paged)::value;
     const size_t lds = (size_t)fused_dense_floats(G, kSplitMax, p.T) * 4;
-    return launch_resident(reinterpret_cast<const void *>(&k_fused_dense<E, G, PG>), p, args, lds,
-                           st);
+    const void *res = reinterpret_cast<const void *>(&k_fused_dense<E, G, PG, true>);
+    const int rows = p.B * p.Hkv;
+    if (rows * p.T <= capacity_of(res, lds))  // one resident round
+      return launch_resident(res, p, args, lds, st);
+    void *params[] = {&args};
+    const CallTimer tm = call_timer();
+    return hipExtLaunchKernel(reinterpret_cast<const void *>(&k_fused_dense<E, G, PG, false>),
+                              dim3(rows * p.T), dim3(kThreads), params, lds, st, tm.start, tm.stop,
+                              0);
   });
 }
 
