@@ -70,6 +70,11 @@ def lib():
                                  ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, P, P, P,
                                  P, P, P]
         L.orc_decode.restype = ctypes.c_int
+        L.orc_flash.argtypes = [P, P, ctypes.c_int, ctypes.c_int64, ctypes.c_int, ctypes.c_int,
+                                ctypes.c_int, ctypes.c_int, P, P, P, P, P, P]
+        L.orc_decode_flash.argtypes = [ctypes.POINTER(_Problem), ctypes.c_int, ctypes.c_int, P,
+                                       ctypes.c_int, P, P, P, P, P]
+        L.orc_decode_flash.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -161,6 +166,26 @@ def bernoulli_weights(q: np.ndarray, u: np.ndarray, B: int, mode: int, iid: bool
     return w, mask
 
 
+def flash(s: np.ndarray, v: np.ndarray, tile: int, S_tile: int, a: np.ndarray):
+    """S2ANTA-flash on one row: scores ``s`` [L], values ``v`` [L, d], per-tile
+    uniforms ``a`` [ceil(L/tile)].  Returns (out [d], idx [T, S_tile],
+    tile weights W_t/Z [T], tile estimates O_t [T, d], tile-local CDF [L])."""
+    s = np.ascontiguousarray(s, dtype=np.float64)
+    v, f = _elem(v)
+    L, d = v.shape
+    T = (L + tile - 1) // tile
+    a = np.ascontiguousarray(a, dtype=np.float32).reshape(-1)
+    assert a.size >= T
+    out = np.empty(d, dtype=np.float64)
+    idx = np.empty((T, S_tile), dtype=np.int32)
+    wt = np.empty(T, dtype=np.float64)
+    to = np.empty((T, d), dtype=np.float64)
+    C = np.empty(L, dtype=np.float64)
+    lib().orc_flash(_p(s), _p(v), f, d, L, d, int(tile), int(S_tile), _p(a), _p(idx), _p(out),
+                    _p(wt), _p(to), _p(C))
+    return out, idx, wt, to, C
+
+
 # --------------------------------------------------------------------------
 # batch driver
 # --------------------------------------------------------------------------
@@ -238,3 +263,33 @@ def decode_workload(wl, kind: Optional[str] = None, rows: Optional[Sequence[int]
     return Result(np.array(outs), np.array(idxs) if idxs else None,
                   np.array(cdfs) if cdfs else None, None, None,
                   np.asarray(all_rows, np.int32), threads)
+
+
+def decode_flash(q: np.ndarray, k: np.ndarray, v: np.ndarray, ctx_len: np.ndarray, scale: float,
+                 tile: int, S_tile: int, u: np.ndarray, rows: Optional[Sequence[int]] = None,
+                 want_cdf: bool = False) -> Result:
+    """S2ANTA-flash over logical caches [B, n, Hkv, d]; ``u`` is [B, Hq,
+    ceil(n/tile)].  Result.idx is [rows, T_max*S_tile] (-1 past a row's tiles),
+    Result.w the tile weights [rows, T_max]."""
+    q, f = _elem(q)
+    k, fk = _elem(k)
+    v, fv = _elem(v)
+    assert f == fk == fv, "q, k and v must share one element type"
+    B, Hq, d = q.shape
+    _, n, Hkv, _ = k.shape
+    Tm = (n + tile - 1) // tile
+    ctx = np.ascontiguousarray(ctx_len, dtype=np.int32)
+    P = _Problem(B, Hq, Hkv, d, n, f, q.ctypes.data, k.ctypes.data, v.ctypes.data,
+                 n * Hkv * d, Hkv * d, d, ctx.ctypes.data, float(scale))
+    rows_a = None if rows is None else np.ascontiguousarray(rows, dtype=np.int32)
+    nr = B * Hq if rows_a is None else rows_a.size
+    uu = np.ascontiguousarray(u, dtype=np.float32).reshape(-1)
+    assert uu.size >= B * Hq * Tm
+    out = np.empty((nr, d), dtype=np.float64)
+    idx = np.empty((nr, Tm * S_tile), dtype=np.int32)
+    wt = np.empty((nr, Tm), dtype=np.float64)
+    C = np.full((nr, n), np.nan, dtype=np.float64) if want_cdf else None
+    threads = lib().orc_decode_flash(ctypes.byref(P), int(tile), int(S_tile), _p(uu),
+                                     0 if rows_a is None else nr, _p(rows_a), _p(out), _p(idx),
+                                     _p(wt), _p(C))
+    return Result(out, idx, C, wt, None, rows_a, threads)

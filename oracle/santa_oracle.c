@@ -23,7 +23,12 @@
  *   orc_gather_mean       (1/S) sum_m v_{J_m}                     (Sec. 2, Eq. "stochastic-add-only-attn")
  *   orc_bernoulli_weights ternary / mean-group query weights      (Sec. 5, Eq. "qk_estimator";
  *                                                                  App. C, Eq. "mean_group_query")
+ *   orc_flash             S2ANTA-flash: per-tile systematic sampling with a
+ *                         fixed budget, tiles merged by their softmax mass
+ *                                                                  (Sec. 3.3; App. "S2ANTA-Flash
+ *                                                                  Pseudocode", Kernels 1 and 2)
  *   orc_decode            all of the above over the rows of a batch
+ *   orc_decode_flash      orc_flash over the rows of a batch
  *
  * Readings of points the paper leaves open:
  *   - F^{-1}(T) counts the CDF values <= T ("right" side of a boundary), so a
@@ -225,6 +230,70 @@ void orc_bernoulli_weights(const void *q, int q_f32, int G, int d, const float *
   }
 }
 
+/* S2ANTA-flash for one query row (Sec. 3.3; App. "S2ANTA-Flash Pseudocode").
+ * Kernel 1, per tile t = [t*tile, min((t+1)*tile, L)): m_t = max s, e_j =
+ * exp(s_j - m_t), l_t = sum e_j; S_tile systematic draws on the tile's own
+ * distribution e_j / l_t with the tile's uniform a[t] (thresholds (i + a[t]) /
+ * S_tile, inverse CDF as in orc_inverse_cdf); tile estimate O_t = (1/S_tile)
+ * sum_i v_{J_{t,i}}.  Kernel 2: W_t = exp(m_t - m*) l_t, Z = sum_t W_t,
+ * O = (1/Z) sum_t W_t O_t.
+ * s: scores [L]; v: value rows (row j at j*row_stride); a: [T] uniforms,
+ * T = ceil(L / tile).  Outputs: out [d]; idx [T*S_tile] logical indices, tile
+ * by tile (optional); wt [T] = W_t / Z (optional); tile_out [T*d] = O_t
+ * (optional); cdf [L] tile-local CDF values (optional). */
+void orc_flash(const double *s, const void *v, int v_f32, int64_t row_stride, int L, int d,
+               int tile, int S_tile, const float *a, int32_t *idx, double *out, double *wt,
+               double *tile_out, double *cdf) {
+  const int T = (L + tile - 1) / tile;
+  double *m = (double *)malloc(sizeof(double) * (size_t)T);
+  double *l = (double *)malloc(sizeof(double) * (size_t)T);
+  double *p = (double *)malloc(sizeof(double) * (size_t)tile);
+  double *C = (double *)malloc(sizeof(double) * (size_t)tile);
+  double *thr = (double *)malloc(sizeof(double) * (size_t)S_tile);
+  int32_t *ix = (int32_t *)malloc(sizeof(int32_t) * (size_t)S_tile);
+  double *ot = (double *)malloc(sizeof(double) * (size_t)d * (size_t)T);
+  for (int t = 0; t < T; ++t) {
+    const int j0 = t * tile, n = (L - j0 < tile) ? L - j0 : tile;
+    /* tile statistics and the tile's own distribution */
+    m[t] = s[j0];
+    for (int j = 1; j < n; ++j)
+      if (s[j0 + j] > m[t]) m[t] = s[j0 + j];
+    l[t] = 0.0;
+    for (int j = 0; j < n; ++j) l[t] += exp(s[j0 + j] - m[t]);
+    orc_softmax(s + j0, n, p);
+    orc_cdf(p, n, C);
+    if (cdf)
+      for (int j = 0; j < n; ++j) cdf[j0 + j] = C[j];
+    /* systematic draws inside the tile and the tile estimate */
+    orc_thresholds(0, a + t, S_tile, thr);
+    orc_inverse_cdf(C, n, thr, S_tile, ix);
+    orc_gather_mean((const char *)v + (int64_t)j0 * row_stride * (v_f32 ? 4 : 2), v_f32, row_stride,
+                    d, ix, S_tile, ot + (int64_t)t * d);
+    if (idx)
+      for (int i = 0; i < S_tile; ++i) idx[(int64_t)t * S_tile + i] = j0 + ix[i];
+  }
+  /* merge: tiles weighted by W_t = exp(m_t - m*) l_t */
+  double ms = m[0];
+  for (int t = 1; t < T; ++t)
+    if (m[t] > ms) ms = m[t];
+  double Z = 0.0;
+  for (int t = 0; t < T; ++t) Z += exp(m[t] - ms) * l[t];
+  for (int i = 0; i < d; ++i) out[i] = 0.0;
+  for (int t = 0; t < T; ++t) {
+    const double w = exp(m[t] - ms) * l[t] / Z;
+    if (wt) wt[t] = w;
+    for (int i = 0; i < d; ++i) out[i] += w * ot[(int64_t)t * d + i];
+  }
+  if (tile_out) memcpy(tile_out, ot, sizeof(double) * (size_t)d * (size_t)T);
+  free(m);
+  free(l);
+  free(p);
+  free(C);
+  free(thr);
+  free(ix);
+  free(ot);
+}
+
 /* ------------------------------------------------------------------------- */
 /* Batch driver                                                              */
 /* ------------------------------------------------------------------------- */
@@ -328,6 +397,54 @@ int orc_decode(const orc_problem_t *P, int kind, int S, const float *u, const fl
     free(p);
     free(C);
     free(T);
+  }
+  return threads;
+}
+
+/* orc_flash over the listed rows (row = b*Hq + h; rows == NULL means all):
+ * u[(b*Hq + h)*T_max + t] is the uniform of tile t, T_max = ceil(n_max / tile).
+ * Outputs compact over the listed rows: out[r*d]; idx[r*T_max*S_tile] (tiles at
+ * or past ceil(L_b / tile) hold -1); wt[r*T_max] (optional, 0 past the row's
+ * tiles); cdf[r*n_max] tile-local CDF (optional).  Returns the thread count. */
+int orc_decode_flash(const orc_problem_t *P, int tile, int S_tile, const float *u, int nrows,
+                     const int32_t *rows, double *out, int32_t *idx, double *wt, double *cdf) {
+  const int G = P->Hq / P->Hkv;
+  const int total = nrows > 0 ? nrows : P->B * P->Hq;
+  const int Tm = (P->n_max + tile - 1) / tile;
+  int threads = 1;
+#pragma omp parallel
+  {
+#ifdef _OPENMP
+#pragma omp single
+    threads = omp_get_num_threads();
+#endif
+    double *qd = (double *)malloc(sizeof(double) * (size_t)P->d);
+    double *s = (double *)malloc(sizeof(double) * (size_t)(P->n_max > 0 ? P->n_max : 1));
+#pragma omp for schedule(dynamic, 1)
+    for (int r = 0; r < total; ++r) {
+      const int row = rows ? rows[r] : r;
+      const int b = row / P->Hq, h = row % P->Hq, kv = h / G;
+      const int L = P->ctx_len[b];
+      double *o = out + (int64_t)r * P->d;
+      int32_t *ix = idx ? idx + (int64_t)r * Tm * S_tile : NULL;
+      double *w = wt ? wt + (int64_t)r * Tm : NULL;
+      if (ix)
+        for (int i = 0; i < Tm * S_tile; ++i) ix[i] = -1;
+      if (w)
+        for (int t = 0; t < Tm; ++t) w[t] = 0.0;
+      if (L <= 0) {
+        for (int i = 0; i < P->d; ++i) o[i] = 0.0;
+        continue;
+      }
+      const int64_t base = (int64_t)b * P->sb + (int64_t)kv * P->sh;
+      const size_t esz = P->is_f32 ? 4 : 2;
+      for (int i = 0; i < P->d; ++i) qd[i] = elem(P->q, P->is_f32, ((int64_t)b * P->Hq + h) * P->d + i);
+      orc_scores(qd, P->d, (const char *)P->k + base * (int64_t)esz, P->is_f32, P->sn, L, P->scale, s);
+      orc_flash(s, (const char *)P->v + base * (int64_t)esz, P->is_f32, P->sn, L, P->d, tile, S_tile,
+                u + (int64_t)row * Tm, ix, o, w, NULL, cdf ? cdf + (int64_t)r * P->n_max : NULL);
+    }
+    free(qd);
+    free(s);
   }
   return threads;
 }

@@ -1,0 +1,152 @@
+"""Pins of the oracle's S2ANTA-flash estimator (Sec. 3.3; App. "S2ANTA-Flash
+Pseudocode", Kernels 1 and 2) against facts that do not come from the oracle
+itself: the exact expectation over each tile's uniform equals dense attention
+(tiles are sampled independently and merged by their exact softmax mass), the
+single-tile case reduces to the systematic estimator of Sec. 2.1, a uniform
+tile sampled with one draw per key returns every key once, the tile weights
+are the tile masses of the dense distribution, and a Monte Carlo mean over
+independent uniforms converges to dense attention.  CPU only."""
+
+import math
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+
+
+def _f32(a):
+    return np.asarray(a, dtype=np.float32)
+
+
+def _row(rng, L, d, sharp=2.0):
+    q = _f32(rng.standard_normal(d) * sharp)
+    k = _f32(rng.standard_normal((L, d)))
+    v = _f32(rng.standard_normal((L, d)))
+    return q, k, v
+
+
+def _dense(q, k, v, scale):
+    s = (k.astype(np.float64) @ q.astype(np.float64)) * scale
+    p = np.exp(s - s.max())
+    p /= p.sum()
+    return p @ v.astype(np.float64), p
+
+
+@pytest.mark.parametrize("L,tile,S_tile", [(5, 2, 1), (40, 16, 3), (64, 16, 16), (100, 32, 4)])
+def test_flash_exact_expectation_equals_dense(L, tile, S_tile):
+    """O = sum_t (W_t/Z) O_t(a_t) with independent a_t; O_t is piecewise
+    constant in a_t with breakpoints frac(S_tile F_t(j)), so integrating each
+    tile over its own uniform gives sum_t (W_t/Z) mu_t = AV exactly."""
+    rng = np.random.default_rng(1000 + L + tile + S_tile)
+    d = 8
+    q, k, v = _row(rng, L, d)
+    scale = 1 / math.sqrt(d)
+    s = O.scores(q.astype(np.float64), k, scale)
+    T = (L + tile - 1) // tile
+    _, _, wt, _, C = O.flash(s, v, tile, S_tile, np.zeros(T, np.float32))
+    mean, unresolved = np.zeros(d), 0.0
+    for t in range(T):
+        Ct = C[t * tile:min((t + 1) * tile, L)]
+        brk = np.unique(np.concatenate([[0.0, 1.0], np.mod(S_tile * Ct, 1.0)]))
+        for lo, hi in zip(brk[:-1], brk[1:]):
+            a = np.zeros(T, np.float32)
+            a[t] = np.float32((lo + hi) / 2)
+            if not (lo < float(a[t]) < hi):
+                unresolved += (hi - lo) * wt[t]          # narrower than float32 spacing
+                continue
+            _, _, _, to, _ = O.flash(s, v, tile, S_tile, a)
+            mean += (hi - lo) * wt[t] * to[t]
+    ref, _ = _dense(q, k, v, scale)
+    assert np.abs(mean - ref).max() <= 1e-12 + unresolved * 2 * np.abs(v).max()
+
+
+def test_flash_tile_weights_are_dense_tile_masses():
+    rng = np.random.default_rng(7)
+    L, d, tile = 77, 4, 16
+    q, k, v = _row(rng, L, d, sharp=3.0)
+    s = O.scores(q.astype(np.float64), k, 0.5)
+    _, _, wt, _, _ = O.flash(s, v, tile, 2, np.full(5, 0.5, np.float32))
+    _, p = _dense(q, k, v, 0.5)
+    masses = np.array([p[t * tile:(t + 1) * tile].sum() for t in range(5)])
+    assert np.allclose(wt, masses, rtol=0, atol=1e-14)
+    assert abs(wt.sum() - 1.0) < 1e-14
+
+
+@pytest.mark.parametrize("L,S", [(10, 1), (33, 5), (64, 64)])
+def test_flash_single_tile_is_systematic(L, S):
+    """With one tile (tile >= L) the flash estimate is the systematic
+    estimator of Sec. 2.1 with the same uniform."""
+    rng = np.random.default_rng(50 + L)
+    d = 6
+    q, k, v = _row(rng, L, d)
+    s = O.scores(q.astype(np.float64), k, 0.4)
+    u = np.float32(rng.random())
+    out, idx, wt, _, _ = O.flash(s, v, 128, S, np.array([u], np.float32))
+    C = O.cdf(O.softmax(s))
+    ref_idx = O.inverse_cdf(C, O.thresholds("systematic", np.array([u]), S))
+    assert np.array_equal(idx[0], ref_idx)
+    assert wt[0] == 1.0
+    assert np.abs(out - O.gather_mean(v, ref_idx)).max() <= 1e-12
+
+
+def test_flash_uniform_tile_one_draw_per_key_returns_every_key():
+    """Equal scores and S_tile = tile: the thresholds (i + a)/tile fall one in
+    each key's interval, so every key of every tile is drawn once and the
+    estimate is exactly the dense average."""
+    L, d, tile = 64, 5, 16
+    rng = np.random.default_rng(3)
+    v = _f32(rng.standard_normal((L, d)))
+    s = np.zeros(L)
+    for a in (0.0, 0.25, 0.999):
+        out, idx, wt, _, _ = O.flash(s, v, tile, tile, np.full(4, a, np.float32))
+        assert np.array_equal(idx.reshape(-1), np.arange(L))
+        assert np.allclose(wt, 0.25, rtol=0, atol=1e-15)
+        assert np.abs(out - v.astype(np.float64).mean(0)).max() <= 1e-12
+
+
+def test_flash_monte_carlo_mean_converges_to_dense():
+    N, L, d, tile, S_tile = 10000, 48, 8, 16, 2
+    rng = np.random.default_rng(91)
+    q, k, v = _row(rng, L, d)
+    Q = np.broadcast_to(q, (N, 1, d)).copy()
+    K = np.broadcast_to(k[None, :, None, :], (N, L, 1, d)).copy()
+    V = np.broadcast_to(v[None, :, None, :], (N, L, 1, d)).copy()
+    u = np.random.default_rng(92).random((N, 1, 3), dtype=np.float32)
+    res = O.decode_flash(Q, K, V, np.full(N, L, np.int32), 0.3, tile, S_tile, u)
+    mean = res.out.mean(0)
+    se = res.out.std(0, ddof=1) / math.sqrt(N)
+    ref, _ = _dense(q, k, v, 0.3)
+    assert np.all(np.abs(mean - ref) <= 5 * se + 1e-12)
+
+
+def test_flash_batch_driver_structure_and_ragged_rows():
+    """Per row: S_tile indices per tile, each inside its tile and
+    non-decreasing, -1 past the row's tiles; batch rows agree with the
+    single-row function; an empty row gives zeros."""
+    rng = np.random.default_rng(5)
+    B, Hq, Hkv, n, d, tile, S_tile = 3, 4, 2, 70, 8, 16, 3
+    q = _f32(rng.standard_normal((B, Hq, d)))
+    k = _f32(rng.standard_normal((B, n, Hkv, d)))
+    v = _f32(rng.standard_normal((B, n, Hkv, d)))
+    ctx = np.array([70, 33, 0], np.int32)
+    Tm = (n + tile - 1) // tile
+    u = rng.random((B, Hq, Tm), dtype=np.float32)
+    res = O.decode_flash(q, k, v, ctx, 0.4, tile, S_tile, u)
+    for r in range(B * Hq):
+        b, h = divmod(r, Hq)
+        L = int(ctx[b])
+        ix = res.idx[r].reshape(Tm, S_tile)
+        if L == 0:
+            assert np.all(ix == -1) and np.all(res.out[r] == 0)
+            continue
+        T = (L + tile - 1) // tile
+        assert np.all(ix[T:] == -1)
+        for t in range(T):
+            assert np.all((ix[t] >= t * tile) & (ix[t] < min((t + 1) * tile, L)))
+            assert np.all(np.diff(ix[t]) >= 0)
+        s = O.scores(q[b, h].astype(np.float64), k[b, :L, h // 2], 0.4)
+        out, idx1, wt, _, _ = O.flash(s, v[b, :L, h // 2], tile, S_tile, u[b, h])
+        assert np.array_equal(idx1.reshape(-1), ix[:T].reshape(-1))
+        assert np.array_equal(out, res.out[r])
+        assert np.allclose(res.w[r, :T], wt) and np.all(res.w[r, T:] == 0)
