@@ -60,7 +60,8 @@ typedef enum {
   SANTA_KIND_DENSE = 0,
   SANTA_KIND_SYSTEMATIC = 1,
   SANTA_KIND_STRATIFIED = 2,
-  SANTA_KIND_BERNOULLI = 3
+  SANTA_KIND_BERNOULLI = 3,
+  SANTA_KIND_FLASH = 4
 } santa_kind_t;
 
 /* Problem shape.  dtype is a santa_dtype_t. */
@@ -111,7 +112,7 @@ typedef struct {
 } santa_kt_t;
 
 /* Bytes of workspace the given call needs (kind: santa_kind_t; S ignored for
- * SANTA_KIND_DENSE).  Returns 0 if the arguments are invalid. */
+ * SANTA_KIND_DENSE and SANTA_KIND_FLASH).  Returns 0 if the arguments are invalid. */
 size_t santa_workspace_size(const santa_shape_t *shape, const santa_kv_t *kv, int32_t S,
                             int32_t kind);
 
@@ -167,6 +168,31 @@ santa_status_t santa_decode_bernoulli_qk(const void *q, const santa_kt_t *kt,
                                          const float *u_q, int32_t S, const float *u,
                                          int32_t *idx_out, uint8_t *feat_mask_out, void *out,
                                          void *ws, size_t ws_bytes, void *stream);
+
+/* S2ANTA-flash (Sec. 3.3, "Speculative Sampling with Deferred Normalization";
+ * App. "S2ANTA-Flash Pseudocode", Kernels 1 and 2).  Each row's keys are cut
+ * into tiles of `tile` keys (tile t = [t*tile, min((t+1)*tile, L))); every
+ * tile draws S_tile samples by systematic sampling on its own distribution
+ * e_j / l_t, e_j = exp(s_j - m_t), m_t = max_t s, l_t = sum e_j (thresholds
+ * (i + a)/S_tile with the tile's uniform a, inverse CDF as above, clamped to
+ * the tile), giving the tile estimate O_t = (1/S_tile) sum_i V_{J_{t,i}}; the
+ * tiles are merged by their softmax mass: out = sum_t W_t O_t / sum_t W_t,
+ * W_t = exp(m_t - max_t m_t) l_t.  The paper's budget is S_tile ~ S/T for a
+ * total of S draws over T tiles; the caller passes S_tile.
+ * tile:    keys per tile, a power of two in [16, 1024].
+ * S_tile:  draws per tile and query head, 1 <= S_tile <= 4096.
+ * u:       float32 [batch, num_q_heads, T_max], T_max = ceil(n_k / tile): the
+ *          uniform in [0,1) of each (row, tile).
+ * idx_out: optional int32 [batch, num_q_heads, T_max, S_tile]: the drawn keys
+ *          (logical positions) tile by tile, -1 for tiles at or past the row's
+ *          length.
+ * The workspace is sized by santa_workspace_size(..., SANTA_KIND_FLASH) (the
+ * dense step's workspace).  Contiguous and paged caches; not available under
+ * SANTA_VARIANT=multi (returns SANTA_ERR_UNSUPPORTED). */
+santa_status_t santa_decode_flash(const void *q, const santa_kv_t *kv, const santa_shape_t *shape,
+                                  float scale, int32_t tile, int32_t S_tile, const float *u,
+                                  int32_t *idx_out, void *out, void *ws, size_t ws_bytes,
+                                  void *stream);
 
 /* Profiling hook (not part of the method).  start_event and stop_event are
  * hipEvent_t handles created by the caller with timing enabled.  The next

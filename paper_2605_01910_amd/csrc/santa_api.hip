@@ -258,7 +258,8 @@ extern "C" {
 size_t santa_workspace_size(const santa_shape_t *shape, const santa_kv_t *kv, int32_t S,
                             int32_t kind) {
   if (check_shape(shape) != SANTA_OK || !kv || kv->n_k < 1) return 0;
-  if (kind < SANTA_KIND_DENSE || kind > SANTA_KIND_BERNOULLI) return 0;
+  if (kind < SANTA_KIND_DENSE || kind > SANTA_KIND_FLASH) return 0;
+  if (kind == SANTA_KIND_FLASH) kind = SANTA_KIND_DENSE;  // the same launch layout
   if (kind != SANTA_KIND_DENSE && (S < 1 || S > (1 << 24))) return 0;
   return make_plan(shape, kv, S, kind).total;
 }
@@ -330,6 +331,26 @@ santa_status_t santa_decode_bernoulli_qk(const void *q, const santa_kt_t *kt,
                                             mode, u_q, u, idx_out, feat_mask_out, out,
                                             static_cast<char *>(ws),
                                             static_cast<hipStream_t>(stream)));
+}
+
+santa_status_t santa_decode_flash(const void *q, const santa_kv_t *kv, const santa_shape_t *shape,
+                                  float scale, int32_t tile, int32_t S_tile, const float *u,
+                                  int32_t *idx_out, void *out, void *ws, size_t ws_bytes,
+                                  void *stream) {
+  TimerScope timer_scope;
+  santa_status_t s = common_checks(q, kv, shape, scale, out, true);
+  if (s != SANTA_OK) return s;
+  if (!is_pow2(tile) || tile < 16 || tile > santa::kSplitMax)
+    return fail(SANTA_ERR_INVALID_ARG, "tile must be a power of two in [16, 1024]");
+  if (S_tile < 1 || S_tile > 4096) return fail(SANTA_ERR_INVALID_ARG, "S_tile must be in [1, 4096]");
+  if (!u) return fail(SANTA_ERR_INVALID_ARG, "u is NULL");
+  const santa::Plan p = make_plan(shape, kv, 0, SANTA_KIND_DENSE);
+  s = check_ws(p, ws, ws_bytes);
+  if (s != SANTA_OK) return s;
+  if (!p.fused) return fail(SANTA_ERR_UNSUPPORTED, "the flash step needs the fused launch layout");
+  return hip_status(santa::launch_fused_flash(p, make_view(kv), q, log2_scale(scale), ilog2(tile),
+                                              S_tile, u, idx_out, out, static_cast<char *>(ws),
+                                              static_cast<hipStream_t>(stream)));
 }
 
 santa_status_t santa_time_next_call(void *start_event, void *stop_event) {

@@ -69,6 +69,9 @@ struct FusedArgs {
   int ustage;     // the group's uniforms (G*S stratified, G systematic) staged in LDS if 1
   int64_t npitch; // stash floats per head row (n_k rounded up to 64)
   float invS, scale_log2;
+  int tile_log2;  // flash: log2 of the tile length (16 .. kSplitMax keys)
+  int S_tile;     // flash: samples per tile and head
+  int Tmax;       // flash: tiles of the longest row, ceil(n_k / tile)
 };
 
 constexpr int kSpinLimit = 1 << 22;
@@ -101,6 +104,13 @@ __host__ __device__ constexpr int fused_sampled_floats(int G, int Lsmax, int T, 
 __host__ __device__ constexpr int fused_dense_floats(int G, int Lsmax, int T) {
   return G * Lsmax + imax(4 * G * kHeadDim, T + kThreads);
 }
+// flash mode of k_fused_dense: s [G][Lsmax] (scores, then tile CDFs), cnt
+// [G][Lsmax] (counts, then weights; after the gather the slot reduction and
+// merge scratch), list [Lsmax], tile statistics [G][2][kSplitMax/16].
+__host__ __device__ constexpr int fused_flash_floats(int G, int Lsmax, int T) {
+  return G * Lsmax + imax(G * Lsmax, imax(4 * G * kHeadDim, T + kThreads)) + Lsmax +
+         2 * G * (kSplitMax / 16);
+}
 // k_stream_cdf: P [G][kSplitMax].
 // k_value_heads: block ends [ncoarse], offsets [T+1], split factors [T], chosen
 // keys and run list [2][kThreads], slot reduction [4][128].
@@ -108,13 +118,13 @@ __host__ __device__ constexpr int value_heads_floats(int T, int ncoarse) {
   return ncoarse + (T + 1) + T + 2 * kThreads + 4 * kHeadDim;
 }
 
-__device__ __forceinline__ void split_geometry(int L, int T, int &Ls, int &Tb) {
+__device__ __forceinline__ void split_geometry(int L, int T, int &Ls, int &Tb, int align = kAlign) {
   if (L <= 0) {
-    Ls = kAlign;
+    Ls = align;
     Tb = 0;
     return;
   }
-  Ls = (((L + T - 1) / T) + kAlign - 1) & ~(kAlign - 1);
+  Ls = (((L + T - 1) / T) + align - 1) & ~(align - 1);
   Tb = (L + Ls - 1) / Ls;
 }
 
@@ -278,6 +288,123 @@ __device__ __forceinline__ void merge_head(const float *part_row, int h, int Tb,
 }
 
 // ---------------------------------------------------------------------------
+// S2ANTA-flash value stage (Sec. 3.3; App. "S2ANTA-Flash Pseudocode", Kernel 1)
+// ---------------------------------------------------------------------------
+// Tile-local CDFs of one head's split, computed by one wave in place: the
+// split (nrows <= kSplitMax scores in s, log2 units) holds tiles of 2^tl2 keys
+// (16 <= tile; the split starts on a tile boundary).  For tile tau: m_tau =
+// max s, P_j = sum_{i <= j in tau} exp2(s_i - m_tau), written over s[j];
+// tm[tau] = m_tau and tl[tau] = P_last.  Lane l owns keys 16l..16l+15 and a
+// tile spans 2^tl2 / 16 aligned lanes, so the tile max is a butterfly and the
+// tile prefix a segmented scan over those lanes, made non-decreasing by a
+// segmented prefix max (fixed order: equal inputs give equal CDFs).
+__device__ __forceinline__ void wave_tile_cdf(float *s, int nrows, int lane, int tl2, float *tm,
+                                              float *tl) {
+  constexpr int CH = kSplitMax / 64;
+  const int j0 = lane * CH;
+  const int seg = (1 << tl2) / CH;  // lanes per tile, 1 .. 64
+  const int pos = lane & (seg - 1);
+  float x[CH];
+#pragma unroll
+  for (int i = 0; i < CH / 4; ++i) {
+    const float4 v = reinterpret_cast<const float4 *>(s + j0)[i];
+    x[4 * i] = v.x;
+    x[4 * i + 1] = v.y;
+    x[4 * i + 2] = v.z;
+    x[4 * i + 3] = v.w;
+  }
+  float m = -kInf;
+#pragma unroll
+  for (int i = 0; i < CH; ++i) m = (j0 + i < nrows) ? fmaxf(m, x[i]) : m;
+  for (int d = 1; d < seg; d <<= 1) m = fmaxf(m, __shfl_xor(m, d));
+  float acc = 0.0f;
+#pragma unroll
+  for (int i = 0; i < CH; ++i) {
+    acc += (j0 + i < nrows) ? fast_exp2(x[i] - m) : 0.0f;
+    x[i] = acc;
+  }
+  float incl = acc;
+  for (int d = 1; d < seg; d <<= 1) {
+    const float y = __shfl_up(incl, d);
+    incl += pos >= d ? y : 0.0f;
+  }
+  for (int d = 1; d < seg; d <<= 1) {
+    const float y = __shfl_up(incl, d);
+    incl = pos >= d ? fmaxf(incl, y) : incl;
+  }
+  const float prev = __shfl_up(incl, 1);
+  const float base = pos == 0 ? 0.0f : prev;
+  if (j0 < nrows) {
+#pragma unroll
+    for (int i = 0; i < CH / 4; ++i)
+      reinterpret_cast<float4 *>(s + j0)[i] =
+          make_float4(fminf(base + x[4 * i], incl), fminf(base + x[4 * i + 1], incl),
+                      fminf(base + x[4 * i + 2], incl), fminf(base + x[4 * i + 3], incl));
+  }
+  if (pos == seg - 1 && (lane / seg) * (1 << tl2) < nrows) {
+    tm[lane / seg] = m;
+    tl[lane / seg] = incl;
+  }
+}
+
+// #{j < n : P_j <= x} over a non-decreasing LDS CDF (n <= kSplitMax): branch-
+// free binary lifting in a rolled loop.
+__device__ __forceinline__ int lds_count_le(const float *P, int n, float x) {
+  int pos = 0;
+#pragma unroll 1
+  for (int step = 1 << (31 - __clz(n)); step > 0; step >>= 1) {
+    const int np = pos + step;
+    const float v = P[min(np, n) - 1];
+    pos = (np <= n && v <= x) ? np : pos;
+  }
+  return pos;
+}
+
+// Flash draws of one split (Kernel 1): every tile tau of the split and every
+// head h takes S_tile systematic draws on the tile's own distribution: draw i
+// is the key whose tile-CDF interval holds ((i + a)/S_tile) l_tau, a = u of
+// (head, tile) (App. A's inverse CDF, clamped to the tile).  Counts go to cnt;
+// then each drawn key's count becomes the weight count * exp2(m_tau - m_w) *
+// l_tau / S_tile (m_w: the split max), so the split's partial sum is
+// o_w = sum_tau exp2(m_tau - m_w) l_tau O_tau with O_tau the tile estimate.
+// Returns (block-uniform) whether any key was drawn.
+template <int G>
+__device__ __forceinline__ bool flash_draws(const FusedArgs &a, const float *P, int pitch, int *cnt,
+                                            const float *tst, const float *mh, int start,
+                                            int nrows, int64_t row0) {
+  const int tid = threadIdx.x, tl2 = a.tile_log2, St = a.S_tile;
+  const int ntile = (nrows + (1 << tl2) - 1) >> tl2;
+  const int per_h = ntile * St;
+  const float invSt = 1.0f / (float)St;
+  const int gt0 = start >> tl2;  // global index of the split's first tile
+  for (int i = tid; i < G * per_h; i += kThreads) {
+    const int h = i / per_h, rem = i - h * per_h, tau = rem / St, is = rem - tau * St;
+    const int t0 = tau << tl2, n = min(1 << tl2, nrows - t0);
+    const float l = tst[(2 * h + 1) * (kSplitMax / 16) + tau];
+    const float ua = a.u[(row0 + h) * a.Tmax + gt0 + tau];
+    const float x = (((float)is + ua) * invSt) * l;
+    const int k = lds_count_le(P + h * pitch + t0, n, x);
+    const int j = t0 + (k < n ? k : n - 1);
+    atomicAdd(&cnt[h * pitch + j], 1);
+    if (a.idx_out) a.idx_out[((row0 + h) * a.Tmax + gt0 + tau) * St + is] = start + j;
+  }
+  __syncthreads();
+  // counts -> weights
+  for (int i = tid; i < G * nrows; i += kThreads) {
+    const int h = i / nrows, j = i - h * nrows;
+    const int c = cnt[h * pitch + j];
+    if (c) {
+      const int tau = j >> tl2;
+      const float m = tst[(2 * h) * (kSplitMax / 16) + tau];
+      const float l = tst[(2 * h + 1) * (kSplitMax / 16) + tau];
+      cnt[h * pitch + j] = __float_as_int((float)c * (fast_exp2(m - mh[h]) * l * invSt));
+    }
+  }
+  __syncthreads();
+  return G * per_h > 0;
+}
+
+// ---------------------------------------------------------------------------
 // Small-batch sampled step
 // ---------------------------------------------------------------------------
 // #{j < nrows : a P_j <= x} over a non-decreasing LDS CDF P (nrows <=
@@ -385,8 +512,8 @@ __device__ __forceinline__ bool claim_keys(const HeadClaim *hc, const int *rng, 
 // over the whole list (4 rows per wave instruction, 4 rows in flight per row
 // slot), sums its 4 row slots with lane swaps and writes the heads' 128
 // partial sums directly: O_h += c_{h,j} V_j (Sec. 2, the stochastic add-only
-// attention).
-template <typename E, int G, bool PAGED>
+// attention).  FW: cnt holds float weights (bit patterns) instead of counts.
+template <typename E, int G, bool PAGED, bool FW = false>
 __device__ __forceinline__ void gather_heads_waves(const KvView &kv, int b, int kvh, int start,
                                                    int nrows, const int *cnt, int pitch, int *list,
                                                    float *__restrict__ part_out) {
@@ -417,7 +544,8 @@ __device__ __forceinline__ void gather_heads_waves(const KvView &kv, int b, int 
       ch[u].to_float(f);
 #pragma unroll
       for (int hw = 0; hw < HW; ++hw) {
-        const float w = (float)cnt[(wave + 4 * hw) * pitch + jj[u]];
+        const int cw = cnt[(wave + 4 * hw) * pitch + jj[u]];
+        const float w = FW ? __int_as_float(cw) : (float)cw;
 #pragma unroll
         for (int i = 0; i < 8; ++i) acc[hw][i] = fmaf(w, f[i], acc[hw][i]);
       }
@@ -585,15 +713,24 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 // min(G, Tb) arrivals of a row merge one head each).  Otherwise one work item
 // per workgroup, hardware-scheduled (large batches): the row's last arrival
 // merges every head and nothing waits, so the grid need not be resident.
-template <typename E, int G, bool PAGED, bool PERSIST>
+// FLASH: the split's value stage is S2ANTA-flash (Sec. 3.3; App. "S2ANTA-Flash
+// Pseudocode"): S_tile draws per tile and head on the tile's own distribution
+// instead of the exact weighted sum; the split publishes o_w = sum_tau
+// exp2(m_tau - m_w) l_tau O_tau with l_w = sum_tau exp2(m_tau - m_w) l_tau, so
+// the same merge gives O = sum_tau W_tau O_tau / sum_tau W_tau (Kernel 2).
+template <typename E, int G, bool PAGED, bool PERSIST, bool FLASH = false>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(PERSIST ? 2 : 3))) void k_fused_dense(FusedArgs a) {
-  // dynamic LDS: s [G][pitch] scores / weights, red [4][G*128] (also the merge scratch)
+  // dynamic LDS: s [G][pitch] scores / weights, red [4][G*128] (also the merge scratch);
+  // flash: s, cnt [G][pitch] (later red), list [pitch], tile statistics [G][2][kSplitMax/16]
   extern __shared__ __attribute__((aligned(16))) float dyn[];
   constexpr int pitch = kSplitMax;
   float *s = dyn;
   float *red = s + G * pitch;
+  int *cnt = reinterpret_cast<int *>(red);
+  int *list = cnt + imax(G * pitch, imax(4 * G * kHeadDim, a.T + kThreads));
+  float *tst = reinterpret_cast<float *>(list + pitch);
   __shared__ float mh[G], lh[G], mtmp[4 * G], den;
-  __shared__ int rank_lds;
+  __shared__ int rank_lds, wave_cnt[4];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, c = tid & 15;
   const int nrk = a.B * a.Hkv, T = a.T;
@@ -601,6 +738,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(PERSIS
   int rho, t;
   map_item(blockIdx.x, T, R, rho, t);
   E *out = static_cast<E *>(a.out);
+  const int align = FLASH ? imax(kAlign, 1 << a.tile_log2) : kAlign;
 
   for (int rbase = 0; rbase < nrk; rbase += R) {
     __builtin_amdgcn_s_setprio(0);
@@ -610,7 +748,18 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(PERSIS
     const int64_t row0 = (int64_t)b * a.Hq + kvh * G;
     const int L = seq_len(a.kv, b);
     int Ls, Tb;
-    split_geometry(L, T, Ls, Tb);
+    split_geometry(L, T, Ls, Tb, align);
+    if constexpr (FLASH) {
+      // tiles no split covers (past the row's length) have no draws
+      if (a.idx_out && (t == Tb - 1 || (Tb == 0 && t == 0))) {
+        const int t_end = (L + (1 << a.tile_log2) - 1) >> a.tile_log2;
+        const int nt = (a.Tmax - t_end) * a.S_tile;
+        for (int i = tid; i < G * nt; i += kThreads) {
+          const int h = i / nt, k = i - h * nt;
+          a.idx_out[((row0 + h) * a.Tmax + t_end) * a.S_tile + k] = -1;
+        }
+      }
+    }
     if (t >= Tb) {
       if (Tb == 0 && t == 0)
         for (int o = tid; o < G * kHeadDim; o += kThreads) store_out(out + row0 * kHeadDim + o, 0.0f);
@@ -627,32 +776,61 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(PERSIS
     constexpr int U = PERSIST ? score_unroll<E, G>() : 4;
     score_tile<E, G, PAGED, U>(a.kv, b, kvh, start, nrows, qr, a.scale_log2, s, pitch, mx);
     block_max_heads<G>(mx, mtmp, mh);
-    for (int h = wave; h < G; h += kThreads / 64) {
-      float *sh = s + h * pitch;
-      const float m = mh[h];
-      float l = 0.0f;
-      for (int j = lane; j < nrows; j += 64) {
-        const float e = fast_exp2(sh[j] - m);
-        sh[j] = e;
-        l += e;
+    if constexpr (FLASH) {
+      // tile CDFs (wave h: head h), the split normaliser l_w, zeroed counts
+      constexpr int TS = kSplitMax / 16;
+      for (int h = wave; h < G; h += kThreads / 64) {
+        wave_tile_cdf(s + h * pitch, nrows, lane, a.tile_log2, tst + 2 * h * TS, tst + (2 * h + 1) * TS);
+        const int ntile = (nrows + (1 << a.tile_log2) - 1) >> a.tile_log2;
+        float l = 0.0f;
+        for (int tau = lane; tau < ntile; tau += 64)
+          l += fast_exp2(tst[2 * h * TS + tau] - mh[h]) * tst[(2 * h + 1) * TS + tau];
+        l = wave_sum(l);
+        if (lane == 0) lh[h] = l;
       }
-      l = wave_sum(l);
-      if (lane == 0) lh[h] = l;
-    }
-    __syncthreads();
-    float acc[G][8];
-    value_tile<E, G, PAGED, U>(a.kv, b, kvh, start, nrows, s, pitch, acc);
-    __builtin_amdgcn_s_setprio(3);  // the merge chain issues ahead of streaming waves
-    reduce_slots<G>(acc, red);
-    float2 *mypart = reinterpret_cast<float2 *>(part_row + (int64_t)t * G * kHeadDim);
-    for (int o2 = tid; o2 < G * kHeadDim / 2; o2 += kThreads) {
-      float2 v = make_float2(0.0f, 0.0f);
+      for (int i = tid; i < G * pitch; i += kThreads) cnt[i] = 0;
+      __syncthreads();
+      __builtin_amdgcn_s_setprio(3);
+      const bool has = flash_draws<G>(a, s, pitch, cnt, tst, mh, start, nrows, row0);
+      // the draws of a split can reach many distinct rows, so all 16 row slots
+      // of the workgroup share the union list (8 rows in flight per slot, 4
+      // for the wider accumulators of fp32 rows or G = 8)
+      if (has) {
+        constexpr int UG = (sizeof(E) == 2 && G <= 4) ? 8 : 4;
+        gather_union<E, G, PAGED, true, true, UG>(a.kv, b, kvh, start, nrows, s, pitch, cnt, list,
+                                                  wave_cnt, part_row + (int64_t)t * G * kHeadDim);
+      } else {
+        float2 *pz = reinterpret_cast<float2 *>(part_row + (int64_t)t * G * kHeadDim);
+        for (int o2 = tid; o2 < G * kHeadDim / 2; o2 += kThreads) st_coherent(pz + o2, make_float2(0.f, 0.f));
+      }
+    } else {
+      for (int h = wave; h < G; h += kThreads / 64) {
+        float *sh = s + h * pitch;
+        const float m = mh[h];
+        float l = 0.0f;
+        for (int j = lane; j < nrows; j += 64) {
+          const float e = fast_exp2(sh[j] - m);
+          sh[j] = e;
+          l += e;
+        }
+        l = wave_sum(l);
+        if (lane == 0) lh[h] = l;
+      }
+      __syncthreads();
+      float acc[G][8];
+      value_tile<E, G, PAGED, U>(a.kv, b, kvh, start, nrows, s, pitch, acc);
+      __builtin_amdgcn_s_setprio(3);  // the merge chain issues ahead of streaming waves
+      reduce_slots<G>(acc, red);
+      float2 *mypart = reinterpret_cast<float2 *>(part_row + (int64_t)t * G * kHeadDim);
+      for (int o2 = tid; o2 < G * kHeadDim / 2; o2 += kThreads) {
+        float2 v = make_float2(0.0f, 0.0f);
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        v.x += red[w * G * kHeadDim + 2 * o2];
-        v.y += red[w * G * kHeadDim + 2 * o2 + 1];
+        for (int w = 0; w < 4; ++w) {
+          v.x += red[w * G * kHeadDim + 2 * o2];
+          v.y += red[w * G * kHeadDim + 2 * o2 + 1];
+        }
+        st_coherent(mypart + o2, v);
       }
-      st_coherent(mypart + o2, v);
     }
     if (tid < G) st_coherent(a.stats + (row0 + tid) * T + t, make_float2(mh[tid], lh[tid]));
 
@@ -993,6 +1171,32 @@ FusedArgs make_args(const Plan &p, const KvView &kv, const void *q, void *out, f
 }
 
 }  // namespace
+
+hipError_t launch_fused_flash(const Plan &p, const KvView &kv, const void *q, float scale_log2,
+                              int tile_log2, int S_tile, const float *u, int32_t *idx_out,
+                              void *out, char *ws, hipStream_t st) {
+  FusedArgs args = make_args(p, kv, q, out, scale_log2, ws);
+  args.u = u;
+  args.idx_out = idx_out;
+  args.tile_log2 = tile_log2;
+  args.S_tile = S_tile;
+  args.Tmax = (p.n_k + (1 << tile_log2) - 1) >> tile_log2;
+  return with_types(p, kv.bt != nullptr, [&](auto eptr, auto gc, auto paged) -> hipError_t {
+    using E = std::remove_pointer_t<decltype(eptr)>;
+    constexpr int G = decltype(gc)::value;
+    constexpr bool PG = decltype(paged)::value;
+    const size_t lds = (size_t)fused_flash_floats(G, kSplitMax, p.T) * 4;
+    const void *res = reinterpret_cast<const void *>(&k_fused_dense<E, G, PG, true, true>);
+    const int rows = p.B * p.Hkv;
+    if (rows * p.T <= capacity_of(res, lds))  // one resident round
+      return launch_resident(res, p, args, lds, st);
+    void *params[] = {&args};
+    const CallTimer tm = call_timer();
+    return hipExtLaunchKernel(reinterpret_cast<const void *>(&k_fused_dense<E, G, PG, false, true>),
+                              dim3(rows * p.T), dim3(kThreads), params, lds, st, tm.start, tm.stop,
+                              0);
+  });
+}
 
 hipError_t launch_fused_dense(const Plan &p, const KvView &kv, const void *q, float scale_log2,
                               void *out, char *ws, hipStream_t st) {

@@ -36,6 +36,10 @@ hipError_t launch_zero(void *ws, size_t bytes, hipStream_t st);
 hipError_t launch_fused_dense(const Plan &p, const KvView &kv, const void *q, float scale_log2,
                               void *out, char *ws, hipStream_t st);
 
+hipError_t launch_fused_flash(const Plan &p, const KvView &kv, const void *q, float scale_log2,
+                              int tile_log2, int S_tile, const float *u, int32_t *idx_out,
+                              void *out, char *ws, hipStream_t st);
+
 hipError_t launch_fused_sampled(const Plan &p, const KvView &kv, const void *q, float scale_log2,
                                 bool strat, const float *u, int32_t *idx_out, void *out, char *ws,
                                 hipStream_t st);

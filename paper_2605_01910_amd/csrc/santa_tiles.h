@@ -583,22 +583,22 @@ __device__ __forceinline__ int compact_union(const int *cnt, int pitch, int nrow
 // heads of the chosen keys is compacted in key order and each chosen V row is
 // read once: O_h += c_{h,j} V_j (Sec. 2, Eq. "stochastic-add-only-attn").  The
 // G x 128 partial sums are written to part_out (global; coherent stores if
-// COHERENT).  P is reused as the reduction buffer.
-template <typename E, int G, bool PAGED, bool COHERENT>
+// COHERENT).  P is reused as the reduction buffer.  FW: cnt holds float
+// weights (bit patterns) instead of integer counts.
+template <typename E, int G, bool PAGED, bool COHERENT, bool FW = false, int U = 4>
 __device__ __forceinline__ void gather_union(const KvView &kv, int b, int kvh, int start, int nrows,
                                              float *P, int pitch, const int *cnt, int *list,
                                              int *wave_cnt, float *__restrict__ part_out) {
   const int tid = threadIdx.x, slot = tid >> 4, c = tid & 15;
   (void)wave_cnt;
   const int nlist = compact_union<G>(cnt, pitch, nrows, list);
-  // gather-add: slot takes list entries slot, slot+16, ...; 4 rows in flight
+  // gather-add: slot takes list entries slot, slot+16, ...; U rows in flight
   const E *V = static_cast<const E *>(kv.v);
   float acc[G][8];
 #pragma unroll
   for (int h = 0; h < G; ++h)
 #pragma unroll
     for (int i = 0; i < 8; ++i) acc[h][i] = 0.0f;
-  constexpr int U = 4;
   for (int e0 = slot; e0 < nlist; e0 += 16 * U) {
     Chunk<E> ch[U];
     int jj[U];
@@ -617,7 +617,8 @@ __device__ __forceinline__ void gather_union(const KvView &kv, int b, int kvh, i
       ch[uu].to_float(f);
 #pragma unroll
       for (int h = 0; h < G; ++h) {
-        const float w = (float)cnt[h * pitch + jj[uu]];
+        const int cw = cnt[h * pitch + jj[uu]];
+        const float w = FW ? __int_as_float(cw) : (float)cw;
 #pragma unroll
         for (int i = 0; i < 8; ++i) acc[h][i] = fmaf(w, f[i], acc[h][i]);
       }

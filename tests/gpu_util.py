@@ -23,7 +23,8 @@ from workload import bf16_bits_to_f32
 BAND = 1e-5
 DENSE_MAX_ABS, DENSE_REL_L2, SAMPLED_MAX_ABS = 2e-2, 5e-3, 2e-2
 KIND_CODE = {"dense": S.SANTA_KIND_DENSE, "systematic": S.SANTA_KIND_SYSTEMATIC,
-             "stratified": S.SANTA_KIND_STRATIFIED, "bernoulli": S.SANTA_KIND_BERNOULLI}
+             "stratified": S.SANTA_KIND_STRATIFIED, "bernoulli": S.SANTA_KIND_BERNOULLI,
+             "flash": S.SANTA_KIND_FLASH}
 
 
 def log(msg: str) -> None:
@@ -75,6 +76,8 @@ def run(w, kind: Optional[str] = None, layout: str = "nhd", want_idx: bool = Tru
     if ws is None:
         ws = S.alloc_workspace(dw.shape, dw.kv, max(Sn, 1), KIND_CODE[kind])
     idx = None
+    if kind == "flash":
+        Sn = ((w.n_max + w.tile - 1) // w.tile) * w.S_tile  # draws per row, tile by tile
     if want_idx and kind != "dense":
         idx = torch.full((w.B, w.Hq, Sn), -7, dtype=torch.int32, device="cuda")
     mask = None
@@ -84,6 +87,8 @@ def run(w, kind: Optional[str] = None, layout: str = "nhd", want_idx: bool = Tru
         S.santa_decode_systematic(dw.q, dw.kv, dw.shape, w.scale, Sn, dw.u, idx, out, ws)
     elif kind == "stratified":
         S.santa_decode_stratified(dw.q, dw.kv, dw.shape, w.scale, Sn, dw.u, idx, out, ws)
+    elif kind == "flash":
+        S.santa_decode_flash(dw.q, dw.kv, dw.shape, w.scale, w.tile, w.S_tile, dw.u, idx, out, ws)
     elif kind == "bernoulli":
         if want_mask:
             mask = torch.full((w.B, w.Hkv, w.d), 7, dtype=torch.uint8, device="cuda")
@@ -144,4 +149,53 @@ def check_sampled(w, out: np.ndarray, idx: np.ndarray, kind: Optional[str] = Non
         e = float(np.abs(out[r] - ref).max())
         worst = max(worst, e)
         assert e <= SAMPLED_MAX_ABS, f"row {r}: sampled max abs error {e:.3e}"
+    return {"band_accepted": band, "max_abs": worst, "rows": len(rows)}
+
+
+def check_flash(w, out: np.ndarray, idx: np.ndarray, rows: Optional[Sequence[int]] = None) -> dict:
+    """S2ANTA-flash acceptance: every drawn index equals the oracle's or lies
+    within 1e-5 of its threshold on the tile-local CDF (band rule); tiles past
+    a row's length hold -1; each output row matches the oracle's merge
+    sum_t (W_t/Z) (1/S_tile) sum_i V[g_{t,i}] of the GPU's own draws within
+    2e-2."""
+    rows = list(range(w.B * w.Hq)) if rows is None else list(rows)
+    tile, St = w.tile, w.S_tile
+    Tm = (w.n_max + tile - 1) // tile
+    band, worst = 0, 0.0
+    for r in rows:
+        b, h = divmod(r, w.Hq)
+        L = int(w.ctx_len[b])
+        g = idx[r].reshape(Tm, St)
+        if L == 0:
+            assert np.all(g == -1) and np.all(out[r] == 0), f"row {r}: empty row convention"
+            continue
+        kb, vb = w.logical_kv(b)
+        T = (L + tile - 1) // tile
+        assert np.all(g[T:] == -1), f"row {r}: draws past the row's tiles"
+        res = O.decode_flash(w.q[b:b + 1], kb.reshape(1, L, w.Hkv, w.d), vb.reshape(1, L, w.Hkv, w.d),
+                             np.array([L], np.int32), w.scale, tile, St,
+                             w.u[b:b + 1, :, :T].copy() if w.u.shape[2] != T else w.u[b:b + 1],
+                             rows=[h], want_cdf=True)
+        o_idx = res.idx[0].reshape(-1, St)[:T]
+        C = res.cdf[0]
+        wt = res.w[0][:T]
+        for t in range(T):
+            t0 = t * tile
+            n = min(tile, L - t0)
+            gt = g[t]
+            assert np.all((gt >= t0) & (gt < t0 + n)), f"row {r} tile {t}: index outside the tile"
+            for i in np.nonzero(gt != o_idx[t])[0]:
+                j = int(gt[i]) - t0
+                x = (i + float(w.u[b, h, t])) / St
+                lo = C[t0 + j - 1] if j > 0 else 0.0
+                ok = (lo - BAND <= x < C[t0 + j] + BAND) or (j == n - 1 and x >= C[t0 + j] - BAND)
+                assert ok, f"row {r} tile {t} draw {i}: GPU {gt[i]}, oracle {o_idx[t][i]}, x={x!r}"
+                band += 1
+        ref = np.zeros(w.d)
+        vk = vb[:, h // w.G, :]
+        for t in range(T):
+            ref += wt[t] * O.gather_mean(np.ascontiguousarray(vk), g[t])
+        e = float(np.abs(out[r] - ref).max())
+        worst = max(worst, e)
+        assert e <= SAMPLED_MAX_ABS, f"row {r}: flash max abs error {e:.3e}"
     return {"band_accepted": band, "max_abs": worst, "rows": len(rows)}

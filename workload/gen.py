@@ -115,6 +115,9 @@ class Workload:
     k_pages: Optional[np.ndarray] = None
     v_pages: Optional[np.ndarray] = None
     block_table: Optional[np.ndarray] = None
+    # S2ANTA-flash value stage: tile length and draws per tile; u is [B, Hq, ceil(n_max/tile)]
+    tile: int = 0
+    S_tile: int = 0
     # Bernoulli score stage
     k_t: Optional[np.ndarray] = None          # feature-major keys [B, Hkv, d, n_pad >= n_max]
     u_q: Optional[np.ndarray] = None          # [B, Hq, d] (mode 0) or [B, Hkv, d] (mode 1)
@@ -168,7 +171,8 @@ def _plant(keys32: np.ndarray, qf: np.ndarray, G: int, scale: float, sink: float
 def make_workload(cfg: int, seed: int = 0, **over) -> Workload:
     """Build configuration ``cfg`` (1..5), optionally with overrides of its
     parameters (``B, Hq, Hkv, n, S, kind, dtype, sink, heavy, len_lo, len_hi,
-    B_draws, mode, paged, page_size, ctx_len``) for smaller test cases."""
+    B_draws, mode, paged, page_size, ctx_len``, and ``tile, S_tile`` for
+    kind="flash") for smaller test cases."""
     p = dict(CONFIGS[cfg])
     p.update(over)
     B, Hq, Hkv, d, n = p["B"], p["Hq"], p["Hkv"], p["d"], p["n"]
@@ -254,12 +258,17 @@ def make_workload(cfg: int, seed: int = 0, **over) -> Workload:
         w.k, w.v = k, v
         del k_seq, v_seq
 
-    # value-stage uniforms: one per row (systematic) or S per row (stratified)
+    # value-stage uniforms: one per row (systematic), S per row (stratified) or
+    # one per row and tile (flash)
     ru = _rng(cfg, STREAM_U, seed)
     if kind in ("systematic", "bernoulli"):
         w.u = ru.random((B, Hq), dtype=np.float32)
     elif kind == "stratified":
         w.u = ru.random((B, Hq, S), dtype=np.float32)
+    elif kind == "flash":
+        w.tile = int(p.get("tile", 256))
+        w.S_tile = int(p.get("S_tile", 16))
+        w.u = ru.random((B, Hq, (n_max + w.tile - 1) // w.tile), dtype=np.float32)
 
     if kind == "bernoulli":
         w.B_draws = int(p.get("B_draws", 1))
