@@ -47,7 +47,11 @@ def parse():
     ap.add_argument("--cfg", type=int, default=2, help="workload configuration (1..5)")
     ap.add_argument("--B", type=int, default=None)
     ap.add_argument("--S", type=int, default=None)
-    ap.add_argument("--kind", default=None)
+    ap.add_argument("--kind", default=None,
+                    help="dense | systematic | stratified | bernoulli | flash")
+    ap.add_argument("--tile", type=int, default=256, help="flash: keys per tile")
+    ap.add_argument("--S-tile", type=int, default=None,
+                    help="flash: draws per tile (default: the budget rule S_tile ~ S / T)")
     ap.add_argument("--layout", default="nhd", choices=["nhd", "hnd"])
     ap.add_argument("--flush-gib", type=float, default=1.0)
     ap.add_argument("--no-dense", action="store_true")
@@ -80,6 +84,12 @@ def main():
         over["S"] = args.S
     if args.kind is not None:
         over["kind"] = args.kind
+    if args.kind == "flash":
+        from workload.gen import CONFIGS
+        n = CONFIGS[args.cfg]["n"]
+        over["tile"] = args.tile
+        over["S_tile"] = args.S_tile or S.flash_tile_budget(over.get("S", CONFIGS[args.cfg]["S"]),
+                                                            (n + args.tile - 1) // args.tile)
     t0 = time.time()
     w = make_workload(args.cfg, seed=0, **over)
     print(f"[bench] workload cfg={args.cfg} B={w.B} Hq={w.Hq} Hkv={w.Hkv} n={w.n_max} "
@@ -106,6 +116,9 @@ def main():
         elif kind == "bernoulli":
             S.santa_decode_bernoulli_qk(dw.q, dw.kt, dw.kv, dw.shape, w.scale, w.B_draws, w.mode,
                                         dw.u_q, w.S, dw.u, idx_out, mask, out, ws, stream)
+        elif kind == "flash":
+            S.santa_decode_flash(dw.q, dw.kv, dw.shape, w.scale, w.tile, w.S_tile, dw.u, idx_out,
+                                 out, ws, stream)
         else:
             S.santa_decode_dense(dw.q, dw.kv, dw.shape, w.scale, out, ws, stream)
 
@@ -119,11 +132,13 @@ def main():
     uniq_rows = 0
     feat_frac = 1.0
     if kind != "dense":
-        idx = torch.empty((w.B, w.Hq, w.S), dtype=torch.int32, device=dev)
+        ns = w.S if kind != "flash" else ((w.n_max + w.tile - 1) // w.tile) * w.S_tile
+        idx = torch.empty((w.B, w.Hq, ns), dtype=torch.int32, device=dev)
         step(idx)
         torch.cuda.synchronize()
-        ix = idx.cpu().numpy().reshape(w.B, w.Hkv, w.G * w.S)
-        uniq_rows = int(sum(len(np.unique(ix[b, k])) for b in range(w.B) for k in range(w.Hkv)))
+        ix = idx.cpu().numpy().reshape(w.B, w.Hkv, w.G * ns)
+        uniq_rows = int(sum(len(np.unique(ix[b, k][ix[b, k] >= 0]))
+                            for b in range(w.B) for k in range(w.Hkv)))
         if kind == "bernoulli":
             m = mask.cpu().numpy()
             feat_frac = float(m.mean())
@@ -221,7 +236,9 @@ def main():
         "dtype": w.dtype,
         "data": "synthetic",
         "config": {
-            "workload": (f"cfg{args.cfg}: {w.kind} S={w.S}, B={w.B}, Hq={w.Hq}, Hkv={w.Hkv}, d={w.d}, "
+            "workload": (f"cfg{args.cfg}: {w.kind} " +
+                         (f"tile={w.tile} S_tile={w.S_tile}, " if kind == "flash" else f"S={w.S}, ") +
+                         f"B={w.B}, Hq={w.Hq}, Hkv={w.Hkv}, d={w.d}, "
                          f"n_k={w.n_max}, {w.dtype}, {cache_desc}, cold cache "
                          f"({args.flush_gib:g} GiB update + {2 * args.flush_gib:g} GiB read per step)"),
             "variant": os.environ.get("SANTA_VARIANT", "fused"),
@@ -271,6 +288,8 @@ def kernel_label(w, kind: str) -> str:
         return "all kernels of one santa_decode_* call"
     if kind == "dense":
         return "k_fused_dense"
+    if kind == "flash":
+        return "k_fused_dense (flash mode)"
     rows = w.B * w.Hkv
     fill = 128
     while fill > 1 and fill * rows > 512:

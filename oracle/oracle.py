@@ -234,6 +234,8 @@ def decode_workload(wl, kind: Optional[str] = None, rows: Optional[Sequence[int]
     through their logical per-sequence arrays (never through the page pool), so
     the GPU's page-table indirection is checked independently."""
     kind = kind or wl.kind
+    if kind == "flash":
+        return _decode_workload_flash(wl, rows, want_cdf)
     S = wl.S if kind != "dense" else 0
     if not wl.paged:
         return decode(kind, wl.q, wl.k, wl.v, wl.ctx_len, wl.scale, S, wl.u, wl.u_q, wl.B_draws,
@@ -293,3 +295,29 @@ def decode_flash(q: np.ndarray, k: np.ndarray, v: np.ndarray, ctx_len: np.ndarra
                                      0 if rows_a is None else nr, _p(rows_a), _p(out), _p(idx),
                                      _p(wt), _p(C))
     return Result(out, idx, C, wt, None, rows_a, threads)
+
+
+def _decode_workload_flash(wl, rows, want_cdf) -> Result:
+    """decode_workload for kind="flash": contiguous workloads in one batch
+    call, paged ones one sequence at a time through their logical arrays."""
+    if not wl.paged:
+        return decode_flash(wl.q, wl.k, wl.v, wl.ctx_len, wl.scale, wl.tile, wl.S_tile, wl.u,
+                            rows, want_cdf)
+    all_rows = list(range(wl.B * wl.Hq)) if rows is None else list(rows)
+    Tm = (wl.n_max + wl.tile - 1) // wl.tile
+    outs, idxs, threads = [], [], 1
+    for r in all_rows:
+        b, h = divmod(r, wl.Hq)
+        kb, vb = wl.logical_kv(b)
+        L = int(wl.ctx_len[b])
+        T = (L + wl.tile - 1) // wl.tile
+        res = decode_flash(wl.q[b:b + 1], kb.reshape(1, L, wl.Hkv, wl.d),
+                           vb.reshape(1, L, wl.Hkv, wl.d), np.array([L], np.int32), wl.scale,
+                           wl.tile, wl.S_tile, np.ascontiguousarray(wl.u[b:b + 1, :, :T]), [h])
+        threads = max(threads, res.threads)
+        ix = np.full(Tm * wl.S_tile, -1, np.int32)
+        ix[:T * wl.S_tile] = res.idx[0][:T * wl.S_tile]
+        outs.append(res.out[0])
+        idxs.append(ix)
+    return Result(np.array(outs), np.array(idxs), None, None, None,
+                  np.asarray(all_rows, np.int32), threads)
