@@ -167,6 +167,24 @@ santa::Plan make_plan(const santa_shape_t *sh, const santa_kv_t *kv, int S, int 
     p.total = off;
     return p;
   }
+  if (kind == SANTA_KIND_BERNOULLI && tune.fused && Tf <= santa::kMaxSplits) {
+    // Bernoulli scores from the feature-major cache, then the value stage of
+    // the two-launch path (one workgroup per query head)
+    p.fused = 1;
+    p.split2 = 1;
+    // splits of at most 512 keys: the feature-row stream of a split is short,
+    // so more workgroups keep more of it in flight
+    p.T = std::min(santa::kMaxSplits,
+                   std::max(Tf, (int)((p.n_k + 511) / 512)));
+    p.Ls = (int)(((p.n_k + p.T - 1) / p.T + 63) & ~63);
+    p.npitch = ((int64_t)p.n_k + 63) & ~int64_t(63);
+    p.off_err = take(4);
+    p.off_stats = take(rows * p.T * 8);
+    p.off_stash = take(rows * (size_t)p.npitch * 2);
+    p.off_coarse = take(rows * (size_t)(p.npitch / 32) * 4);
+    p.total = off;
+    return p;
+  }
   p.off_stats = take(rows * p.T * 8);
   p.off_part = take((size_t)p.B * p.Hkv * p.T * p.G * D * 4);
   if (kind != SANTA_KIND_DENSE) {
@@ -327,6 +345,10 @@ santa_status_t santa_decode_bernoulli_qk(const void *q, const santa_kt_t *kt,
   s = check_ws(p, ws, ws_bytes);
   if (s != SANTA_OK) return s;
   santa::KtView ktv{kt->k_t, kt->stride_b, kt->stride_h, kt->stride_d};
+  if (p.fused)
+    return hip_status(santa::launch_fused_bernoulli(
+        p, make_view(kv), ktv, q, log2_scale(scale), B_draws, mode, u_q, u, idx_out,
+        feat_mask_out, out, static_cast<char *>(ws), static_cast<hipStream_t>(stream)));
   return hip_status(santa::launch_bernoulli(p, make_view(kv), ktv, q, log2_scale(scale), B_draws,
                                             mode, u_q, u, idx_out, feat_mask_out, out,
                                             static_cast<char *>(ws),

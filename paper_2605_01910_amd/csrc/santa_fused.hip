@@ -872,33 +872,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(PERSIS
 // ---------------------------------------------------------------------------
 // Large-batch sampled step: two launches
 // ---------------------------------------------------------------------------
-// One work item per workgroup, items row-major; the hardware dispatcher
-// balances them.  Writes the stash, the block ends and the statistics.
-template <typename E, int G, bool PAGED>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(sizeof(E) == 2 && G <= 4 && !PAGED ? 8 : (G <= 4 ? 4 : 2)))) void k_stream_cdf(FusedArgs a) {
-  extern __shared__ __attribute__((aligned(16))) float dyn[];
+// Split outputs of the two-launch path, after the split's CDF P (pitch kSplitMax,
+// nrows keys per head) and maxima mh are in LDS: the statistics (m_t, l_t =
+// P_last), each key's CDF within its 32-key block as a 16-bit fraction of the
+// block's mass (the stash) and the CDF at every block end.
+template <int G>
+__device__ __forceinline__ void write_split_stash(const FusedArgs &a, const float *P, const float *mh,
+                                                  int nrows, int64_t row0, int t, int start) {
   constexpr int pitch = kSplitMax;
-  const int T = a.T;
-  float *P = dyn;
-  __shared__ float mh[G], mtmp[4 * G];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int rowkv = blockIdx.x / T, t = blockIdx.x % T;
-  const int b = rowkv / a.Hkv, kvh = rowkv % a.Hkv;
-  const int64_t row0 = (int64_t)b * a.Hq + kvh * G;
-  const int L = seq_len(a.kv, b);
-  int Ls, Tb;
-  split_geometry(L, T, Ls, Tb);
-  if (t >= Tb) return;
-  const int start = t * Ls, nrows = min(Ls, L - start);
-
-  const QRegs<E, G> qr = load_q<E, G>(static_cast<const E *>(a.q), b, a.Hq, kvh, tid & 15);
-  float mx[G];
-  // 4 rows per lane and batch: this kernel relies on many resident waves
-  // (64 VGPRs) rather than on deep per-wave buffering
-  score_tile<E, G, PAGED, 4>(a.kv, b, kvh, start, nrows, qr, a.scale_log2, P, pitch, mx);
-  block_max_heads<G>(mx, mtmp, mh);
-  for (int h = wave; h < G; h += kThreads / 64) wave_split_cdf_m(P + h * pitch, nrows, lane, mh[h]);
-  __syncthreads();
+  const int tid = threadIdx.x, T = a.T;
   if (tid < G) a.stats[(row0 + tid) * T + t] = make_float2(mh[tid], P[tid * pitch + nrows - 1]);
   // stash: 8 keys per 16-byte store; key j of 32-key block k holds
   // round(65535 (P_j - P_{32k-1}) / (P_{block end} - P_{32k-1})) (P_{-1} = 0),
@@ -934,6 +916,212 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(sizeof
         make_float2(ph[min(k * kBlock + kBlock - 1, nrows - 1)],
                     ph[min(k * kBlock + 2 * kBlock - 1, nrows - 1)]);
   }
+}
+
+// One work item per workgroup, items row-major; the hardware dispatcher
+// balances them.  Writes the stash, the block ends and the statistics.
+template <typename E, int G, bool PAGED>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(sizeof(E) == 2 && G <= 4 && !PAGED ? 8 : (G <= 4 ? 4 : 2)))) void k_stream_cdf(FusedArgs a) {
+  extern __shared__ __attribute__((aligned(16))) float dyn[];
+  constexpr int pitch = kSplitMax;
+  const int T = a.T;
+  float *P = dyn;
+  __shared__ float mh[G], mtmp[4 * G];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int rowkv = blockIdx.x / T, t = blockIdx.x % T;
+  const int b = rowkv / a.Hkv, kvh = rowkv % a.Hkv;
+  const int64_t row0 = (int64_t)b * a.Hq + kvh * G;
+  const int L = seq_len(a.kv, b);
+  int Ls, Tb;
+  split_geometry(L, T, Ls, Tb);
+  if (t >= Tb) return;
+  const int start = t * Ls, nrows = min(Ls, L - start);
+
+  const QRegs<E, G> qr = load_q<E, G>(static_cast<const E *>(a.q), b, a.Hq, kvh, tid & 15);
+  float mx[G];
+  // 4 rows per lane and batch: this kernel relies on many resident waves
+  // (64 VGPRs) rather than on deep per-wave buffering
+  score_tile<E, G, PAGED, 4>(a.kv, b, kvh, start, nrows, qr, a.scale_log2, P, pitch, mx);
+  block_max_heads<G>(mx, mtmp, mh);
+  for (int h = wave; h < G; h += kThreads / 64) wave_split_cdf_m(P + h * pitch, nrows, lane, mh[h]);
+  __syncthreads();
+  write_split_stash<G>(a, P, mh, nrows, row0, t, start);
+}
+
+// Query weights of one GQA group for the Bernoulli score stage (Sec. 5, Eq.
+// "qk_estimator"; App. C, Eq. "mean_group_query"), one feature per thread of
+// the first 128: pi_i = |q_i| / norm (mode 0, per head) or m_i / norm (mode
+// 1, m_i the group's mean |q_i|), the stratified count c_i = #{n < B : (n +
+// u_i)/B < pi_i} taken in float32, and w = sign(q_i) c_i norm / B (mode 0) or
+// c_i (norm / B) q_{g,i} / m_i (mode 1).  Writes wl[g*128 + i], the list fl of
+// features with a nonzero weight in some head (in feature order) and, if
+// mask is not null, the group's feature mask.  Returns the list length
+// (block-uniform).  Every thread of the workgroup calls it.
+template <typename E, int G>
+__device__ __forceinline__ int bern_group_weights(const E *__restrict__ q, int64_t row0, int64_t grp,
+                                                  int Bd, int mode, const float *__restrict__ u_q,
+                                                  float *wl, int *fl, uint8_t *mask) {
+  __shared__ float tmp[4];
+  __shared__ int wc[2];
+  const int i = threadIdx.x, lane = i & 63, wave = i >> 6;
+  const bool act = i < kHeadDim;
+  auto max128 = [&](float v) -> float {  // max over the first 128 threads (values >= 0)
+    v = wave_max(act ? v : 0.0f);
+    if (lane == 0) tmp[wave] = v;
+    __syncthreads();
+    const float r = fmaxf(tmp[0], tmp[1]);
+    __syncthreads();
+    return r;
+  };
+  float qv[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) qv[g] = act ? to_f32(q[(row0 + g) * kHeadDim + i]) : 0.0f;
+  float w[G];
+  const float fB = (float)Bd;
+  if (mode == 0) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const float norm = max128(fabsf(qv[g]));
+      const float pi = norm > 0.0f ? fabsf(qv[g]) / norm : 0.0f;
+      const float ug = act ? u_q[(row0 + g) * kHeadDim + i] : 1.0f;
+      int cnt = 0;
+      for (int n = 0; n < Bd; ++n) cnt += (((float)n + ug) / fB) < pi;
+      const float sgn = qv[g] > 0.0f ? 1.0f : (qv[g] < 0.0f ? -1.0f : 0.0f);
+      w[g] = sgn * (float)cnt * (norm / fB);
+    }
+  } else {
+    float m = 0.0f;
+#pragma unroll
+    for (int g = 0; g < G; ++g) m += fabsf(qv[g]);
+    m = m / (float)G;
+    const float norm = max128(m);
+    const float pi = norm > 0.0f ? m / norm : 0.0f;
+    const float ug = act ? u_q[grp * kHeadDim + i] : 1.0f;
+    int cnt = 0;
+    for (int n = 0; n < Bd; ++n) cnt += (((float)n + ug) / fB) < pi;
+    const float mhat = (float)cnt * (norm / fB);
+#pragma unroll
+    for (int g = 0; g < G; ++g) w[g] = m > 0.0f ? mhat * qv[g] / m : 0.0f;
+  }
+  bool keep = false;
+#pragma unroll
+  for (int g = 0; g < G; ++g) keep |= act && w[g] != 0.0f;
+  if (act) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) wl[g * kHeadDim + i] = w[g];
+    if (mask) mask[grp * kHeadDim + i] = keep ? 1 : 0;
+  }
+  const uint64_t bm = __ballot(keep);
+  if (lane == 0 && wave < 2) wc[wave] = __popcll(bm);
+  __syncthreads();
+  if (keep) fl[(wave ? wc[0] : 0) + __popcll(bm & ((1ull << lane) - 1ull))] = i;
+  const int nf = wc[0] + wc[1];
+  __syncthreads();
+  return nf;
+}
+
+// Bernoulli score stage of the two-launch path (Sec. 5, Eq. "qk_estimator";
+// App. C): every split computes its group's query weights, then s_j = scale *
+// sum_{i in F} w_{h,i} K^T_{i,j} over the selected feature rows F of the
+// feature-major cache only; then the split's CDF and the same stash, block
+// ends and statistics as k_stream_cdf, so that k_value_heads finishes the
+// step.  Thread (feature slot fs, key chunk kc) reads 8 consecutive keys of
+// one feature row per 128-bit load, four features in flight; the slots'
+// partial scores are added in slot order.  Split 0 writes the feature mask.
+template <typename E, int G>
+__global__ __launch_bounds__(kThreads) void k_bern_stream(FusedArgs a, KtView kt, int Bd, int mode,
+                                                           const float *__restrict__ u_q,
+                                                           uint8_t *__restrict__ mask_out) {
+  extern __shared__ __attribute__((aligned(16))) float dyn[];
+  constexpr int pitch = kSplitMax;
+  float *P = dyn;  // [G][pitch] scores, then the split CDF
+  __shared__ float wl[G * kHeadDim];
+  __shared__ int fl[kHeadDim];
+  __shared__ float mh[G];
+  const int T = a.T, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int rowkv = blockIdx.x / T, t = blockIdx.x % T;
+  const int b = rowkv / a.Hkv, kvh = rowkv % a.Hkv;
+  const int64_t row0 = (int64_t)b * a.Hq + kvh * G;
+  const int L = seq_len(a.kv, b);
+  int Ls, Tb;
+  split_geometry(L, T, Ls, Tb);
+  if (t >= max(Tb, 1)) return;
+  const int nf = bern_group_weights<E, G>(static_cast<const E *>(a.q), row0, rowkv, Bd, mode, u_q,
+                                          wl, fl, t == 0 ? mask_out : nullptr);
+  if (t >= Tb) return;  // empty row: split 0 only wrote the mask
+  const int start = t * Ls, nrows = min(Ls, L - start);
+
+  const int nchunk = Ls >> 3, FS = kThreads / nchunk;
+  const int kc = tid % nchunk, fs = tid / nchunk;
+  const E *ktb = static_cast<const E *>(kt.kt) + (int64_t)b * kt.sb + (int64_t)kvh * kt.sh;
+  const int p0 = start + kc * 8;
+  const bool full = p0 + 8 <= L;
+  float acc[G][8];
+#pragma unroll
+  for (int h = 0; h < G; ++h)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[h][e] = 0.0f;
+  auto add = [&](const float (&kf)[8], int i) {
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float wv = wl[h * kHeadDim + i];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(wv, kf[e], acc[h][e]);
+    }
+  };
+  if (fs < FS) {
+    constexpr int UF = 4;
+    int fi = fs;
+    if (full) {
+      for (; fi + (UF - 1) * FS < nf; fi += UF * FS) {
+        Chunk<E> ch[UF];
+#pragma unroll
+        for (int u = 0; u < UF; ++u) ch[u] = Chunk<E>::load(ktb + (int64_t)fl[fi + u * FS] * kt.sd + p0);
+#pragma unroll
+        for (int u = 0; u < UF; ++u) {
+          float kf[8];
+          ch[u].to_float(kf);
+          add(kf, fl[fi + u * FS]);
+        }
+      }
+    }
+    for (; fi < nf; fi += FS) {
+      const int i = fl[fi];
+      const E *rp = ktb + (int64_t)i * kt.sd + p0;
+      float kf[8];
+      if (full) {
+        Chunk<E>::load(rp).to_float(kf);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) kf[e] = p0 + e < L ? to_f32(rp[e]) : 0.0f;
+      }
+      add(kf, i);
+    }
+  }
+  // slot partials added in slot order: slot 0 stores, slots 1.. add in turn
+  for (int r = 0; r < FS; ++r) {
+    if (fs == r) {
+#pragma unroll
+      for (int h = 0; h < G; ++h)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          float *d = P + h * pitch + kc * 8 + e;
+          *d = r == 0 ? acc[h][e] : *d + acc[h][e];
+        }
+    }
+    __syncthreads();
+  }
+  for (int o = tid; o < G * nrows; o += kThreads) {
+    const int h = o / nrows, j = o - h * nrows;
+    P[h * pitch + j] *= a.scale_log2;
+  }
+  __syncthreads();
+  for (int h = wave; h < G; h += kThreads / 64) {
+    const float m = wave_split_cdf(P + h * pitch, nrows, lane);
+    if (lane == 0) mh[h] = m;
+  }
+  __syncthreads();
+  write_split_stash<G>(a, P, mh, nrows, row0, t, start);
 }
 
 // Inverse CDF of one threshold (global units) for one query head: split
@@ -1171,6 +1359,32 @@ FusedArgs make_args(const Plan &p, const KvView &kv, const void *q, void *out, f
 }
 
 }  // namespace
+
+hipError_t launch_fused_bernoulli(const Plan &p, const KvView &kv, const KtView &kt,
+                                 const void *q, float scale_log2, int Bd, int mode,
+                                 const float *u_q, const float *u, int32_t *idx_out,
+                                 uint8_t *mask_out, void *out, char *ws, hipStream_t st) {
+  FusedArgs args = make_args(p, kv, q, out, scale_log2, ws);
+  args.u = u;
+  args.idx_out = idx_out;
+  const CallTimer tm = call_timer();
+  return with_types(p, false, [&](auto eptr, auto gc, auto) -> hipError_t {
+    using E = std::remove_pointer_t<decltype(eptr)>;
+    constexpr int G = decltype(gc)::value;
+    void *params1[] = {&args, const_cast<KtView *>(&kt), &Bd, &mode, &u_q, &mask_out};
+    const size_t lds1 = (size_t)G * kSplitMax * 4;
+    hipError_t e = hipExtLaunchKernel(reinterpret_cast<const void *>(&k_bern_stream<E, G>),
+                                      dim3(p.B * p.Hkv * p.T), dim3(kThreads), params1, lds1, st,
+                                      tm.start, nullptr, 0);
+    if (e != hipSuccess) return e;
+    int g = G;
+    void *params2[] = {&args, &g};
+    const size_t lds2 = (size_t)value_heads_floats(p.T, (int)(p.npitch / kBlock)) * 4;
+    return hipExtLaunchKernel(reinterpret_cast<const void *>(&k_value_heads<E, false, false>),
+                              dim3(p.B * p.Hq), dim3(kThreads), params2, lds2, st, nullptr, tm.stop,
+                              0);
+  });
+}
 
 hipError_t launch_fused_flash(const Plan &p, const KvView &kv, const void *q, float scale_log2,
                               int tile_log2, int S_tile, const float *u, int32_t *idx_out,

@@ -33,6 +33,17 @@ hipError_t launch_bernoulli(const Plan &p, const KvView &kv, const KtView &kt, c
 
 hipError_t launch_zero(void *ws, size_t bytes, hipStream_t st);
 
+// Bernoulli query weights, selected-feature lists and the feature mask of
+// every GQA group (k_bern_prep); `start` (nullable) is recorded at dispatch.
+hipError_t launch_bern_prep(const Plan &p, const void *q, int Bd, int mode, const float *u_q,
+                            float *bw, int *blist, int *bn, uint8_t *mask_out, hipStream_t st,
+                            hipEvent_t start);
+
+hipError_t launch_fused_bernoulli(const Plan &p, const KvView &kv, const KtView &kt,
+                                 const void *q, float scale_log2, int Bd, int mode,
+                                 const float *u_q, const float *u, int32_t *idx_out,
+                                 uint8_t *mask_out, void *out, char *ws, hipStream_t st);
+
 hipError_t launch_fused_dense(const Plan &p, const KvView &kv, const void *q, float scale_log2,
                               void *out, char *ws, hipStream_t st);
 

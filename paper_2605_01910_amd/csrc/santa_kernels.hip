@@ -504,6 +504,19 @@ hipError_t launch_sampled(const Plan &p, const KvView &kv, const void *q, float 
   });
 }
 
+hipError_t launch_bern_prep(const Plan &p, const void *q, int Bd, int mode, const float *u_q,
+                            float *bw, int *blist, int *bn, uint8_t *mask_out, hipStream_t st,
+                            hipEvent_t start) {
+  return with_types(p, false, [&](auto eptr, auto gc, auto) -> hipError_t {
+    using E = std::remove_pointer_t<decltype(eptr)>;
+    constexpr int G = decltype(gc)::value;
+    hipExtLaunchKernelGGL(k_bern_prep<E, G>, dim3(p.B * p.Hkv), dim3(kHeadDim), 0, st, start,
+                          nullptr, 0, static_cast<const E *>(q), p.Hq, p.Hkv, Bd, mode, u_q, bw,
+                          blist, bn, mask_out);
+    return hipGetLastError();
+  });
+}
+
 hipError_t launch_bernoulli(const Plan &p, const KvView &kv, const KtView &kt, const void *q,
                             float scale_log2, int Bd, int mode, const float *u_q, const float *u,
                             int32_t *idx_out, uint8_t *mask_out, void *out, char *ws,
