@@ -74,6 +74,9 @@ struct FusedArgs {
   int Tmax;       // flash: tiles of the longest row, ceil(n_k / tile)
 };
 
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
 constexpr int kSpinLimit = 1 << 22;
 constexpr int kAlign = 64;         // split lengths and stash rows are multiples of this many keys
 constexpr int kBlock = 32;         // keys per block of the two-level CDF search
@@ -902,8 +905,9 @@ __device__ __forceinline__ void write_split_stash(const FusedArgs &a, const floa
       const uint32_t q1 = j1 < nrows ? (uint32_t)fminf(fmaf(ph[min(j1, nrows - 1)] - lo, sc, 0.5f), 65535.0f) : 65535u;
       w[e] = q0 | (q1 << 16);
     }
-    *reinterpret_cast<uint4 *>(a.qstash + (row0 + h) * a.npitch + start + j) =
-        make_uint4(w[0], w[1], w[2], w[3]);
+    // non-temporal: the stash is read once, by the value kernel
+    const u32x4 sv = {w[0], w[1], w[2], w[3]};
+    __builtin_nontemporal_store(sv, reinterpret_cast<u32x4 *>(a.qstash + (row0 + h) * a.npitch + start + j));
   }
   // block ends, in pairs (start / 32 is even); an odd last count also writes
   // the (unused) slot after the row's last block
@@ -912,9 +916,9 @@ __device__ __forceinline__ void write_split_stash(const FusedArgs &a, const floa
   for (int i = tid; i < G * nbh; i += kThreads) {
     const int h = i / nbh, k = 2 * (i - h * nbh);
     const float *ph = P + h * pitch;
-    *reinterpret_cast<float2 *>(a.coarse + (row0 + h) * ncoarse + start / kBlock + k) =
-        make_float2(ph[min(k * kBlock + kBlock - 1, nrows - 1)],
-                    ph[min(k * kBlock + 2 * kBlock - 1, nrows - 1)]);
+    const f32x2 cv = {ph[min(k * kBlock + kBlock - 1, nrows - 1)],
+                      ph[min(k * kBlock + 2 * kBlock - 1, nrows - 1)]};
+    __builtin_nontemporal_store(cv, reinterpret_cast<f32x2 *>(a.coarse + (row0 + h) * ncoarse + start / kBlock + k));
   }
 }
 
