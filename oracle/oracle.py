@@ -20,9 +20,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "santa_oracle.c")
 LIB = os.path.join(HERE, "libsanta_oracle.so")
 
-DENSE, SYSTEMATIC, STRATIFIED, IID, BERNOULLI_SYS = range(5)
+DENSE, SYSTEMATIC, STRATIFIED, IID, BERNOULLI_SYS, IID_SPACINGS = range(6)
 KIND = {"dense": DENSE, "systematic": SYSTEMATIC, "stratified": STRATIFIED, "iid": IID,
-        "bernoulli": BERNOULLI_SYS}
+        "bernoulli": BERNOULLI_SYS, "iid_spacings": IID_SPACINGS}
 
 
 def build(verbose: bool = False) -> str:
@@ -128,8 +128,9 @@ def cdf(p: np.ndarray) -> np.ndarray:
 
 
 def thresholds(scheme: str, u: np.ndarray, S: int) -> np.ndarray:
-    """scheme in {'systematic', 'stratified', 'iid'}; u float32 ([1] or [S])."""
-    code = {"systematic": 0, "stratified": 1, "iid": 2}[scheme]
+    """scheme in {'systematic', 'stratified', 'iid', 'iid_spacings'}; u float32
+    ([1], [S], or [S+1] for 'iid_spacings')."""
+    code = {"systematic": 0, "stratified": 1, "iid": 2, "iid_spacings": 3}[scheme]
     u = np.ascontiguousarray(u, dtype=np.float32).reshape(-1)
     T = np.empty(S, dtype=np.float64)
     lib().orc_thresholds(code, _p(u), S, _p(T))

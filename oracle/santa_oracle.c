@@ -121,13 +121,29 @@ void orc_cdf(const double *p, int L, double *C) {
  *   scheme 0, systematic:  T_m = U + m/S with U = u[0]/S uniform on [0, 1/S);
  *   scheme 1, stratified:  T_m uniform on I_m = [m/S, (m+1)/S): T_m = (m + u[m])/S;
  *   scheme 2, i.i.d.:      S independent uniforms u[0..S) in increasing order, whose
- *                          inverse-CDF images are S i.i.d. categorical draws (Sec. 2). */
+ *                          inverse-CDF images are S i.i.d. categorical draws (Sec. 2);
+ *   scheme 3, i.i.d. by spacings: the same S sorted uniforms built from S + 1
+ *                          independent uniforms u[0..S] without a sort: with
+ *                          E_i = -ln(1 - u_i) (unit exponentials), T_m = C_m / C_S,
+ *                          C_m = sum_{i<=m} E_i -- the normalised partial sums of
+ *                          S + 1 exponentials are distributed as the order statistics
+ *                          of S independent uniforms (Renyi's representation). */
 static int cmp_double(const void *a, const void *b) {
   double x = *(const double *)a, y = *(const double *)b;
   return (x > y) - (x < y);
 }
 
 void orc_thresholds(int scheme, const float *u, int S, double *T) {
+  if (scheme == 3) {
+    double C = 0.0;
+    for (int m = 0; m < S; ++m) {
+      C += -log(1.0 - (double)u[m]);
+      T[m] = C;
+    }
+    const double total = C - log(1.0 - (double)u[S]);
+    for (int m = 0; m < S; ++m) T[m] /= total;
+    return;
+  }
   for (int m = 0; m < S; ++m) {
     if (scheme == 0)
       T[m] = ((double)m + (double)u[0]) / (double)S;
@@ -309,13 +325,15 @@ typedef struct {
   double scale;
 } orc_problem_t;
 
-enum { ORC_DENSE = 0, ORC_SYSTEMATIC = 1, ORC_STRATIFIED = 2, ORC_IID = 3, ORC_BERNOULLI_SYS = 4 };
+enum { ORC_DENSE = 0, ORC_SYSTEMATIC = 1, ORC_STRATIFIED = 2, ORC_IID = 3, ORC_BERNOULLI_SYS = 4,
+       ORC_IID_SPACINGS = 5 };
 
 /* One decode step for the listed rows (row = b*Hq + h; rows == NULL means all):
  *   kind dense:        out = AV
  *   kind systematic:   u[b*Hq + h], thresholds (m+u)/S
  *   kind stratified:   u[(b*Hq + h)*S + m]
  *   kind iid:          u[(b*Hq + h)*S + m], sorted
+ *   kind iid spacings: u[(b*Hq + h)*(S+1) + i], thresholds by exponential spacings
  *   kind bernoulli:    Bernoulli scores from u_q (mode 0: [B, Hq, d*(iid?B:1)]; mode 1:
  *                      [B, Hkv, d*(iid?B:1)]) followed by systematic sampling with u[b*Hq + h].
  * Outputs are compact over the listed rows: out[r*d], idx[r*S] (sampled kinds),
@@ -384,6 +402,8 @@ int orc_decode(const orc_problem_t *P, int kind, int S, const float *u, const fl
         for (int j = 0; j < L; ++j) cdf[(int64_t)r * P->n_max + j] = C[j];
       if (kind == ORC_SYSTEMATIC || kind == ORC_BERNOULLI_SYS)
         orc_thresholds(0, u + (int64_t)row, S, T);
+      else if (kind == ORC_IID_SPACINGS)
+        orc_thresholds(3, u + (int64_t)row * (S + 1), S, T);
       else
         orc_thresholds(kind == ORC_STRATIFIED ? 1 : 2, u + (int64_t)row * S, S, T);
       int32_t *ix = idx + (int64_t)r * S;
