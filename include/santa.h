@@ -61,7 +61,8 @@ typedef enum {
   SANTA_KIND_SYSTEMATIC = 1,
   SANTA_KIND_STRATIFIED = 2,
   SANTA_KIND_BERNOULLI = 3,
-  SANTA_KIND_FLASH = 4
+  SANTA_KIND_FLASH = 4,
+  SANTA_KIND_IID = 5
 } santa_kind_t;
 
 /* Problem shape.  dtype is a santa_dtype_t. */
@@ -144,6 +145,20 @@ santa_status_t santa_decode_stratified(const void *q, const santa_kv_t *kv,
                                        const santa_shape_t *shape, float scale, int32_t S,
                                        const float *u, int32_t *idx_out, void *out, void *ws,
                                        size_t ws_bytes, void *stream);
+
+/* SANTA with i.i.d. draws (Sec. 2, Eq. "stochastic-add-only-attn": S indices
+ * drawn independently from the attention distribution, with replacement).
+ * The draws are the inverse CDF (as above) of S sorted independent uniforms,
+ * built without a sort from S + 1 uniforms per row (u: float32 [batch,
+ * num_q_heads, S + 1], in [0,1)): E_i = -ln(1 - u_i), T_m = C_m / C_S with
+ * C_m = sum_{i<=m} E_i (the normalised partial sums of S + 1 unit
+ * exponentials are the order statistics of S uniforms); out = (1/S)
+ * sum_m V_{J_m}.  Requires G*(2S + 1) <= 4096 (G = num_q_heads /
+ * num_kv_heads); workspace as SANTA_KIND_IID.  Not available under
+ * SANTA_VARIANT=multi (returns SANTA_ERR_UNSUPPORTED). */
+santa_status_t santa_decode_iid(const void *q, const santa_kv_t *kv, const santa_shape_t *shape,
+                                float scale, int32_t S, const float *u, int32_t *idx_out,
+                                void *out, void *ws, size_t ws_bytes, void *stream);
 
 /* Bernoulli qK^T score sampling (Sec. 5, Eq. "qk_estimator"; App. C) followed
  * by the systematic value stage.

@@ -237,6 +237,8 @@ def decode_workload(wl, kind: Optional[str] = None, rows: Optional[Sequence[int]
     kind = kind or wl.kind
     if kind == "flash":
         return _decode_workload_flash(wl, rows, want_cdf)
+    if kind == "iid":  # the workload's i.i.d. uniforms are S + 1 per row (spacings)
+        kind = "iid_spacings"
     S = wl.S if kind != "dense" else 0
     if not wl.paged:
         return decode(kind, wl.q, wl.k, wl.v, wl.ctx_len, wl.scale, S, wl.u, wl.u_q, wl.B_draws,

@@ -259,8 +259,9 @@ santa_status_t sampled(const void *q, const santa_kv_t *kv, const santa_shape_t 
   s = check_ws(p, ws, ws_bytes);
   if (s != SANTA_OK) return s;
   if (p.fused)
-    return hip_status(santa::launch_fused_sampled(p, make_view(kv), q, log2_scale(scale), strat, u,
-                                                  idx_out, out, static_cast<char *>(ws),
+    return hip_status(santa::launch_fused_sampled(p, make_view(kv), q, log2_scale(scale),
+                                                  strat ? 1 : 0, u, idx_out, out,
+                                                  static_cast<char *>(ws),
                                                   static_cast<hipStream_t>(stream)));
   return hip_status(santa::launch_sampled(p, make_view(kv), q, log2_scale(scale), strat, u, idx_out,
                                           out, static_cast<char *>(ws),
@@ -276,7 +277,7 @@ extern "C" {
 size_t santa_workspace_size(const santa_shape_t *shape, const santa_kv_t *kv, int32_t S,
                             int32_t kind) {
   if (check_shape(shape) != SANTA_OK || !kv || kv->n_k < 1) return 0;
-  if (kind < SANTA_KIND_DENSE || kind > SANTA_KIND_FLASH) return 0;
+  if (kind < SANTA_KIND_DENSE || kind > SANTA_KIND_IID) return 0;
   if (kind == SANTA_KIND_FLASH) kind = SANTA_KIND_DENSE;  // the same launch layout
   if (kind != SANTA_KIND_DENSE && (S < 1 || S > (1 << 24))) return 0;
   return make_plan(shape, kv, S, kind).total;
@@ -353,6 +354,25 @@ santa_status_t santa_decode_bernoulli_qk(const void *q, const santa_kt_t *kt,
                                             mode, u_q, u, idx_out, feat_mask_out, out,
                                             static_cast<char *>(ws),
                                             static_cast<hipStream_t>(stream)));
+}
+
+santa_status_t santa_decode_iid(const void *q, const santa_kv_t *kv, const santa_shape_t *shape,
+                                float scale, int32_t S, const float *u, int32_t *idx_out,
+                                void *out, void *ws, size_t ws_bytes, void *stream) {
+  TimerScope timer_scope;
+  santa_status_t s = common_checks(q, kv, shape, scale, out, true);
+  if (s != SANTA_OK) return s;
+  const int G = shape->num_q_heads / shape->num_kv_heads;
+  if (S < 1 || (int64_t)G * (2 * S + 1) > 4096)
+    return fail(SANTA_ERR_INVALID_ARG, "S must satisfy 1 <= S and G*(2S+1) <= 4096 for the i.i.d. step");
+  if (!u) return fail(SANTA_ERR_INVALID_ARG, "u is NULL");
+  const santa::Plan p = make_plan(shape, kv, S, SANTA_KIND_IID);
+  s = check_ws(p, ws, ws_bytes);
+  if (s != SANTA_OK) return s;
+  if (!p.fused) return fail(SANTA_ERR_UNSUPPORTED, "the i.i.d. step needs the fused launch layout");
+  return hip_status(santa::launch_fused_sampled(p, make_view(kv), q, log2_scale(scale), 2, u,
+                                                idx_out, out, static_cast<char *>(ws),
+                                                static_cast<hipStream_t>(stream)));
 }
 
 santa_status_t santa_decode_flash(const void *q, const santa_kv_t *kv, const santa_shape_t *shape,

@@ -424,6 +424,56 @@ __device__ __forceinline__ int lds_cdf_count(const float *Ph, int nrows, float a
   return pos;
 }
 
+// Sampling modes of the sampled kernels: the thresholds tau_r of one head
+// (Sec. 2.1, "Construction"; Sec. 2 for the i.i.d. draws), in global CDF
+// units (Z the row's total):
+//   kSys:   ((r + u)/S) Z with one uniform u (uh[0]);
+//   kStrat: ((r + u_r)/S) Z (uh[r]);
+//   kIid:   T_r Z with T the head's sorted i.i.d. thresholds (uh[r], built by
+//           wave_iid_thresholds).
+constexpr int kSys = 0, kStrat = 1, kIid = 2;
+
+template <int MODE>
+__device__ __forceinline__ float tau_of(const float *uh, int r, float invS, float Z) {
+  if constexpr (MODE == kIid) return uh[r] * Z;
+  else return threshold(r, MODE == kStrat ? uh[r] : uh[0], invS, Z);
+}
+
+// Sorted thresholds of the i.i.d. estimator from S + 1 uniforms u without a
+// sort, by one wave: E_i = -log2(1 - u_i) (unit exponentials up to the factor
+// ln 2, which the ratio cancels), C_m = sum_{i <= m} E_i in double, T_m = C_m /
+// C_S for m < S -- the normalised partial sums of S + 1 exponentials are the
+// order statistics of S independent uniforms.  Lane l sums a contiguous chunk
+// of the E_i; the chunk totals are joined by a wave scan made non-decreasing
+// by a prefix max and every partial sum is capped at its lane's total, so T
+// is non-decreasing.  u: S + 1 floats; T: S floats (LDS).
+__device__ __forceinline__ void wave_iid_thresholds(const float *u, int S, float *T, int lane) {
+  const int n = S + 1, ch = (n + 63) >> 6, i0 = lane * ch;
+  double tot = 0.0;
+  for (int k = 0; k < ch; ++k)
+    if (i0 + k < n) tot -= (double)__builtin_amdgcn_logf(1.0f - u[i0 + k]);
+  double incl = tot;
+  for (int d = 1; d < 64; d <<= 1) {
+    const double y = __shfl_up(incl, d);
+    incl += lane >= d ? y : 0.0;
+  }
+  for (int d = 1; d < 64; d <<= 1) {
+    const double y = __shfl_up(incl, d);
+    incl = lane >= d ? fmax(incl, y) : incl;
+  }
+  const double prev = __shfl_up(incl, 1);
+  const double total = __shfl(incl, 63);
+  const double inv = total > 0.0 ? 1.0 / total : 0.0;
+  double run = lane == 0 ? 0.0 : prev;
+  for (int k = 0; k < ch; ++k) {
+    const int i = i0 + k;
+    if (i < n) {
+      run -= (double)__builtin_amdgcn_logf(1.0f - u[i]);
+      if (i < S) T[i] = (float)(fmin(run, incl) * inv);
+    }
+  }
+}
+
 // Claims and inverse CDF of one split when the group's uniforms are few
 // (G*S <= kUStageMax): the G*S thresholds tau = ((r + u)/S) Z are numbered
 // n = r*G + h (the G heads of one r on neighbouring lanes) and thread i
@@ -433,7 +483,7 @@ __device__ __forceinline__ int lds_cdf_count(const float *Ph, int nrows, float a
 // head, so a wave usually searches once.  Counts per key go to cnt (LDS),
 // indices to idx_out.  Returns (block-uniform) whether the split holds any
 // sample.
-template <int G, bool STRAT>
+template <int G, int MODE>
 __device__ __forceinline__ bool claim_scan(const HeadClaim *hc, const float *ul, int S, float invS,
                                            const float *P, int pitch, int start, int nrows,
                                            int64_t row0, int *cnt, int32_t *__restrict__ idx_out) {
@@ -445,7 +495,7 @@ __device__ __forceinline__ bool claim_scan(const HeadClaim *hc, const float *ul,
 #pragma unroll 1
   for (int n = tid; n < G * S; n += kThreads) {
     const int r = n / G;
-    const float tau = threshold(r, STRAT ? ul[h * S + r] : ul[h], invS, c.Z);
+    const float tau = tau_of<MODE>(ul + h * (MODE == kSys ? 1 : S), r, invS, c.Z);
     if ((tau >= c.lo) & (tau < c.hi)) {
       const int pos = lds_cdf_count(Ph, nrows, c.a, tau - c.lo);
       const int j = pos < nrows ? pos : nrows - 1;
@@ -461,7 +511,7 @@ __device__ __forceinline__ bool claim_scan(const HeadClaim *hc, const float *ul,
 // non-decreasing in r (fp32 rounding is monotone), so the claimed r form the
 // range [#{r : tau_r < lo}, #{r : tau_r < hi}); threads 2h and 2h+1 count the
 // two ends by binary search.
-template <int G, bool STRAT>
+template <int G, int MODE>
 __device__ __forceinline__ void claim_ranges(const HeadClaim *hc, const float *us, int64_t ustride,
                                              int S, float invS, int *rng /* [G][2] */) {
   const int tid = threadIdx.x;
@@ -473,7 +523,7 @@ __device__ __forceinline__ void claim_ranges(const HeadClaim *hc, const float *u
     int pos = 0;
     for (int step = 1 << (31 - __clz(S)); step > 0; step >>= 1) {
       const int np = pos + step;
-      if (np <= S && threshold(np - 1, STRAT ? uh[np - 1] : uh[0], invS, c.Z) < bound) pos = np;
+      if (np <= S && tau_of<MODE>(uh, np - 1, invS, c.Z) < bound) pos = np;
     }
     rng[tid] = pos;
   }
@@ -484,7 +534,7 @@ __device__ __forceinline__ void claim_ranges(const HeadClaim *hc, const float *u
 // split): key #{j : a P_j <= tau - lo}, clamped to the split.  Counts per key
 // go to cnt (LDS), indices to idx_out.  Returns (block-uniform) whether the
 // split holds any sample.
-template <int G, bool STRAT>
+template <int G, int MODE>
 __device__ __forceinline__ bool claim_keys(const HeadClaim *hc, const int *rng, const float *us,
                                            int64_t ustride, int S, float invS, const float *P,
                                            int pitch, int start, int nrows, int64_t row0, int *cnt,
@@ -501,7 +551,7 @@ __device__ __forceinline__ bool claim_keys(const HeadClaim *hc, const int *rng, 
     for (int k = 1; k < G; ++k) h += (i >= first[k]) ? 1 : 0;
     const int r = rng[2 * h] + (i - first[h]);
     const HeadClaim c = hc[h];
-    const float tau = threshold(r, STRAT ? us[h * ustride + r] : us[h * ustride], invS, c.Z);
+    const float tau = tau_of<MODE>(us + h * ustride, r, invS, c.Z);
     const int pos = lds_cdf_count(P + h * pitch, nrows, c.a, tau - c.lo);
     const int j = pos < nrows ? pos : nrows - 1;
     atomicAdd(&cnt[h * pitch + j], 1);
@@ -568,8 +618,9 @@ __device__ __forceinline__ void gather_heads_waves(const KvView &kv, int b, int 
   }
 }
 
-template <typename E, int G, bool PAGED, bool STRAT>
+template <typename E, int G, bool PAGED, int MODE>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void k_fused_sampled(FusedArgs a) {
+  constexpr bool STRAT = MODE == kStrat;
   extern __shared__ __attribute__((aligned(16))) float dyn[];
   constexpr int pitch = kSplitMax;
   const int T = a.T;
@@ -613,12 +664,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         __hip_atomic_load(sync + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     float *part_row = a.part + (int64_t)rowkv * T * G * kHeadDim;
 
-    // uniforms of the group: G*S (stratified) or G (systematic) consecutive
-    // floats, staged in LDS when there are few of them; the first
-    // kUReg*kThreads are fetched into registers before the keys stream
-    const float *us = STRAT ? a.u + row0 * a.S : a.u + row0;
-    const int64_t ustride = STRAT ? a.S : 1;
-    const int nu = STRAT ? G * a.S : G;
+    // uniforms of the group: G*S (stratified), G*(S+1) (i.i.d.) or G
+    // (systematic) consecutive floats, staged in LDS when there are few of
+    // them (always for i.i.d.); the first kUReg*kThreads are fetched into
+    // registers before the keys stream
+    const int upr = MODE == kIid ? a.S + 1 : (STRAT ? a.S : 1);  // uniforms per head
+    const float *us = a.u + row0 * upr;
+    const int64_t ustride = upr;
+    const int nu = G * upr;
     float ureg[kUReg];
     if (a.ustage) {
 #pragma unroll
@@ -662,6 +715,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         if (i < nu) ul[i] = ureg[k];
       }
       for (int i = tid + kUReg * kThreads; i < nu; i += kThreads) ul[i] = us[i];
+      if constexpr (MODE == kIid) {
+        // each head's S + 1 uniforms become its S sorted thresholds, after
+        // the raw uniforms in LDS
+        __syncthreads();
+        for (int h = wave; h < G; h += kThreads / 64)
+          wave_iid_thresholds(ul + h * upr, a.S, ul + nu + h * a.S, lane);
+      }
     }
     row_wait_unless(sync, base + (unsigned long long)Tb, arrived, a.err);
 
@@ -674,12 +734,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     __syncthreads();
     bool has;
     if (a.ustage) {
-      has = claim_scan<G, STRAT>(hc, ul, a.S, a.invS, P, pitch, start, nrows, row0, cnt,
-                                 a.idx_out);
+      has = claim_scan<G, MODE>(hc, MODE == kIid ? ul + nu : ul, a.S, a.invS, P, pitch, start,
+                                nrows, row0, cnt, a.idx_out);
     } else {
-      claim_ranges<G, STRAT>(hc, us, ustride, a.S, a.invS, rng);
-      has = claim_keys<G, STRAT>(hc, rng, us, ustride, a.S, a.invS, P, pitch, start, nrows, row0,
-                                 cnt, a.idx_out);
+      claim_ranges<G, MODE>(hc, us, ustride, a.S, a.invS, rng);
+      has = claim_keys<G, MODE>(hc, rng, us, ustride, a.S, a.invS, P, pitch, start, nrows, row0,
+                                cnt, a.idx_out);
     }
     __syncthreads();  // counts complete; offl/all are no longer needed
     if (has) {
@@ -1187,8 +1247,9 @@ __device__ __forceinline__ int invert_threshold(const uint16_t *Qst, const float
 // chosen keys of a chunk are non-decreasing, so equal keys form runs, and each
 // run's V row is read once and added with its length: O = (1/S) sum_r
 // V_{idx_r} (Sec. 2, the stochastic add-only attention).
-template <typename E, bool PAGED, bool STRAT>
+template <typename E, bool PAGED, int MODE>
 __global__ __launch_bounds__(kThreads) void k_value_heads(FusedArgs a, int G) {
+  constexpr bool STRAT = MODE == kStrat;
   extern __shared__ __attribute__((aligned(16))) float dyn[];
   __shared__ int wave_cnt[4];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, slot = tid >> 4, c = tid & 15;
@@ -1211,6 +1272,7 @@ __global__ __launch_bounds__(kThreads) void k_value_heads(FusedArgs a, int G) {
   int *keys = reinterpret_cast<int *>(al + a.T);            // [kThreads]
   int *runs = keys + kThreads;                               // [kThreads]
   float *red = reinterpret_cast<float *>(runs + kThreads);  // [4][128]
+  float *Tq = red + 4 * kHeadDim;                            // [S] i.i.d. thresholds
   {
     // the head's block ends, in pairs (ncoarse is even)
     const float2 *src = reinterpret_cast<const float2 *>(a.coarse + rowq * ncoarse);
@@ -1218,6 +1280,9 @@ __global__ __launch_bounds__(kThreads) void k_value_heads(FusedArgs a, int G) {
     for (int i = tid; i < nc2; i += kThreads) reinterpret_cast<float2 *>(cl)[i] = src[i];
   }
   if (wave == 0) head_offsets_wave<false>(a.stats + rowq * a.T, Tb, lane, off, al);
+  if constexpr (MODE == kIid) {
+    if (wave == 1) wave_iid_thresholds(a.u + rowq * (a.S + 1), a.S, Tq, lane);
+  }
   __syncthreads();
   const float Z = off[Tb];
   const uint16_t *Qst = a.qstash + rowq * a.npitch;
@@ -1226,14 +1291,15 @@ __global__ __launch_bounds__(kThreads) void k_value_heads(FusedArgs a, int G) {
   float acc[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc[i] = 0.0f;
-  const float u0 = STRAT ? 0.0f : a.u[rowq];
+  const float u0 = MODE == kSys ? a.u[rowq] : 0.0f;
   for (int r0 = 0; r0 < a.S; r0 += kThreads) {
     const int n = min(kThreads, a.S - r0);
     const int r = r0 + tid;
     int key = 0;
     if (tid < n) {
       const float ur = STRAT ? a.u[rowq * a.S + r] : u0;
-      key = invert_threshold(Qst, cl, off, al, Tb, Ls, L, threshold(r, ur, a.invS, Z));
+      const float tau = MODE == kIid ? Tq[r] * Z : threshold(r, ur, a.invS, Z);
+      key = invert_threshold(Qst, cl, off, al, Tb, Ls, L, tau);
       keys[tid] = key;
       if (a.idx_out) a.idx_out[rowq * a.S + r] = key;
     }
@@ -1384,7 +1450,7 @@ hipError_t launch_fused_bernoulli(const Plan &p, const KvView &kv, const KtView 
     int g = G;
     void *params2[] = {&args, &g};
     const size_t lds2 = (size_t)value_heads_floats(p.T, (int)(p.npitch / kBlock)) * 4;
-    return hipExtLaunchKernel(reinterpret_cast<const void *>(&k_value_heads<E, false, false>),
+    return hipExtLaunchKernel(reinterpret_cast<const void *>(&k_value_heads<E, false, kSys>),
                               dim3(p.B * p.Hq), dim3(kThreads), params2, lds2, st, nullptr, tm.stop,
                               0);
   });
@@ -1437,7 +1503,7 @@ hipError_t launch_fused_dense(const Plan &p, const KvView &kv, const void *q, fl
 }
 
 hipError_t launch_fused_sampled(const Plan &p, const KvView &kv, const void *q, float scale_log2,
-                                bool strat, const float *u, int32_t *idx_out, void *out, char *ws,
+                                int mode, const float *u, int32_t *idx_out, void *out, char *ws,
                                 hipStream_t st) {
   FusedArgs args = make_args(p, kv, q, out, scale_log2, ws);
   args.u = u;
@@ -1456,18 +1522,23 @@ hipError_t launch_fused_sampled(const Plan &p, const KvView &kv, const void *q, 
       if (e != hipSuccess) return e;
       int g = G;
       void *params2[] = {&args, &g};
-      const size_t lds2 = (size_t)value_heads_floats(p.T, (int)(p.npitch / kBlock)) * 4;
-      const void *fn2 = strat ? reinterpret_cast<const void *>(&k_value_heads<E, PG, true>)
-                              : reinterpret_cast<const void *>(&k_value_heads<E, PG, false>);
+      const size_t lds2 = (size_t)(value_heads_floats(p.T, (int)(p.npitch / kBlock)) +
+                                   (mode == kIid ? p.S : 0)) * 4;
+      const void *fn2 = mode == kStrat ? reinterpret_cast<const void *>(&k_value_heads<E, PG, kStrat>)
+                        : mode == kIid ? reinterpret_cast<const void *>(&k_value_heads<E, PG, kIid>)
+                                       : reinterpret_cast<const void *>(&k_value_heads<E, PG, kSys>);
       return hipExtLaunchKernel(fn2, dim3(p.B * p.Hq), dim3(kThreads), params2, lds2, st, nullptr,
                                 tm.stop, 0);
     }
-    const void *fn = strat ? reinterpret_cast<const void *>(&k_fused_sampled<E, G, PG, true>)
-                           : reinterpret_cast<const void *>(&k_fused_sampled<E, G, PG, false>);
-    // stage the group's uniforms in LDS when they are few
-    const size_t nu = strat ? (size_t)G * p.S : (size_t)G;
+    const void *fn = mode == kStrat ? reinterpret_cast<const void *>(&k_fused_sampled<E, G, PG, kStrat>)
+                     : mode == kIid ? reinterpret_cast<const void *>(&k_fused_sampled<E, G, PG, kIid>)
+                                    : reinterpret_cast<const void *>(&k_fused_sampled<E, G, PG, kSys>);
+    // stage the group's uniforms in LDS when they are few (the host keeps the
+    // i.i.d. ones within the limit; their sorted thresholds follow them)
+    const size_t nu = (size_t)G * (mode == kIid ? p.S + 1 : (mode == kStrat ? p.S : 1));
     args.ustage = nu <= (size_t)kUStageMax;
-    const size_t lds = (size_t)fused_sampled_floats(G, kSplitMax, p.T, args.ustage ? (int)nu : 0) * 4;
+    const size_t staged = args.ustage ? nu + (mode == kIid ? (size_t)G * p.S : 0) : 0;
+    const size_t lds = (size_t)fused_sampled_floats(G, kSplitMax, p.T, (int)staged) * 4;
     return launch_resident(fn, p, args, lds, st);
   });
 }

@@ -51,8 +51,9 @@ hipError_t launch_fused_flash(const Plan &p, const KvView &kv, const void *q, fl
                               int tile_log2, int S_tile, const float *u, int32_t *idx_out,
                               void *out, char *ws, hipStream_t st);
 
+// mode: 0 systematic, 1 stratified, 2 i.i.d. (thresholds by exponential spacings)
 hipError_t launch_fused_sampled(const Plan &p, const KvView &kv, const void *q, float scale_log2,
-                                bool strat, const float *u, int32_t *idx_out, void *out, char *ws,
+                                int mode, const float *u, int32_t *idx_out, void *out, char *ws,
                                 hipStream_t st);
 
 // Compile-time dispatch over the GQA group size, element type and cache kind.

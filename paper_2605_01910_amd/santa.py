@@ -21,13 +21,13 @@ LIB_PATH = os.path.join(_HERE, "libsanta.so")
 SANTA_OK, SANTA_ERR_INVALID_ARG, SANTA_ERR_UNSUPPORTED, SANTA_ERR_WORKSPACE, SANTA_ERR_HIP = range(5)
 SANTA_BF16, SANTA_F32 = 0, 1
 (SANTA_KIND_DENSE, SANTA_KIND_SYSTEMATIC, SANTA_KIND_STRATIFIED, SANTA_KIND_BERNOULLI,
- SANTA_KIND_FLASH) = range(5)
+ SANTA_KIND_FLASH, SANTA_KIND_IID) = range(6)
 
 # every symbol include/santa.h declares
 EXPORTS = ("santa_workspace_size", "santa_workspace_init", "santa_decode_dense",
            "santa_decode_systematic", "santa_decode_stratified", "santa_decode_bernoulli_qk",
-           "santa_decode_flash", "santa_time_next_call", "santa_status_string",
-           "santa_last_error")
+           "santa_decode_iid", "santa_decode_flash", "santa_time_next_call",
+           "santa_status_string", "santa_last_error")
 
 
 class SantaError(RuntimeError):
@@ -79,13 +79,14 @@ def load() -> ctypes.CDLL:
     L.santa_decode_bernoulli_qk.argtypes = [P, TP, KP, SP, ctypes.c_float, I32, I32, P, I32, P,
                                             P, P, P, P, SZ, P]
     L.santa_decode_flash.argtypes = [P, KP, SP, ctypes.c_float, I32, I32, P, P, P, P, SZ, P]
+    L.santa_decode_iid.argtypes = [P, KP, SP, ctypes.c_float, I32, P, P, P, P, SZ, P]
     L.santa_time_next_call.argtypes = [P, P]
     L.santa_status_string.argtypes = [ctypes.c_int]
     L.santa_status_string.restype = ctypes.c_char_p
     L.santa_last_error.restype = ctypes.c_char_p
     for name in ("santa_workspace_init", "santa_decode_dense", "santa_decode_systematic",
                  "santa_decode_stratified", "santa_decode_bernoulli_qk", "santa_decode_flash",
-                 "santa_time_next_call"):
+                 "santa_decode_iid", "santa_time_next_call"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -224,6 +225,14 @@ def santa_decode_bernoulli_qk(q: torch.Tensor, kt: santa_kt_t, kv: santa_kv_t,
                                             int(mode), _ptr(u_q), int(S), _ptr(u), _ptr(idx_out),
                                             _ptr(feat_mask_out), _ptr(out), _ptr(ws),
                                             ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def santa_decode_iid(q: torch.Tensor, kv: santa_kv_t, shape: santa_shape_t, scale: float,
+                     S: int, u: torch.Tensor, idx_out: Optional[torch.Tensor], out: torch.Tensor,
+                     ws: torch.Tensor, stream=None) -> None:
+    _check(load().santa_decode_iid(_ptr(q), ctypes.byref(kv), ctypes.byref(shape), float(scale),
+                                   int(S), _ptr(u), _ptr(idx_out), _ptr(out), _ptr(ws),
+                                   ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def santa_decode_flash(q: torch.Tensor, kv: santa_kv_t, shape: santa_shape_t, scale: float,

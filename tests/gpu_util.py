@@ -24,7 +24,7 @@ BAND = 1e-5
 DENSE_MAX_ABS, DENSE_REL_L2, SAMPLED_MAX_ABS = 2e-2, 5e-3, 2e-2
 KIND_CODE = {"dense": S.SANTA_KIND_DENSE, "systematic": S.SANTA_KIND_SYSTEMATIC,
              "stratified": S.SANTA_KIND_STRATIFIED, "bernoulli": S.SANTA_KIND_BERNOULLI,
-             "flash": S.SANTA_KIND_FLASH}
+             "flash": S.SANTA_KIND_FLASH, "iid": S.SANTA_KIND_IID}
 
 
 def log(msg: str) -> None:
@@ -89,6 +89,8 @@ def run(w, kind: Optional[str] = None, layout: str = "nhd", want_idx: bool = Tru
         S.santa_decode_stratified(dw.q, dw.kv, dw.shape, w.scale, Sn, dw.u, idx, out, ws)
     elif kind == "flash":
         S.santa_decode_flash(dw.q, dw.kv, dw.shape, w.scale, w.tile, w.S_tile, dw.u, idx, out, ws)
+    elif kind == "iid":
+        S.santa_decode_iid(dw.q, dw.kv, dw.shape, w.scale, Sn, dw.u, idx, out, ws)
     elif kind == "bernoulli":
         if want_mask:
             mask = torch.full((w.B, w.Hkv, w.d), 7, dtype=torch.uint8, device="cuda")
@@ -115,6 +117,8 @@ def check_dense(w, out: np.ndarray, rows: Optional[Sequence[int]] = None) -> dic
 def _thresholds(w, kind: str, row: int) -> np.ndarray:
     if kind == "stratified":
         return O.thresholds("stratified", w.u.reshape(-1, w.S)[row], w.S)
+    if kind == "iid":
+        return O.thresholds("iid_spacings", w.u.reshape(-1, w.S + 1)[row], w.S)
     return O.thresholds("systematic", w.u.reshape(-1)[row:row + 1], w.S)
 
 
@@ -135,7 +139,7 @@ def check_sampled(w, out: np.ndarray, idx: np.ndarray, kind: Optional[str] = Non
         assert np.all((g >= 0) & (g < L)), f"row {r}: index out of range {g.min()}..{g.max()}"
         o_idx = res.idx[i]
         C = res.cdf[i, :L]
-        T = _thresholds(w, "stratified" if kind == "stratified" else "systematic", r)
+        T = _thresholds(w, kind if kind in ("stratified", "iid") else "systematic", r)
         diff = np.nonzero(g != o_idx)[0]
         for m in diff:
             gm = int(g[m])

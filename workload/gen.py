@@ -258,13 +258,15 @@ def make_workload(cfg: int, seed: int = 0, **over) -> Workload:
         w.k, w.v = k, v
         del k_seq, v_seq
 
-    # value-stage uniforms: one per row (systematic), S per row (stratified) or
-    # one per row and tile (flash)
+    # value-stage uniforms: one per row (systematic), S per row (stratified),
+    # S + 1 per row (i.i.d. by exponential spacings) or one per row and tile (flash)
     ru = _rng(cfg, STREAM_U, seed)
     if kind in ("systematic", "bernoulli"):
         w.u = ru.random((B, Hq), dtype=np.float32)
     elif kind == "stratified":
         w.u = ru.random((B, Hq, S), dtype=np.float32)
+    elif kind == "iid":
+        w.u = ru.random((B, Hq, S + 1), dtype=np.float32)
     elif kind == "flash":
         w.tile = int(p.get("tile", 256))
         w.S_tile = int(p.get("S_tile", 16))
