@@ -48,7 +48,7 @@ def parse():
     ap.add_argument("--B", type=int, default=None)
     ap.add_argument("--S", type=int, default=None)
     ap.add_argument("--kind", default=None,
-                    help="dense | systematic | stratified | bernoulli | flash")
+                    help="dense | systematic | stratified | iid | bernoulli | flash")
     ap.add_argument("--tile", type=int, default=256, help="flash: keys per tile")
     ap.add_argument("--S-tile", type=int, default=None,
                     help="flash: draws per tile (default: the budget rule S_tile ~ S / T)")
@@ -119,6 +119,8 @@ def main():
         elif kind == "flash":
             S.santa_decode_flash(dw.q, dw.kv, dw.shape, w.scale, w.tile, w.S_tile, dw.u, idx_out,
                                  out, ws, stream)
+        elif kind == "iid":
+            S.santa_decode_iid(dw.q, dw.kv, dw.shape, w.scale, w.S, dw.u, idx_out, out, ws, stream)
         else:
             S.santa_decode_dense(dw.q, dw.kv, dw.shape, w.scale, out, ws, stream)
 
