@@ -13,6 +13,8 @@ namespace santa {
 constexpr float kInf = __builtin_huge_valf();
 
 typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2_t;
+typedef unsigned int nt_u32x4 __attribute__((ext_vector_type(4)));
+typedef float nt_f32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -36,6 +38,12 @@ struct Chunk<uint16_t> {
   __device__ __forceinline__ static Chunk zero() { return Chunk{make_uint4(0, 0, 0, 0)}; }
   __device__ __forceinline__ static Chunk load(const uint16_t *p) {
     return Chunk{*reinterpret_cast<const uint4 *>(p)};
+  }
+  // non-temporal (nt): for rows streamed once, so they do not displace
+  // reused lines in L2 and the memory-side cache
+  __device__ __forceinline__ static Chunk load_nt(const uint16_t *p) {
+    const nt_u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const nt_u32x4 *>(p));
+    return Chunk{make_uint4(v[0], v[1], v[2], v[3])};
   }
   __device__ __forceinline__ void to_float(float (&f)[8]) const {
     f[0] = bf16_lo(w.x); f[1] = bf16_hi(w.x); f[2] = bf16_lo(w.y); f[3] = bf16_hi(w.y);
@@ -61,6 +69,11 @@ struct Chunk<float> {
   }
   __device__ __forceinline__ static Chunk load(const float *p) {
     return Chunk{reinterpret_cast<const float4 *>(p)[0], reinterpret_cast<const float4 *>(p)[1]};
+  }
+  __device__ __forceinline__ static Chunk load_nt(const float *p) {
+    const nt_f32x4 x = __builtin_nontemporal_load(reinterpret_cast<const nt_f32x4 *>(p));
+    const nt_f32x4 y = __builtin_nontemporal_load(reinterpret_cast<const nt_f32x4 *>(p) + 1);
+    return Chunk{make_float4(x[0], x[1], x[2], x[3]), make_float4(y[0], y[1], y[2], y[3])};
   }
   __device__ __forceinline__ void to_float(float (&f)[8]) const {
     f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w; f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;

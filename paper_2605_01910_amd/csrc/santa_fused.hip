@@ -1140,7 +1140,7 @@ __global__ __launch_bounds__(kThreads) void k_bern_stream(FusedArgs a, KtView kt
       for (; fi + (UF - 1) * FS < nf; fi += UF * FS) {
         Chunk<E> ch[UF];
 #pragma unroll
-        for (int u = 0; u < UF; ++u) ch[u] = Chunk<E>::load(ktb + (int64_t)fl[fi + u * FS] * kt.sd + p0);
+        for (int u = 0; u < UF; ++u) ch[u] = Chunk<E>::load_nt(ktb + (int64_t)fl[fi + u * FS] * kt.sd + p0);
 #pragma unroll
         for (int u = 0; u < UF; ++u) {
           float kf[8];
@@ -1154,7 +1154,7 @@ __global__ __launch_bounds__(kThreads) void k_bern_stream(FusedArgs a, KtView kt
       const E *rp = ktb + (int64_t)i * kt.sd + p0;
       float kf[8];
       if (full) {
-        Chunk<E>::load(rp).to_float(kf);
+        Chunk<E>::load_nt(rp).to_float(kf);
       } else {
 #pragma unroll
         for (int e = 0; e < 8; ++e) kf[e] = p0 + e < L ? to_f32(rp[e]) : 0.0f;

@@ -103,11 +103,15 @@ __device__ __forceinline__ int64_t row16_offset(const KvView &kv, const PageWin 
 }
 
 // 16 bytes at byte offset lb from p through a buffer resource (uniform base in
-// scalar registers, one 32-bit lane offset; no range limit is used).
+// scalar registers, one 32-bit lane offset; no range limit is used).  The load
+// is non-temporal (cache-policy bit nt = 2): every key is read once per step,
+// and marking the stream so keeps it from evicting the lines that are reused
+// (the CDF stash, statistics, gathered value rows); measured, it also streams
+// faster than the default policy.
 __device__ __forceinline__ uint4 buffer_load16(const void *p, uint32_t lb) {
   const __amdgpu_buffer_rsrc_t rs =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), 0, 0x7fffffff, 0x00020000);
-  const auto v = __builtin_amdgcn_raw_buffer_load_b128(rs, lb, 0, 0);
+  const auto v = __builtin_amdgcn_raw_buffer_load_b128(rs, lb, 0, 2);
   return make_uint4(v[0], v[1], v[2], v[3]);
 }
 
@@ -118,7 +122,7 @@ __device__ __forceinline__ Chunk<E> load_key_row(const E *base, const KvView &kv
                                                  int b, int kvh, int row0, int slot, int c,
                                                  uint32_t lb) {
   if constexpr (PAGED) {
-    if (kv.ps_log2 < 4) return Chunk<E>::load(base + row_offset<true>(kv, b, kvh, row0 + slot) + c * 8);
+    if (kv.ps_log2 < 4) return Chunk<E>::load_nt(base + row_offset<true>(kv, b, kvh, row0 + slot) + c * 8);
   }
   const E *p = base + row16_offset<PAGED>(kv, pw, b, kvh, row0);
   if constexpr (sizeof(E) == 2) {
@@ -607,7 +611,7 @@ __device__ __forceinline__ void gather_union(const KvView &kv, int b, int kvh, i
       const int e = e0 + uu * 16;
       jj[uu] = e < nlist ? list[e] : -1;
       ch[uu] = jj[uu] >= 0
-                   ? Chunk<E>::load(V + row_offset<PAGED>(kv, b, kvh, start + jj[uu]) + c * 8)
+                   ? Chunk<E>::load_nt(V + row_offset<PAGED>(kv, b, kvh, start + jj[uu]) + c * 8)
                    : Chunk<E>::zero();
     }
 #pragma unroll
