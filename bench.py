@@ -18,7 +18,11 @@ kernel of the same library is timed the same way on the same inputs.
 
 value = algorithmic bytes / mean step time, where algorithmic bytes = all keys
 + the unique value rows the step gathers (counted from idx_out in an untimed
-call) + q + out + uniforms.  Prints one JSON line.
+call) + q + out + uniforms.  `attainable_read` times the library's
+streaming-read calibration kernel (santa_stream_read) over the same number of
+bytes under the same protocol: the rate a plain read of those bytes reaches on
+this device, and the step's kernel rate as a fraction of it.  Prints one JSON
+line.
 """
 
 from __future__ import annotations
@@ -212,6 +216,16 @@ def main():
         res["speedup_vs_dense"] = round(float(dus.mean() / us.mean()), 3)
         print(f"[bench] dense: call mean {dus.mean():.2f} us | kernel mean {dkus.mean():.2f} us",
               file=sys.stderr, flush=True)
+    # attainable rate: the streaming-read calibration kernel on a buffer of the
+    # step's algorithmic byte count, same cold-cache protocol and timing
+    rd_bytes = (alg_bytes // 16) * 16
+    rd_buf = torch.zeros(rd_bytes // 4, dtype=torch.float32, device=dev)
+    rd_sink = torch.empty(S.STREAM_READ_GROUPS, dtype=torch.int32, device=dev)
+    _, rdk = timed(lambda: S.santa_stream_read(rd_buf, rd_sink, stream), args.steps, args.warmup)
+    del rd_buf
+    rd_gbs = rd_bytes / (rdk.mean() * 1e-6) / 1e9
+    print(f"[bench] streaming read of {rd_bytes} B: kernel mean {rdk.mean():.2f} us "
+          f"({rd_gbs:.0f} GB/s)", file=sys.stderr, flush=True)
     if not args.profile:
         warm, wk = timed(step, args.steps, 2, cold=False)
         res["warm_us_per_step"] = round(float(warm.mean()), 3)
@@ -268,6 +282,15 @@ def main():
             "frac": round(kgbs / PEAK_HBM_GBS, 4),
             "traffic": None,
         },
+        "attainable_read": {
+            "kernel": "k_stream_read (santa_stream_read)",
+            "bytes": rd_bytes,
+            "kernel_us": round(float(rdk.mean()), 3),
+            "achieved": round(rd_gbs, 1),
+            "unit": "GB/s",
+            "frac_of_peak": round(rd_gbs / PEAK_HBM_GBS, 4),
+            "step_frac": round(kgbs / rd_gbs, 4),
+        },
         "timed_wall_s": round(wall, 3),
     }
 
@@ -303,13 +326,16 @@ def kernel_label(w, kind: str) -> str:
 
 
 def kernel_source_hash() -> str:
-    """Hash of the HIP sources (file names and contents), as recorded with the
-    counter runs under profiles/."""
+    """Hash of the decode kernels' HIP sources (file names and contents), as
+    recorded with the counter runs under profiles/ (the streaming-read
+    calibration kernel's file is not part of it)."""
     import glob
     import hashlib
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2605_01910_amd", "csrc")
     for f in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.h"))):
+        if os.path.basename(f) == "santa_measure.hip":
+            continue
         h.update(os.path.basename(f).encode())
         with open(f, "rb") as fh:
             h.update(fh.read())

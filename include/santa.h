@@ -211,8 +211,9 @@ santa_status_t santa_decode_flash(const void *q, const santa_kv_t *kv, const san
 
 /* Profiling hook (not part of the method).  start_event and stop_event are
  * hipEvent_t handles created by the caller with timing enabled.  The next
- * santa_decode_* call made on the calling thread attaches them to its own
- * kernels: the GPU records start_event when the call's first kernel is
+ * santa_decode_* (or santa_stream_read) call made on the calling thread
+ * attaches them to its own kernels: the GPU records start_event when the
+ * call's first kernel is
  * dispatched and stop_event when its last kernel completes, so
  * hipEventElapsedTime(start, stop) is the call's execution time on the device
  * without host launch latency.  One-shot: that call consumes the request even
@@ -220,6 +221,22 @@ santa_status_t santa_decode_flash(const void *q, const santa_kv_t *kv, const san
  * NULL is SANTA_ERR_INVALID_ARG.  The events stay owned by the caller and must
  * outlive the call's kernels. */
 santa_status_t santa_time_next_call(void *start_event, void *stop_event);
+
+/* Measurement helper (not part of the method): the attainable HBM read rate.
+ * Streams `bytes` from the device buffer buf with the load the decode kernels
+ * use for keys (16 bytes per lane, non-temporal, up to 16 loads in flight per
+ * lane) over at most SANTA_STREAM_READ_GROUPS workgroups, each reading one
+ * contiguous share, and writes to sink[w] (device,
+ * caller-owned, SANTA_STREAM_READ_GROUPS uint32) the XOR of all 32-bit words
+ * workgroup w read; words past the grid keep their contents, so with sink
+ * zeroed first the XOR over sink is the XOR over the buffer.  buf must be
+ * 16-byte aligned and bytes a positive multiple of 16 below
+ * 2^34 * SANTA_STREAM_READ_GROUPS (else SANTA_ERR_INVALID_ARG).  Asynchronous
+ * on `stream`; santa_time_next_call applies to it as to a decode call.  Timed
+ * on a buffer the size of a step's algorithmic bytes, it is the ceiling those
+ * bytes can be read at. */
+#define SANTA_STREAM_READ_GROUPS 4096
+santa_status_t santa_stream_read(const void *buf, size_t bytes, uint32_t *sink, void *stream);
 
 /* Human-readable name of a status code. */
 const char *santa_status_string(santa_status_t status);

@@ -13,7 +13,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libsanta.so")
-SOURCES = ["santa_api.hip", "santa_kernels.hip", "santa_fused.hip"]
+SOURCES = ["santa_api.hip", "santa_kernels.hip", "santa_fused.hip", "santa_measure.hip"]
 ARCH = "gfx950"
 
 

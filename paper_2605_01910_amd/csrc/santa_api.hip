@@ -395,6 +395,18 @@ santa_status_t santa_decode_flash(const void *q, const santa_kv_t *kv, const san
                                               static_cast<hipStream_t>(stream)));
 }
 
+santa_status_t santa_stream_read(const void *buf, size_t bytes, uint32_t *sink, void *stream) {
+  TimerScope timer_scope;
+  g_last_error.clear();
+  if (!buf || !sink) return fail(SANTA_ERR_INVALID_ARG, "buf or sink is NULL");
+  if (bytes == 0 || bytes % 16) return fail(SANTA_ERR_INVALID_ARG, "bytes must be a positive multiple of 16");
+  if (bytes / 16 / SANTA_STREAM_READ_GROUPS >= (size_t(1) << 30))
+    return fail(SANTA_ERR_INVALID_ARG, "bytes too large");
+  if (reinterpret_cast<uintptr_t>(buf) & 15) return fail(SANTA_ERR_INVALID_ARG, "buf must be 16-byte aligned");
+  return hip_status(santa::launch_stream_read(buf, bytes, sink, SANTA_STREAM_READ_GROUPS,
+                                              static_cast<hipStream_t>(stream)));
+}
+
 santa_status_t santa_time_next_call(void *start_event, void *stop_event) {
   g_last_error.clear();
   if ((start_event == nullptr) != (stop_event == nullptr))

@@ -12,7 +12,7 @@ namespace santa {
 // Events the GPU records around the kernels of one call (santa_time_next_call):
 // `start` when the call's first kernel is dispatched, `stop` when its last
 // kernel completes.  Null events launch normally.  Thread-local, consumed by
-// the next santa_decode_* call on the thread.
+// the next santa_decode_* or santa_stream_read call on the thread.
 struct CallTimer {
   hipEvent_t start = nullptr;
   hipEvent_t stop = nullptr;
@@ -32,6 +32,12 @@ hipError_t launch_bernoulli(const Plan &p, const KvView &kv, const KtView &kt, c
                             hipStream_t st);
 
 hipError_t launch_zero(void *ws, size_t bytes, hipStream_t st);
+
+// Streaming-read calibration (santa_stream_read): at most `max_groups`
+// workgroups read `bytes` (a multiple of 16) from buf; sink[w] gets workgroup
+// w's XOR fold (words past the grid are left as they were).
+hipError_t launch_stream_read(const void *buf, size_t bytes, uint32_t *sink, int max_groups,
+                              hipStream_t st);
 
 // Bernoulli query weights, selected-feature lists and the feature mask of
 // every GQA group (k_bern_prep); `start` (nullable) is recorded at dispatch.

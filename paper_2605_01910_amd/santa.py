@@ -26,8 +26,10 @@ SANTA_BF16, SANTA_F32 = 0, 1
 # every symbol include/santa.h declares
 EXPORTS = ("santa_workspace_size", "santa_workspace_init", "santa_decode_dense",
            "santa_decode_systematic", "santa_decode_stratified", "santa_decode_bernoulli_qk",
-           "santa_decode_iid", "santa_decode_flash", "santa_time_next_call",
+           "santa_decode_iid", "santa_decode_flash", "santa_stream_read", "santa_time_next_call",
            "santa_status_string", "santa_last_error")
+
+STREAM_READ_GROUPS = 4096  # SANTA_STREAM_READ_GROUPS: uint32 words of the sink
 
 
 class SantaError(RuntimeError):
@@ -80,13 +82,14 @@ def load() -> ctypes.CDLL:
                                             P, P, P, P, SZ, P]
     L.santa_decode_flash.argtypes = [P, KP, SP, ctypes.c_float, I32, I32, P, P, P, P, SZ, P]
     L.santa_decode_iid.argtypes = [P, KP, SP, ctypes.c_float, I32, P, P, P, P, SZ, P]
+    L.santa_stream_read.argtypes = [P, SZ, P, P]
     L.santa_time_next_call.argtypes = [P, P]
     L.santa_status_string.argtypes = [ctypes.c_int]
     L.santa_status_string.restype = ctypes.c_char_p
     L.santa_last_error.restype = ctypes.c_char_p
     for name in ("santa_workspace_init", "santa_decode_dense", "santa_decode_systematic",
                  "santa_decode_stratified", "santa_decode_bernoulli_qk", "santa_decode_flash",
-                 "santa_decode_iid", "santa_time_next_call"):
+                 "santa_decode_iid", "santa_stream_read", "santa_time_next_call"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -250,9 +253,26 @@ def flash_tile_budget(S: int, n_tiles: int) -> int:
     return max(1, (2 * int(S) + int(n_tiles)) // (2 * int(n_tiles)))
 
 
+def santa_stream_read(buf, sink, stream=None) -> None:
+    """Stream all bytes of the CUDA tensor `buf` (16-byte aligned, a multiple of
+    16 bytes) through the decode kernels' key load; `sink` is an int32 CUDA
+    tensor of STREAM_READ_GROUPS words whose first words receive each
+    workgroup's XOR fold of what it read (the rest keep their contents).  A measurement helper: timed with santa_time_next_call, it
+    gives the attainable read rate for that many bytes."""
+    if not (buf.is_cuda and sink.is_cuda):
+        raise ValueError("buf and sink must be CUDA tensors")
+    if sink.dtype != torch.int32 or sink.numel() < STREAM_READ_GROUPS or not sink.is_contiguous():
+        raise ValueError(f"sink must be a contiguous int32 tensor of >= {STREAM_READ_GROUPS} words")
+    if not buf.is_contiguous():
+        raise ValueError("buf must be contiguous")
+    _check(load().santa_stream_read(ctypes.c_void_p(buf.data_ptr()),
+                                    ctypes.c_size_t(buf.numel() * buf.element_size()),
+                                    ctypes.c_void_p(sink.data_ptr()), _stream(stream)))
+
+
 def santa_time_next_call(start, stop) -> None:
-    """Attach two timing events to the kernels of the next santa_decode_* call on
-    this thread (start: first kernel dispatched, stop: last kernel done).
+    """Attach two timing events to the kernels of the next santa_decode_* (or
+    santa_stream_read) call on this thread (start: first kernel dispatched, stop: last kernel done).
     `start`/`stop` are torch.cuda.Event objects that have been recorded at least
     once (so their HIP event exists), raw hipEvent_t handles, or both None."""
     def handle(e):

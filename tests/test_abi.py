@@ -116,3 +116,16 @@ def test_time_next_call_needs_both_events_or_neither():
     assert st == S.SANTA_ERR_INVALID_ARG
     assert b"both" in lib.santa_last_error()
     assert lib.santa_time_next_call(None, None) == S.SANTA_OK
+
+
+def test_stream_read_validation():
+    # every rejection happens on the host, before a launch
+    lib = S.load()
+    P = ctypes.c_void_p
+    ok_buf, ok_sink = P(0x100000), P(0x200000)
+    assert lib.santa_stream_read(None, 1024, ok_sink, None) == S.SANTA_ERR_INVALID_ARG
+    assert lib.santa_stream_read(ok_buf, 1024, None, None) == S.SANTA_ERR_INVALID_ARG
+    assert lib.santa_stream_read(ok_buf, 0, ok_sink, None) == S.SANTA_ERR_INVALID_ARG
+    assert lib.santa_stream_read(ok_buf, 1000, ok_sink, None) == S.SANTA_ERR_INVALID_ARG
+    assert lib.santa_stream_read(P(0x100008), 1024, ok_sink, None) == S.SANTA_ERR_INVALID_ARG
+    assert b"aligned" in lib.santa_last_error()
