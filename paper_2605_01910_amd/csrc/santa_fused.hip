@@ -474,15 +474,14 @@ __device__ __forceinline__ void wave_iid_thresholds(const float *u, int S, float
   }
 }
 
-// Claims and inverse CDF of one split when the group's uniforms are few
-// (G*S <= kUStageMax): the G*S thresholds tau = ((r + u)/S) Z are numbered
-// n = r*G + h (the G heads of one r on neighbouring lanes) and thread i
-// evaluates n = i, i + kThreads, ...; those with lo <= tau < hi belong to this
-// split and map to the key #{j : a P_j <= tau - lo} (the CDF interval holding
-// tau, App. A), clamped to the split.  A split's claims form one range of r per
-// head, so a wave usually searches once.  Counts per key go to cnt (LDS),
-// indices to idx_out.  Returns (block-uniform) whether the split holds any
-// sample.
+// Claims and inverse CDF of one split for thresholds held in LDS without a
+// closed-form count (the i.i.d. mode's sorted T_r Z; G*S <= kUStageMax): the
+// G*S thresholds are numbered n = r*G + h (the G heads of one r on
+// neighbouring lanes) and thread i evaluates n = i, i + kThreads, ...; those
+// with lo <= tau < hi belong to this split and map to the key #{j : a P_j <=
+// tau - lo} (the CDF interval holding tau, App. A), clamped to the split.
+// Counts per key go to cnt (LDS), indices to idx_out.  Returns (block-uniform)
+// whether the split holds any sample.
 template <int G, int MODE>
 __device__ __forceinline__ bool claim_scan(const HeadClaim *hc, const float *ul, int S, float invS,
                                            const float *P, int pitch, int start, int nrows,
@@ -505,6 +504,55 @@ __device__ __forceinline__ bool claim_scan(const HeadClaim *hc, const float *ul,
     }
   }
   return __syncthreads_or(any) != 0;
+}
+
+// Number of one head's thresholds below y, N(y) = #{r < S : tau_r < y}, for
+// sorted thresholds (kSys, kStrat; uniforms in LDS).  tau_r is non-decreasing
+// in r (its fp32 evaluation is monotone), so N is its closed-form estimate --
+// kSys: ceil(y S/Z - u); kStrat: floor(y S/Z) + 1, the strata up to y's --
+// corrected until tau_{N-1} < y <= tau_N holds for tau as evaluated by the
+// claims (tau_of).  The estimate is off by at most one step of fp32 rounding
+// for S below 2^23: both neighbours are checked at once, and a loop only runs
+// when a check fails.  u0 is the head's uniform (kSys); sZ = S / Z; y = +inf
+// gives S.
+template <int MODE>
+__device__ __forceinline__ int count_below(const float *uh, float u0, int S, float invS, float Z,
+                                           float sZ, float y) {
+  static_assert(MODE == kSys || MODE == kStrat, "sorted thresholds with a closed form");
+  auto tau = [&](int r) {
+    return MODE == kSys ? threshold(r, u0, invS, Z) : tau_of<MODE>(uh, r, invS, Z);
+  };
+  const float q = fminf(y * sZ, (float)S + 2.0f);
+  int n = MODE == kSys ? (int)ceilf(q - u0) : (int)floorf(q) + 1;
+  n = min(max(n, 0), S);
+  const float tm = n > 0 ? tau(n - 1) : -kInf;
+  const float tp = n < S ? tau(n) : kInf;
+  if (tm >= y) {
+    --n;
+    while (n > 0 && tau(n - 1) >= y) --n;
+  } else if (tp < y) {
+    ++n;
+    while (n < S && tau(n) < y) ++n;
+  }
+  return n;
+}
+
+// Claimed ranges of one split for sorted thresholds (kSys, kStrat; uniforms
+// in LDS): head h claims r in [N(lo), N(hi)) -- exactly the r with lo <= tau_r
+// < hi -- found in closed form by threads 2h and 2h + 1 (count_below), so
+// claim_keys then inverts only the claimed thresholds.  rng: [G][2] (LDS).
+template <int G, int MODE>
+__device__ __forceinline__ void claim_ranges_closed(const HeadClaim *hc, const float *ul, int S,
+                                                    float invS, int *rng) {
+  const int tid = threadIdx.x;
+  if (tid < 2 * G) {
+    const int h = tid >> 1;
+    const HeadClaim c = hc[h];
+    const float *uh = ul + h * (MODE == kSys ? 1 : S);
+    rng[tid] = count_below<MODE>(uh, MODE == kSys ? uh[0] : 0.0f, S, invS, c.Z, (float)S / c.Z,
+                                 (tid & 1) ? c.hi : c.lo);
+  }
+  __syncthreads();
 }
 
 // Threshold r of head h is claimed iff lo <= tau_r < hi.  tau_r is
@@ -560,20 +608,20 @@ __device__ __forceinline__ bool claim_keys(const HeadClaim *hc, const int *rng, 
   return total > 0;
 }
 
-// Value stage of one split with one query head per wave (G >= 4): after the
-// union of chosen keys is compacted, wave w accumulates heads w, w + 4, ...
-// over the whole list (4 rows per wave instruction, 4 rows in flight per row
-// slot), sums its 4 row slots with lane swaps and writes the heads' 128
-// partial sums directly: O_h += c_{h,j} V_j (Sec. 2, the stochastic add-only
-// attention).  FW: cnt holds float weights (bit patterns) instead of counts.
+// Value stage of one split with one query head per wave (G >= 4), for a short
+// compacted union list (list[0..nlist), the group's chosen keys in key order):
+// wave w accumulates heads w, w + 4, ... over the whole list (4 rows per wave
+// instruction, 4 rows in flight per row slot), sums its 4 row slots with lane
+// swaps and writes the heads' 128 partial sums directly, with no workgroup
+// reduction: O_h += c_{h,j} V_j (Sec. 2, the stochastic add-only attention).
+// FW: cnt holds float weights (bit patterns) instead of counts.
 template <typename E, int G, bool PAGED, bool FW = false>
 __device__ __forceinline__ void gather_heads_waves(const KvView &kv, int b, int kvh, int start,
-                                                   int nrows, const int *cnt, int pitch, int *list,
-                                                   float *__restrict__ part_out) {
+                                                   const int *cnt, int pitch, const int *list,
+                                                   int nlist, float *__restrict__ part_out) {
   static_assert(G % 4 == 0, "one head per wave needs G >= 4");
   constexpr int HW = G / 4, U = 4;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, rs = lane >> 4, c = lane & 15;
-  const int nlist = compact_union<G>(cnt, pitch, nrows, list);
   const E *V = static_cast<const E *>(kv.v);
   float acc[HW][8];
 #pragma unroll
@@ -632,7 +680,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   float *ul = reinterpret_cast<float *>(list + fused_list_ints(G, pitch, T));
   __shared__ HeadClaim hc[G];
   __shared__ float mh[G], lh[G], mtmp[8 * G];
-  __shared__ int wave_cnt[4], rank_lds, rng[2 * G];
+  __shared__ int rank_lds, rng[2 * G];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nrk = a.B * a.Hkv;
@@ -733,9 +781,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     }
     __syncthreads();
     bool has;
-    if (a.ustage) {
-      has = claim_scan<G, MODE>(hc, MODE == kIid ? ul + nu : ul, a.S, a.invS, P, pitch, start,
-                                nrows, row0, cnt, a.idx_out);
+    if (a.ustage && MODE != kIid) {
+      constexpr int M = MODE == kIid ? kSys : MODE;
+      claim_ranges_closed<G, M>(hc, ul, a.S, a.invS, rng);
+      has = claim_keys<G, M>(hc, rng, ul, M == kSys ? 1 : a.S, a.S, a.invS, P, pitch, start,
+                             nrows, row0, cnt, a.idx_out);
+    } else if (a.ustage) {
+      has = claim_scan<G, MODE>(hc, ul + nu, a.S, a.invS, P, pitch, start, nrows, row0, cnt,
+                                a.idx_out);
     } else {
       claim_ranges<G, MODE>(hc, us, ustride, a.S, a.invS, rng);
       has = claim_keys<G, MODE>(hc, rng, us, ustride, a.S, a.invS, P, pitch, start, nrows, row0,
@@ -743,12 +796,22 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     }
     __syncthreads();  // counts complete; offl/all are no longer needed
     if (has) {
-      if constexpr (G >= 4)
-        gather_heads_waves<E, G, PAGED>(a.kv, b, kvh, start, nrows, cnt, pitch, list,
-                                        part_row + (int64_t)t * G * kHeadDim);
-      else
-        gather_union<E, G, PAGED, true>(a.kv, b, kvh, start, nrows, P, pitch, cnt, list, wave_cnt,
-                                        part_row + (int64_t)t * G * kHeadDim);
+      float *po = part_row + (int64_t)t * G * kHeadDim;
+      if constexpr (G >= 4) {
+        // a short union (one pass of a wave's 16 rows) goes one head per wave,
+        // with no workgroup reduction; a long one (large S) is shared by all
+        // 16 row slots of the workgroup, so it takes nlist / (16 UG) dependent
+        // passes instead of nlist / 16
+        const int nlist = compact_union<G>(cnt, pitch, nrows, list);
+        constexpr int UG = (sizeof(E) == 2 && G <= 4) ? 8 : 4;
+        if (nlist <= 16)
+          gather_heads_waves<E, G, PAGED>(a.kv, b, kvh, start, cnt, pitch, list, nlist, po);
+        else
+          gather_list<E, G, PAGED, true, false, UG>(a.kv, b, kvh, start, list, nlist, P, pitch,
+                                                    cnt, po);
+      } else {
+        gather_union<E, G, PAGED, true>(a.kv, b, kvh, start, nrows, P, pitch, cnt, list, po);
+      }
     } else {  // a split without samples contributes zeros
       float2 *pz = reinterpret_cast<float2 *>(part_row + (int64_t)t * G * kHeadDim);
       for (int o2 = tid; o2 < G * kHeadDim / 2; o2 += kThreads) st_coherent(pz + o2, make_float2(0.f, 0.f));
@@ -793,7 +856,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(PERSIS
   int *list = cnt + imax(G * pitch, imax(4 * G * kHeadDim, a.T + kThreads));
   float *tst = reinterpret_cast<float *>(list + pitch);
   __shared__ float mh[G], lh[G], mtmp[4 * G], den;
-  __shared__ int rank_lds, wave_cnt[4];
+  __shared__ int rank_lds;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, c = tid & 15;
   const int nrk = a.B * a.Hkv, T = a.T;
@@ -861,7 +924,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(PERSIS
       if (has) {
         constexpr int UG = (sizeof(E) == 2 && G <= 4) ? 8 : 4;
         gather_union<E, G, PAGED, true, true, UG>(a.kv, b, kvh, start, nrows, s, pitch, cnt, list,
-                                                  wave_cnt, part_row + (int64_t)t * G * kHeadDim);
+                                                  part_row + (int64_t)t * G * kHeadDim);
       } else {
         float2 *pz = reinterpret_cast<float2 *>(part_row + (int64_t)t * G * kHeadDim);
         for (int o2 = tid; o2 < G * kHeadDim / 2; o2 += kThreads) st_coherent(pz + o2, make_float2(0.f, 0.f));

@@ -231,7 +231,6 @@ __global__ __launch_bounds__(kThreads) void k_sample(
   __shared__ __attribute__((aligned(16))) float P[G * kSplitMax];  // split CDF; reused as the slot-reduction buffer
   __shared__ int cnt[G * kSplitMax];
   __shared__ int list[kSplitMax];
-  __shared__ int wave_cnt[4];
 
   if (tid < G) {
     const int64_t r = row0 + tid;
@@ -255,7 +254,7 @@ __global__ __launch_bounds__(kThreads) void k_sample(
   __syncthreads();
   claim_search<G, STRAT>(start, nrows, row0, S, invS, STRAT ? u + row0 * S : u + row0,
                          STRAT ? S : 1, hc, P, kSplitMax, cnt, idx_out);
-  gather_union<E, G, PAGED, false>(kv, b, kvh, start, nrows, P, kSplitMax, cnt, list, wave_cnt,
+  gather_union<E, G, PAGED, false>(kv, b, kvh, start, nrows, P, kSplitMax, cnt, list,
                                    part + sid * G * kHeadDim);
   if (tid == 0) flags[sid] = 1;
 }

@@ -583,19 +583,18 @@ __device__ __forceinline__ int compact_union(const int *cnt, int pitch, int nrow
   return nlist;
 }
 
-// Value stage of one split after claim_search: the union over the group's
-// heads of the chosen keys is compacted in key order and each chosen V row is
-// read once: O_h += c_{h,j} V_j (Sec. 2, Eq. "stochastic-add-only-attn").  The
-// G x 128 partial sums are written to part_out (global; coherent stores if
-// COHERENT).  P is reused as the reduction buffer.  FW: cnt holds float
-// weights (bit patterns) instead of integer counts.
+// Value stage of one split over a compacted union list (the group's chosen
+// keys in key order, list[0..nlist)): each chosen V row is read once and
+// added to every head with its count, O_h += c_{h,j} V_j (Sec. 2, Eq.
+// "stochastic-add-only-attn").  The workgroup's 16 row slots share the list,
+// U rows in flight each.  The G x 128 partial sums are written to part_out
+// (global; coherent stores if COHERENT).  P is reused as the reduction
+// buffer.  FW: cnt holds float weights (bit patterns) instead of integer counts.
 template <typename E, int G, bool PAGED, bool COHERENT, bool FW = false, int U = 4>
-__device__ __forceinline__ void gather_union(const KvView &kv, int b, int kvh, int start, int nrows,
-                                             float *P, int pitch, const int *cnt, int *list,
-                                             int *wave_cnt, float *__restrict__ part_out) {
+__device__ __forceinline__ void gather_list(const KvView &kv, int b, int kvh, int start,
+                                            const int *list, int nlist, float *P, int pitch,
+                                            const int *cnt, float *__restrict__ part_out) {
   const int tid = threadIdx.x, slot = tid >> 4, c = tid & 15;
-  (void)wave_cnt;
-  const int nlist = compact_union<G>(cnt, pitch, nrows, list);
   // gather-add: slot takes list entries slot, slot+16, ...; U rows in flight
   const E *V = static_cast<const E *>(kv.v);
   float acc[G][8];
@@ -641,6 +640,16 @@ __device__ __forceinline__ void gather_union(const KvView &kv, int b, int kvh, i
     else
       reinterpret_cast<float2 *>(part_out)[o2] = v;
   }
+}
+
+// Value stage of one split after the claims: the union over the group's heads
+// of the chosen keys is compacted in key order, then gathered by gather_list.
+template <typename E, int G, bool PAGED, bool COHERENT, bool FW = false, int U = 4>
+__device__ __forceinline__ void gather_union(const KvView &kv, int b, int kvh, int start, int nrows,
+                                             float *P, int pitch, const int *cnt, int *list,
+                                             float *__restrict__ part_out) {
+  const int nlist = compact_union<G>(cnt, pitch, nrows, list);
+  gather_list<E, G, PAGED, COHERENT, FW, U>(kv, b, kvh, start, list, nlist, P, pitch, cnt, part_out);
 }
 
 }  // namespace santa

@@ -24,6 +24,15 @@ def test_cfg2_full_every_row():
     log(f"  dense {check_dense(w, d)}")
 
 
+@pytest.mark.parametrize("kind,S", [("systematic", 128), ("systematic", 2048)])
+def test_cfg2_shape_paper_budgets_every_row(kind, S):
+    """The batch-1 32k shape at the paper's two operating budgets."""
+    w = make_workload(2, seed=0, kind=kind, S=S)
+    log(f"[full cfg2 shape] {kind} S={S}")
+    out, idx, _ = run(w)
+    log(f"  sampled {check_sampled(w, out, idx)}")
+
+
 @pytest.mark.timeout(300)
 @pytest.mark.parametrize("S", [128, 256, 512])
 def test_cfg3_full_every_row(S):

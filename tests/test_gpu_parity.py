@@ -51,6 +51,11 @@ SAMPLED_CASES = {
     "strat_g1_bf16": (2, "stratified", dict(B=2, Hq=4, Hkv=4, n=1100, S=32)),
     "sys_empty_row": (2, "systematic", dict(B=3, n=600, S=32, ctx_len=[600, 0, 5])),
     "cfg4_paged_sys": (4, "systematic", dict(B=4, len_lo=700, len_hi=3000)),
+    # large budgets in the one-launch kernel: closed-form claim ranges with
+    # hundreds of claims per split and long union lists (the shared gather)
+    "sys_s2048_long_union": (2, "systematic", dict(B=1, n=20000, S=2048)),
+    "strat_s1024_staged_limit": (2, "stratified", dict(B=1, n=12000, S=1024)),
+    "strat_s1100_unstaged": (2, "stratified", dict(B=1, n=6000, S=1100)),
 }
 
 
