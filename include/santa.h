@@ -32,8 +32,15 @@
  *   ctx_len 0 yields a zero output and idx -1.
  * - Workspace: `ws` must be at least santa_workspace_size(...) bytes, 256-byte
  *   aligned, and initialised once by santa_workspace_init() (or zero-filled)
- *   before its first use.  Every call leaves it ready for the next call.  Calls
- *   that share one workspace must be ordered (same stream or synchronised).
+ *   before its first use.  Every call leaves it ready for the next call, of
+ *   any kind and shape, provided the workspace is large enough for that call.
+ *   Calls that share one workspace must be ordered (same stream or
+ *   synchronised).
+ * - Bounded waits: the single-launch paths wait on other workgroups of the
+ *   same launch with a spin limit.  A wait that gives up sets the int32 at
+ *   byte 0 of the workspace to nonzero; that call's outputs are then not
+ *   valid and the workspace needs santa_workspace_init() again.  The library
+ *   never reads the flag back (it does not synchronise); callers may.
  * - The library is stateless apart from the thread-local error message.
  */
 #ifndef SANTA_H

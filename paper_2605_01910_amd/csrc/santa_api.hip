@@ -51,13 +51,17 @@ int choose_split(int64_t rows, int64_t n_k) {
 // tests of both paths; a workspace must be sized under the same settings):
 //   SANTA_VARIANT=multi  use the multi-kernel path instead of the fused launch
 //   SANTA_SPLITS=T       splits per row of the fused path
+//   SANTA_QUEUE=1        large batches: stream and value stage in one launch with
+//                        per-XCD work queues (k_stream_value) instead of two
 struct Tuning {
   int fused, splits;
-  int sampled_path;  // 0: by size, 1: one persistent launch, 2: two launches
+  int sampled_path;  // 0: by size, 1: one persistent launch, 2: stream + value stage
+  int queue;         // stream + value stage in one launch (per-XCD work queues)
 };
 
 Tuning tuning() {
-  Tuning r{1, 0, 0};
+  Tuning r{1, 0, 0, 0};
+  if (const char *v = std::getenv("SANTA_QUEUE")) r.queue = std::atoi(v) != 0;
   if (const char *v = std::getenv("SANTA_VARIANT")) r.fused = std::string(v) != "multi";
   if (const char *v = std::getenv("SANTA_SPLITS")) r.splits = std::atoi(v);
   if (const char *v = std::getenv("SANTA_SAMPLED")) {
@@ -140,14 +144,16 @@ santa::Plan make_plan(const santa_shape_t *sh, const santa_kv_t *kv, int S, int 
   };
   const Tuning tune = tuning();
   const int Tf = fused_splits((int64_t)p.B * p.Hkv, p.n_k);
-  if (kind != SANTA_KIND_BERNOULLI && tune.fused && Tf <= santa::kMaxSplits) {
+  if (kind != SANTA_KIND_BERNOULLI && tune.fused && Tf <= santa::kMaxSplits &&
+      (int64_t)p.B * p.Hkv <= santa::kSyncRowsMax) {
     // fused layout: counters first (they must start at zero: santa_workspace_init);
-    // every fused path keeps them at the same offsets, so calls of different
-    // kinds and shapes can share one workspace
+    // every fused path keeps them at the same offsets and size, whatever the
+    // shape, so calls of different kinds and shapes can share one workspace in
+    // any order (no data section of one layout overlaps another's counters)
     p.fused = 1;
     p.T = Tf;
-    p.off_err = take(4);
-    p.off_sync = take((size_t)p.B * p.Hkv * santa::kSyncStride * 4);
+    p.off_err = take(santa::kErrBytes);
+    p.off_sync = take((size_t)santa::kSyncRowsMax * santa::kSyncStride * 4);
     // rows use ceil(L_b / T) keys per split rounded up to 64; Ls is the longest
     p.Ls = (int)(((p.n_k + p.T - 1) / p.T + 63) & ~63);
     const bool sampled = kind != SANTA_KIND_DENSE;
@@ -156,6 +162,7 @@ santa::Plan make_plan(const santa_shape_t *sh, const santa_kv_t *kv, int S, int 
     p.split2 = sampled && (tune.sampled_path == 2 ||
                            (tune.sampled_path == 0 && (int64_t)p.B * p.Hkv * p.T > 1024));
     if (p.split2) {
+      p.queue = tune.queue;
       p.npitch = ((int64_t)p.n_k + 63) & ~int64_t(63);
       p.off_stats = take(rows * p.T * 8);
       p.off_stash = take(rows * (size_t)p.npitch * 2);   // 16-bit in-block CDF

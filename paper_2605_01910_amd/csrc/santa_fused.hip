@@ -65,6 +65,7 @@ struct FusedArgs {
   float *coarse;  // [B*Hq][npitch/32]  two-launch path: the CDF at every 32-key block end
   unsigned long long *sync;  // [B*Hkv][kSyncStride/2] arrival counter, counter base
   int *err;       // [1]                set if a wait gave up
+  unsigned *tickets;  // [8]            one-launch large-batch path: next ticket of each XCD queue
   int B, Hq, Hkv, T, S;
   int ustage;     // the group's uniforms (G*S stratified, G systematic) staged in LDS if 1
   int64_t npitch; // stash floats per head row (n_k rounded up to 64)
@@ -1045,17 +1046,24 @@ __device__ __forceinline__ void write_split_stash(const FusedArgs &a, const floa
   }
 }
 
-// One work item per workgroup, items row-major; the hardware dispatcher
-// balances them.  Writes the stash, the block ends and the statistics.
+// Waves per SIMD of the key-stream kernels: many resident waves keep the
+// stream's loads in flight (64 VGPRs for bf16 rows with G <= 4).
 template <typename E, int G, bool PAGED>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(sizeof(E) == 2 && G <= 4 && !PAGED ? 8 : (G <= 4 ? 4 : 2)))) void k_stream_cdf(FusedArgs a) {
+constexpr int stream_waves() {
+  return sizeof(E) == 2 && G <= 4 && !PAGED ? 8 : (G <= 4 ? 4 : 2);
+}
+
+// Split t of KV row rowkv (= b * Hkv + kvh): scores, CDF, then the stash, the
+// block ends and the statistics.  Splits past the row's last (t >= Tb) write
+// nothing.
+template <typename E, int G, bool PAGED>
+__device__ __forceinline__ void stream_cdf_item(const FusedArgs &a, int rowkv, int t) {
   extern __shared__ __attribute__((aligned(16))) float dyn[];
   constexpr int pitch = kSplitMax;
   const int T = a.T;
   float *P = dyn;
   __shared__ float mh[G], mtmp[4 * G];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int rowkv = blockIdx.x / T, t = blockIdx.x % T;
   const int b = rowkv / a.Hkv, kvh = rowkv % a.Hkv;
   const int64_t row0 = (int64_t)b * a.Hq + kvh * G;
   const int L = seq_len(a.kv, b);
@@ -1073,6 +1081,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(sizeof
   for (int h = wave; h < G; h += kThreads / 64) wave_split_cdf_m(P + h * pitch, nrows, lane, mh[h]);
   __syncthreads();
   write_split_stash<G>(a, P, mh, nrows, row0, t, start);
+}
+
+// One work item per workgroup, items row-major; the hardware dispatcher
+// balances them.  Writes the stash, the block ends and the statistics.
+template <typename E, int G, bool PAGED>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(stream_waves<E, G, PAGED>()))) void k_stream_cdf(FusedArgs a) {
+  stream_cdf_item<E, G, PAGED>(a, blockIdx.x / a.T, blockIdx.x % a.T);
 }
 
 // Query weights of one GQA group for the Bernoulli score stage (Sec. 5, Eq.
@@ -1310,13 +1325,14 @@ __device__ __forceinline__ int invert_threshold(const uint16_t *Qst, const float
 // chosen keys of a chunk are non-decreasing, so equal keys form runs, and each
 // run's V row is read once and added with its length: O = (1/S) sum_r
 // V_{idx_r} (Sec. 2, the stochastic add-only attention).
-template <typename E, bool PAGED, int MODE>
-__global__ __launch_bounds__(kThreads) void k_value_heads(FusedArgs a, int G) {
+// COHERENT: the statistics were published by other workgroups of the same
+// launch and are read with coherent loads.
+template <typename E, bool PAGED, int MODE, bool COHERENT>
+__device__ __forceinline__ void value_head_item(const FusedArgs &a, int G, int64_t rowq) {
   constexpr bool STRAT = MODE == kStrat;
   extern __shared__ __attribute__((aligned(16))) float dyn[];
   __shared__ int wave_cnt[4];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, slot = tid >> 4, c = tid & 15;
-  const int64_t rowq = blockIdx.x;
   const int b = (int)(rowq / a.Hq), kvh = (int)(rowq % a.Hq) / G;
   E *out = static_cast<E *>(a.out) + rowq * kHeadDim;
   const int L = seq_len(a.kv, b);
@@ -1342,7 +1358,7 @@ __global__ __launch_bounds__(kThreads) void k_value_heads(FusedArgs a, int G) {
     const int nc2 = ((L + kBlock - 1) / kBlock + 1) >> 1;
     for (int i = tid; i < nc2; i += kThreads) reinterpret_cast<float2 *>(cl)[i] = src[i];
   }
-  if (wave == 0) head_offsets_wave<false>(a.stats + rowq * a.T, Tb, lane, off, al);
+  if (wave == 0) head_offsets_wave<COHERENT>(a.stats + rowq * a.T, Tb, lane, off, al);
   if constexpr (MODE == kIid) {
     if (wave == 1) wave_iid_thresholds(a.u + rowq * (a.S + 1), a.S, Tq, lane);
   }
@@ -1419,6 +1435,70 @@ __global__ __launch_bounds__(kThreads) void k_value_heads(FusedArgs a, int G) {
   }
 }
 
+template <typename E, bool PAGED, int MODE>
+__global__ __launch_bounds__(kThreads) void k_value_heads(FusedArgs a, int G) {
+  value_head_item<E, PAGED, MODE, false>(a, G, blockIdx.x);
+}
+
+// Both stages of the two-launch path in one launch, as one work queue per XCD.
+// Workgroup w serves queue x = w % 8, which holds the KV rows rho = x, x + 8,
+// ...: first every split of those rows (the key stream, as k_stream_cdf), then
+// one item per query head of those rows (the value stage, as k_value_heads).
+// A workgroup takes the next ticket of its queue when it starts, so the value
+// item of a head begins as soon as its row's splits have arrived, while other
+// rows are still streaming, instead of after the whole grid.  A value item
+// waits only for stream items of its own queue, every one of which was taken
+// earlier by a running workgroup and waits for nothing, so the waits end.
+// When the dispatcher places workgroup w on XCD w % 8, a row's writers and
+// readers share one L2.  Counters: tickets[x] (the last taker of a queue
+// clears it) and, per KV row, sync[4] (split arrivals) and sync[5] (value
+// items done; the last one clears both), so every counter is zero between
+// calls.  A wait that gives up sets the error flag; the workspace must then be
+// cleared again (santa_workspace_init).  Opt-in (SANTA_QUEUE=1): at batch 16
+// and 32k keys it measured 249 us against 205 us for the two launches, since
+// a split may arrive only once its stash stores have completed, and under the
+// full read stream that wait holds its workgroup slot; the two-launch kernel
+// ends without it.
+template <typename E, int G, bool PAGED, int MODE>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(stream_waves<E, G, PAGED>()))) void k_stream_value(FusedArgs a) {
+  __shared__ int ticket;
+  const int x = blockIdx.x & 7, nq = gridDim.x >> 3;
+  const int rows = a.B * a.Hkv;
+  const int nrx = (rows - x + 7) >> 3;  // rows of this queue
+  if (threadIdx.x == 0) {
+    const unsigned v = __hip_atomic_fetch_add(a.tickets + x, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if ((int)v == nq - 1) __hip_atomic_store(a.tickets + x, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    ticket = (int)v;
+  }
+  __syncthreads();
+  const int w = ticket;
+  const int ns = nrx * a.T;
+  if (w < ns) {
+    const int rowkv = x + 8 * (w / a.T);
+    stream_cdf_item<E, G, PAGED>(a, rowkv, w % a.T);
+    wait_stores();
+    __syncthreads();
+    if (threadIdx.x == 0)
+      __hip_atomic_fetch_add(a.sync + (int64_t)rowkv * (kSyncStride / 2) + 4, 1ull, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+    return;
+  }
+  const int v = w - ns;
+  if (v >= nrx * G) return;
+  const int rowkv = x + 8 * (v / G), h = v % G;
+  unsigned long long *cnt = a.sync + (int64_t)rowkv * (kSyncStride / 2) + 4;
+  row_wait(cnt, (unsigned long long)a.T, a.err);
+  const int b = rowkv / a.Hkv, kvh = rowkv % a.Hkv;
+  value_head_item<E, PAGED, MODE, true>(a, G, (int64_t)b * a.Hq + kvh * G + h);
+  if (threadIdx.x == 0) {
+    const unsigned long long d = __hip_atomic_fetch_add(cnt + 1, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (d == (unsigned long long)(G - 1)) {
+      __hip_atomic_store(cnt, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(cnt + 1, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
@@ -1480,6 +1560,7 @@ FusedArgs make_args(const Plan &p, const KvView &kv, const void *q, void *out, f
   a.coarse = p.off_coarse ? reinterpret_cast<float *>(ws + p.off_coarse) : nullptr;
   a.sync = p.off_sync ? reinterpret_cast<unsigned long long *>(ws + p.off_sync) : nullptr;
   a.err = reinterpret_cast<int *>(ws + p.off_err);
+  a.tickets = reinterpret_cast<unsigned *>(ws + p.off_err + kTicketOffset);
   a.B = p.B;
   a.Hq = p.Hq;
   a.Hkv = p.Hkv;
@@ -1575,6 +1656,22 @@ hipError_t launch_fused_sampled(const Plan &p, const KvView &kv, const void *q, 
     using E = std::remove_pointer_t<decltype(eptr)>;
     constexpr int G = decltype(gc)::value;
     constexpr bool PG = decltype(paged)::value;
+    if (p.split2 && p.queue) {
+      // both stages in one launch: per XCD queue, the splits of its rows, then
+      // one item per query head of those rows
+      const int rows = p.B * p.Hkv;
+      const size_t lds1 = (size_t)G * kSplitMax * 4;
+      const size_t lds2 = (size_t)(value_heads_floats(p.T, (int)(p.npitch / kBlock)) +
+                                   (mode == kIid ? p.S : 0)) * 4;
+      const int nq = ((rows + 7) / 8) * (p.T + G);
+      const void *fn = mode == kStrat ? reinterpret_cast<const void *>(&k_stream_value<E, G, PG, kStrat>)
+                       : mode == kIid ? reinterpret_cast<const void *>(&k_stream_value<E, G, PG, kIid>)
+                                      : reinterpret_cast<const void *>(&k_stream_value<E, G, PG, kSys>);
+      void *params[] = {&args};
+      const CallTimer tm = call_timer();
+      return hipExtLaunchKernel(fn, dim3(8 * nq), dim3(kThreads), params, std::max(lds1, lds2), st,
+                                tm.start, tm.stop, 0);
+    }
     if (p.split2) {
       const CallTimer tm = call_timer();
       void *params[] = {&args};

@@ -13,6 +13,9 @@ constexpr int kThreads = 256;   // threads per workgroup (4 waves of 64)
 constexpr int kSplitMax = 1024; // largest KV split (keys) handled by one workgroup
 constexpr int kMaxSplits = 256; // largest number of splits per row in the fused kernels
 constexpr int kSyncStride = 64; // ints per row of fused-path counters (256 B apart)
+constexpr int kSyncRowsMax = 4096; // KV rows (batch * kv heads) of the fused paths' counter area
+constexpr int kTicketOffset = 64; // bytes from the error flag to the 8 per-XCD ticket counters
+constexpr int kErrBytes = 128;    // error flag and ticket counters
 
 // Per-call launch plan.  The KV sequence of every (batch, kv head) row is cut
 // into T splits of Ls keys; each split is one workgroup.  All sizes below are
@@ -27,8 +30,10 @@ struct Plan {
   int S;        // samples per row (0 for dense)
   int kind;     // santa_kind_t
   int fused;    // 1: single persistent launch (per-row split lengths), 0: multi-kernel
-  int split2;   // fused sampled: 1 = two launches (stream + CDF stash, then one
-                // workgroup per query head), 0 = one persistent launch
+  int split2;   // fused sampled: 1 = stream + CDF stash, then one workgroup per
+                // query head; 0 = one persistent launch
+  int queue;    // split2: 1 = both stages in one launch (per-XCD work queues),
+                // 0 = two launches
   int64_t npitch;  // two-launch sampled: stash entries per query head (n_k rounded up to 64)
   // workspace carve-up (byte offsets, 256-aligned)
   size_t off_stats;  // float2 [B*Hq*T]     per-split (max, sum) in log2 units
@@ -43,8 +48,11 @@ struct Plan {
   size_t off_bw;     // float  [B*Hq*128]   Bernoulli query weights
   size_t off_blist;  // int    [B*Hkv*128]  Bernoulli feature list
   size_t off_bn;     // int    [B*Hkv]      Bernoulli feature count
-  size_t off_err;    // int    [1]          fused: a wait gave up
-  size_t off_sync;   // u64    [B*Hkv*kSyncStride/2] fused: per-row arrival counter and base
+  size_t off_err;    // int    [1]          fused: a wait gave up; at +kTicketOffset
+                     // uint [8] per-XCD ticket counters of the one-launch split2 path
+  size_t off_sync;   // u64    [kSyncRowsMax*kSyncStride/2] fused: per-row counters; the area
+                     // has the same offset and size in every fused layout, so calls of any
+                     // shape find their counters where earlier calls left them
   size_t total;
 };
 

@@ -8,7 +8,7 @@ import numpy as np
 import pytest
 import torch
 
-from tests.gpu_util import (DeviceWorkload, check_dense, check_sampled, log, run)
+from tests.gpu_util import (KIND_CODE, DeviceWorkload, check_dense, check_sampled, log, run)
 from workload import make_workload
 
 pytestmark = pytest.mark.gpu
@@ -177,13 +177,16 @@ def test_fused_barrier_flag_stays_clear():
     assert int(ws[:4].view(torch.int32).item()) == 0
 
 
+@pytest.mark.parametrize("queue", [1, 0])
 @pytest.mark.parametrize("case", sorted(SAMPLED_CASES))
-def test_two_launch_sampled_parity(case, monkeypatch):
-    """The large-batch sampled path (stream + CDF stash launch, then one
-    workgroup per query head) on every sampled case."""
+def test_two_launch_sampled_parity(case, queue, monkeypatch):
+    """The large-batch sampled path (key stream with CDF stash, then one
+    workgroup per query head) on every sampled case, in both forms: two
+    launches (queue=0, the default) and one launch with per-XCD work queues."""
     monkeypatch.setenv("SANTA_SAMPLED", "split")
+    monkeypatch.setenv("SANTA_QUEUE", str(queue))
     cfg, kind, over = SAMPLED_CASES[case]
-    log(f"[two-launch/{kind}] {case} cfg={cfg} {over}")
+    log(f"[two-launch/{kind} queue={queue}] {case} cfg={cfg} {over}")
     w = make_workload(cfg, seed=23, kind=kind, **over)
     out, idx, _ = run(w, kind)
     log(f"  {check_sampled(w, out, idx, kind)}")
@@ -243,3 +246,39 @@ def test_workspace_shared_by_both_sampled_paths(monkeypatch):
         monkeypatch.setenv("SANTA_SAMPLED", path)
         out, idx, _ = run(w, dw=dw, ws=ws)
         check_sampled(w, out, idx)
+
+
+def test_stream_value_queue_matches_two_launches(monkeypatch):
+    """The one-launch work-queue form of the large-batch path gives bitwise the
+    two-launch result on the same inputs, leaves its per-XCD tickets and its
+    per-row counters at zero after every call (calls of other shapes follow on
+    the same workspace) and never sets the wait flag."""
+    from paper_2605_01910_amd import santa as S
+    monkeypatch.setenv("SANTA_SAMPLED", "split")
+    cases = [(3, "systematic", dict(B=16, n=3000, S=256)),           # 128 KV rows
+             (2, "stratified", dict(B=3, n=1100, S=64, ctx_len=[1100, 5, 700])),  # 24 rows
+             (2, "systematic", dict(B=9, Hq=16, Hkv=2, n=2048, S=128)),           # 18 rows, G = 8
+             (2, "iid", dict(B=5, n=1500, S=96, ctx_len=[1500, 1, 0, 999, 64]))]
+    works = [make_workload(c, seed=61 + i, kind=k, **o) for i, (c, k, o) in enumerate(cases)]
+    dws = [DeviceWorkload(w) for w in works]
+    ws = max((S.alloc_workspace(d.shape, d.kv, w.S, KIND_CODE[w.kind]) for w, d in zip(works, dws)),
+             key=lambda x: x.numel())
+    off_sync = 256  # the error flag and the ticket counters take the first 256 bytes
+    # shapes grow and shrink in turn: 128, 24, 18, 40 KV rows (the counter
+    # area has one size in every layout, so no call sees another's data there)
+    for rep in range(2):
+        for w, d in zip(works, dws):
+            rows = w.B * w.Hkv
+            log(f"[queue rep={rep}] {w.kind} B={w.B} Hq={w.Hq} Hkv={w.Hkv} n={w.n_max} S={w.S}")
+            monkeypatch.setenv("SANTA_QUEUE", "1")
+            out1, idx1, _ = run(w, dw=d, ws=ws)
+            torch.cuda.synchronize()
+            assert int(ws[:4].view(torch.int32).item()) == 0
+            assert int(ws[64:96].view(torch.int32).abs().sum().item()) == 0
+            cnt = ws[off_sync:off_sync + rows * 256].view(torch.int64).view(rows, 32)[:, 4:6]
+            assert int(cnt.abs().sum().item()) == 0
+            check_sampled(w, out1, idx1)
+            monkeypatch.setenv("SANTA_QUEUE", "0")
+            out0, idx0, _ = run(w, dw=d, ws=ws)
+            assert np.array_equal(idx0, idx1)
+            assert np.array_equal(out0, out1)
