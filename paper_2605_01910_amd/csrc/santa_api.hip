@@ -142,18 +142,19 @@ santa::Plan make_plan(const santa_shape_t *sh, const santa_kv_t *kv, int S, int 
     off = align256(off + bytes);
     return o;
   };
+  // Every layout, fused or not, starts with the error flag (with the
+  // work-queue tickets) and the fused paths' counter area, at the same offsets
+  // and of the same size, so that calls of any kind and shape can share one
+  // workspace in any order: no layout puts data where another keeps counters.
+  // The counters must start at zero (santa_workspace_init).
+  p.off_err = take(santa::kErrBytes);
+  p.off_sync = take((size_t)santa::kSyncRowsMax * santa::kSyncStride * 4);
   const Tuning tune = tuning();
   const int Tf = fused_splits((int64_t)p.B * p.Hkv, p.n_k);
   if (kind != SANTA_KIND_BERNOULLI && tune.fused && Tf <= santa::kMaxSplits &&
       (int64_t)p.B * p.Hkv <= santa::kSyncRowsMax) {
-    // fused layout: counters first (they must start at zero: santa_workspace_init);
-    // every fused path keeps them at the same offsets and size, whatever the
-    // shape, so calls of different kinds and shapes can share one workspace in
-    // any order (no data section of one layout overlaps another's counters)
     p.fused = 1;
     p.T = Tf;
-    p.off_err = take(santa::kErrBytes);
-    p.off_sync = take((size_t)santa::kSyncRowsMax * santa::kSyncStride * 4);
     // rows use ceil(L_b / T) keys per split rounded up to 64; Ls is the longest
     p.Ls = (int)(((p.n_k + p.T - 1) / p.T + 63) & ~63);
     const bool sampled = kind != SANTA_KIND_DENSE;
@@ -185,7 +186,6 @@ santa::Plan make_plan(const santa_shape_t *sh, const santa_kv_t *kv, int S, int 
                    std::max(Tf, (int)((p.n_k + 511) / 512)));
     p.Ls = (int)(((p.n_k + p.T - 1) / p.T + 63) & ~63);
     p.npitch = ((int64_t)p.n_k + 63) & ~int64_t(63);
-    p.off_err = take(4);
     p.off_stats = take(rows * p.T * 8);
     p.off_stash = take(rows * (size_t)p.npitch * 2);
     p.off_coarse = take(rows * (size_t)(p.npitch / 32) * 4);

@@ -51,8 +51,8 @@ struct Plan {
   size_t off_err;    // int    [1]          fused: a wait gave up; at +kTicketOffset
                      // uint [8] per-XCD ticket counters of the one-launch split2 path
   size_t off_sync;   // u64    [kSyncRowsMax*kSyncStride/2] fused: per-row counters; the area
-                     // has the same offset and size in every fused layout, so calls of any
-                     // shape find their counters where earlier calls left them
+                     // has the same offset and size in every layout, so calls of any kind
+                     // and shape find their counters where earlier calls left them
   size_t total;
 };
 

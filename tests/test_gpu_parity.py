@@ -282,3 +282,37 @@ def test_stream_value_queue_matches_two_launches(monkeypatch):
             out0, idx0, _ = run(w, dw=d, ws=ws)
             assert np.array_equal(idx0, idx1)
             assert np.array_equal(out0, out1)
+
+
+def test_workspace_shared_by_every_kind(monkeypatch):
+    """Every layout keeps the error flag and the counter area at the front, so
+    one workspace serves Bernoulli, multi-kernel, one-launch, two-launch and
+    dense calls interleaved in any order."""
+    from paper_2605_01910_amd import santa as S
+    ws_ = make_workload(2, B=2, n=3000, kind="systematic", S=128, seed=71)
+    wb = make_workload(5, B=2, n=1500, mode=1, B_draws=1, seed=72)
+    ds, db = DeviceWorkload(ws_), DeviceWorkload(wb)
+    spaces = [S.alloc_workspace(db.shape, db.kv, wb.S, S.SANTA_KIND_BERNOULLI),
+              S.alloc_workspace(ds.shape, ds.kv, 1, S.SANTA_KIND_DENSE)]
+    for var, path in (("fused", "fused"), ("fused", "split"), ("multi", "fused")):
+        monkeypatch.setenv("SANTA_VARIANT", var)
+        monkeypatch.setenv("SANTA_SAMPLED", path)
+        spaces.append(S.alloc_workspace(ds.shape, ds.kv, ws_.S, S.SANTA_KIND_SYSTEMATIC))
+    ws = max(spaces, key=lambda x: x.numel())
+    order = ["fused", "bernoulli", "fused", "multi", "fused", "split", "bernoulli", "split",
+             "dense", "multi", "fused"]
+    log(f"[workspace] {' '.join(order)}")
+    for step in order:
+        monkeypatch.setenv("SANTA_VARIANT", "multi" if step == "multi" else "fused")
+        monkeypatch.setenv("SANTA_SAMPLED", "split" if step == "split" else "fused")
+        if step == "bernoulli":
+            out, idx, _ = run(wb, "bernoulli", dw=db, ws=ws)
+            check_sampled(wb, out, idx, "bernoulli")
+        elif step == "dense":
+            d, _, _ = run(ws_, "dense", dw=ds, ws=ws)
+            check_dense(ws_, d)
+        else:
+            out, idx, _ = run(ws_, dw=ds, ws=ws)
+            check_sampled(ws_, out, idx)
+        torch.cuda.synchronize()
+        assert int(ws[:4].view(torch.int32).item()) == 0, step
