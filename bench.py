@@ -59,6 +59,9 @@ def parse():
     ap.add_argument("--layout", default="nhd", choices=["nhd", "hnd"])
     ap.add_argument("--flush-gib", type=float, default=1.0)
     ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--append", action="store_true",
+                    help="pass the current token's rows as k_new / v_new: every call (sampled "
+                         "and dense) writes them into the cache inside its launch")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--profile", action="store_true",
@@ -102,6 +105,14 @@ def main():
     from tests.gpu_util import DeviceWorkload, KIND_CODE
     dw = DeviceWorkload(w, layout=args.layout)
     kind = w.kind
+    if args.append:
+        if kind == "bernoulli":
+            sys.exit("--append is not available with Bernoulli scores")
+        from tests.gpu_util import current_rows
+        rows = current_rows(dw, w)
+        k_new = torch.stack([k.clone() for k, _ in rows]).contiguous()
+        v_new = torch.stack([v.clone() for _, v in rows]).contiguous()
+        dw.kv.k_new, dw.kv.v_new = k_new.data_ptr(), v_new.data_ptr()
     out = torch.empty_like(dw.q)
     ws = S.alloc_workspace(dw.shape, dw.kv, max(w.S, 1), KIND_CODE[kind])
     ws_dense = S.alloc_workspace(dw.shape, dw.kv, 1, S.SANTA_KIND_DENSE)
@@ -237,6 +248,8 @@ def main():
                       f"ctx {int(w.ctx_len.min())}..{int(w.ctx_len.max())})")
     else:
         cache_desc = f"{args.layout} cache"
+    if args.append:
+        cache_desc += ", fused current-token append"
     kgbs = alg_bytes / (kus.mean() * 1e-6) / 1e9
     line = {
         "metric": METRIC,

@@ -108,6 +108,21 @@ typedef struct {
   int32_t page_size;
   int32_t max_pages;
   int32_t n_k;
+  /* Fused current-token append (nullable, both or neither; 16-byte aligned,
+   * [batch, num_kv_heads, head_dim] in the cache's dtype).  A decode step
+   * first stores the new token's key and value in the cache, then attends
+   * over it; FlashAttention-2's decode call fuses that store, the paper's
+   * kernels take a cache that already holds the token (App. Decode-Step
+   * Kernel Microbenchmark Details, note on KV-cache appends).  When set, the
+   * call writes k_new / v_new into row ctx_len[b] - 1 (n_k - 1 without
+   * ctx_len) of every (b, kv head), through the block table for paged
+   * caches, inside the attention launch, and attends over the cache with
+   * those rows: the cache memory must be writable and ctx_len[b] >= 1.
+   * Supported by the dense, flash and sampled calls on their fused paths;
+   * the Bernoulli call and the multi-kernel path return
+   * SANTA_ERR_UNSUPPORTED. */
+  const void *k_new;
+  const void *v_new;
 } santa_kv_t;
 
 /* Feature-major key cache for the Bernoulli score stage: element (b, k, i, j)

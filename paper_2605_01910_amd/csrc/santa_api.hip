@@ -113,6 +113,9 @@ santa_status_t check_kv(const santa_kv_t *kv, const santa_shape_t *sh, bool need
   if ((need_k && (reinterpret_cast<uintptr_t>(kv->k) & 15)) ||
       (reinterpret_cast<uintptr_t>(kv->v) & 15))
     return fail(SANTA_ERR_UNSUPPORTED, "k and v must be 16-byte aligned");
+  if (!kv->k_new != !kv->v_new) return fail(SANTA_ERR_INVALID_ARG, "k_new and v_new go together");
+  if ((reinterpret_cast<uintptr_t>(kv->k_new) & 15) || (reinterpret_cast<uintptr_t>(kv->v_new) & 15))
+    return fail(SANTA_ERR_UNSUPPORTED, "k_new and v_new must be 16-byte aligned");
   if (kv->block_table) {
     if (!is_pow2(kv->page_size)) return fail(SANTA_ERR_UNSUPPORTED, "page_size must be a power of two");
     if (kv->max_pages < 1) return fail(SANTA_ERR_INVALID_ARG, "max_pages must be >= 1");
@@ -231,6 +234,8 @@ santa::KvView make_view(const santa_kv_t *kv) {
   v.ps_log2 = kv->block_table ? ilog2(kv->page_size) : 0;
   v.max_pages = kv->max_pages;
   v.n_k = kv->n_k;
+  v.k_new = kv->k_new;
+  v.v_new = kv->v_new;
   return v;
 }
 
@@ -264,6 +269,8 @@ santa_status_t sampled(const void *q, const santa_kv_t *kv, const santa_shape_t 
   if (!u) return fail(SANTA_ERR_INVALID_ARG, "u is NULL");
   const santa::Plan p = make_plan(sh, kv, S, strat ? SANTA_KIND_STRATIFIED : SANTA_KIND_SYSTEMATIC);
   s = check_ws(p, ws, ws_bytes);
+  if (s == SANTA_OK && kv->k_new && !p.fused)
+    s = fail(SANTA_ERR_UNSUPPORTED, "the fused append (k_new, v_new) needs the fused path");
   if (s != SANTA_OK) return s;
   if (p.fused)
     return hip_status(santa::launch_fused_sampled(p, make_view(kv), q, log2_scale(scale),
@@ -305,6 +312,8 @@ santa_status_t santa_decode_dense(const void *q, const santa_kv_t *kv, const san
   if (s != SANTA_OK) return s;
   const santa::Plan p = make_plan(shape, kv, 0, SANTA_KIND_DENSE);
   s = check_ws(p, ws, ws_bytes);
+  if (s == SANTA_OK && kv->k_new && !p.fused)
+    s = fail(SANTA_ERR_UNSUPPORTED, "the fused append (k_new, v_new) needs the fused path");
   if (s != SANTA_OK) return s;
   if (p.fused)
     return hip_status(santa::launch_fused_dense(p, make_view(kv), q, log2_scale(scale), out,
@@ -351,6 +360,8 @@ santa_status_t santa_decode_bernoulli_qk(const void *q, const santa_kt_t *kt,
   if (S < 1 || S > (1 << 24)) return fail(SANTA_ERR_INVALID_ARG, "S must be in [1, 2^24]");
   const santa::Plan p = make_plan(shape, kv, S, SANTA_KIND_BERNOULLI);
   s = check_ws(p, ws, ws_bytes);
+  if (s == SANTA_OK && kv->k_new)
+    s = fail(SANTA_ERR_UNSUPPORTED, "the fused append (k_new, v_new) is not available with Bernoulli scores");
   if (s != SANTA_OK) return s;
   santa::KtView ktv{kt->k_t, kt->stride_b, kt->stride_h, kt->stride_d};
   if (p.fused)
@@ -375,6 +386,8 @@ santa_status_t santa_decode_iid(const void *q, const santa_kv_t *kv, const santa
   if (!u) return fail(SANTA_ERR_INVALID_ARG, "u is NULL");
   const santa::Plan p = make_plan(shape, kv, S, SANTA_KIND_IID);
   s = check_ws(p, ws, ws_bytes);
+  if (s == SANTA_OK && kv->k_new && !p.fused)
+    s = fail(SANTA_ERR_UNSUPPORTED, "the fused append (k_new, v_new) needs the fused path");
   if (s != SANTA_OK) return s;
   if (!p.fused) return fail(SANTA_ERR_UNSUPPORTED, "the i.i.d. step needs the fused launch layout");
   return hip_status(santa::launch_fused_sampled(p, make_view(kv), q, log2_scale(scale), 2, u,
@@ -395,6 +408,8 @@ santa_status_t santa_decode_flash(const void *q, const santa_kv_t *kv, const san
   if (!u) return fail(SANTA_ERR_INVALID_ARG, "u is NULL");
   const santa::Plan p = make_plan(shape, kv, 0, SANTA_KIND_DENSE);
   s = check_ws(p, ws, ws_bytes);
+  if (s == SANTA_OK && kv->k_new && !p.fused)
+    s = fail(SANTA_ERR_UNSUPPORTED, "the fused append (k_new, v_new) needs the fused path");
   if (s != SANTA_OK) return s;
   if (!p.fused) return fail(SANTA_ERR_UNSUPPORTED, "the flash step needs the fused launch layout");
   return hip_status(santa::launch_fused_flash(p, make_view(kv), q, log2_scale(scale), ilog2(tile),

@@ -667,7 +667,9 @@ __device__ __forceinline__ void gather_heads_waves(const KvView &kv, int b, int 
   }
 }
 
-template <typename E, int G, bool PAGED, int MODE>
+// APPEND: the fused current-token append (append_current) is compiled in;
+// calls without one run the kernel without that code.
+template <typename E, int G, bool PAGED, int MODE, bool APPEND = false>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void k_fused_sampled(FusedArgs a) {
   constexpr bool STRAT = MODE == kStrat;
   extern __shared__ __attribute__((aligned(16))) float dyn[];
@@ -708,6 +710,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
       continue;
     }
     const int start = t * Ls, nrows = min(Ls, L - start);
+    if constexpr (APPEND) append_current<E, PAGED>(a.kv, b, kvh, a.Hkv, start, nrows, L);
     unsigned long long *sync = a.sync + (int64_t)rowkv * (kSyncStride / 2);
     const unsigned long long base =
         __hip_atomic_load(sync + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -845,7 +848,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 // instead of the exact weighted sum; the split publishes o_w = sum_tau
 // exp2(m_tau - m_w) l_tau O_tau with l_w = sum_tau exp2(m_tau - m_w) l_tau, so
 // the same merge gives O = sum_tau W_tau O_tau / sum_tau W_tau (Kernel 2).
-template <typename E, int G, bool PAGED, bool PERSIST, bool FLASH = false>
+template <typename E, int G, bool PAGED, bool PERSIST, bool FLASH = false, bool APPEND = false>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(PERSIST ? 2 : 3))) void k_fused_dense(FusedArgs a) {
   // dynamic LDS: s [G][pitch] scores / weights, red [4][G*128] (also the merge scratch);
   // flash: s, cnt [G][pitch] (later red), list [pitch], tile statistics [G][2][kSplitMax/16]
@@ -893,6 +896,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(PERSIS
       continue;
     }
     const int start = t * Ls, nrows = min(Ls, L - start);
+    if constexpr (APPEND) append_current<E, PAGED>(a.kv, b, kvh, a.Hkv, start, nrows, L);
     unsigned long long *sync = a.sync + (int64_t)rowkv * (kSyncStride / 2);
     const unsigned long long base =
         __hip_atomic_load(sync + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1056,7 +1060,7 @@ constexpr int stream_waves() {
 // Split t of KV row rowkv (= b * Hkv + kvh): scores, CDF, then the stash, the
 // block ends and the statistics.  Splits past the row's last (t >= Tb) write
 // nothing.
-template <typename E, int G, bool PAGED>
+template <typename E, int G, bool PAGED, bool APPEND = true>
 __device__ __forceinline__ void stream_cdf_item(const FusedArgs &a, int rowkv, int t) {
   extern __shared__ __attribute__((aligned(16))) float dyn[];
   constexpr int pitch = kSplitMax;
@@ -1071,6 +1075,7 @@ __device__ __forceinline__ void stream_cdf_item(const FusedArgs &a, int rowkv, i
   split_geometry(L, T, Ls, Tb);
   if (t >= Tb) return;
   const int start = t * Ls, nrows = min(Ls, L - start);
+  if constexpr (APPEND) append_current<E, PAGED>(a.kv, b, kvh, a.Hkv, start, nrows, L);
 
   const QRegs<E, G> qr = load_q<E, G>(static_cast<const E *>(a.q), b, a.Hq, kvh, tid & 15);
   float mx[G];
@@ -1085,9 +1090,9 @@ __device__ __forceinline__ void stream_cdf_item(const FusedArgs &a, int rowkv, i
 
 // One work item per workgroup, items row-major; the hardware dispatcher
 // balances them.  Writes the stash, the block ends and the statistics.
-template <typename E, int G, bool PAGED>
+template <typename E, int G, bool PAGED, bool APPEND = false>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(stream_waves<E, G, PAGED>()))) void k_stream_cdf(FusedArgs a) {
-  stream_cdf_item<E, G, PAGED>(a, blockIdx.x / a.T, blockIdx.x % a.T);
+  stream_cdf_item<E, G, PAGED, APPEND>(a, blockIdx.x / a.T, blockIdx.x % a.T);
 }
 
 // Query weights of one GQA group for the Bernoulli score stage (Sec. 5, Eq.
@@ -1614,13 +1619,16 @@ hipError_t launch_fused_flash(const Plan &p, const KvView &kv, const void *q, fl
     constexpr int G = decltype(gc)::value;
     constexpr bool PG = decltype(paged)::value;
     const size_t lds = (size_t)fused_flash_floats(G, kSplitMax, p.T) * 4;
-    const void *res = reinterpret_cast<const void *>(&k_fused_dense<E, G, PG, true, true>);
+    const bool ap = kv.k_new != nullptr;
+    const void *res = ap ? reinterpret_cast<const void *>(&k_fused_dense<E, G, PG, true, true, true>)
+                         : reinterpret_cast<const void *>(&k_fused_dense<E, G, PG, true, true>);
     const int rows = p.B * p.Hkv;
     if (rows * p.T <= capacity_of(res, lds))  // one resident round
       return launch_resident(res, p, args, lds, st);
     void *params[] = {&args};
     const CallTimer tm = call_timer();
-    return hipExtLaunchKernel(reinterpret_cast<const void *>(&k_fused_dense<E, G, PG, false, true>),
+    return hipExtLaunchKernel(ap ? reinterpret_cast<const void *>(&k_fused_dense<E, G, PG, false, true, true>)
+                                 : reinterpret_cast<const void *>(&k_fused_dense<E, G, PG, false, true>),
                               dim3(rows * p.T), dim3(kThreads), params, lds, st, tm.start, tm.stop,
                               0);
   });
@@ -1634,13 +1642,16 @@ hipError_t launch_fused_dense(const Plan &p, const KvView &kv, const void *q, fl
     constexpr int G = decltype(gc)::value;
     constexpr bool PG = decltype(paged)::value;
     const size_t lds = (size_t)fused_dense_floats(G, kSplitMax, p.T) * 4;
-    const void *res = reinterpret_cast<const void *>(&k_fused_dense<E, G, PG, true>);
+    const bool ap = kv.k_new != nullptr;
+    const void *res = ap ? reinterpret_cast<const void *>(&k_fused_dense<E, G, PG, true, false, true>)
+                         : reinterpret_cast<const void *>(&k_fused_dense<E, G, PG, true>);
     const int rows = p.B * p.Hkv;
     if (rows * p.T <= capacity_of(res, lds))  // one resident round
       return launch_resident(res, p, args, lds, st);
     void *params[] = {&args};
     const CallTimer tm = call_timer();
-    return hipExtLaunchKernel(reinterpret_cast<const void *>(&k_fused_dense<E, G, PG, false>),
+    return hipExtLaunchKernel(ap ? reinterpret_cast<const void *>(&k_fused_dense<E, G, PG, false, false, true>)
+                                 : reinterpret_cast<const void *>(&k_fused_dense<E, G, PG, false>),
                               dim3(rows * p.T), dim3(kThreads), params, lds, st, tm.start, tm.stop,
                               0);
   });
@@ -1676,7 +1687,8 @@ hipError_t launch_fused_sampled(const Plan &p, const KvView &kv, const void *q, 
       const CallTimer tm = call_timer();
       void *params[] = {&args};
       const size_t lds1 = (size_t)G * kSplitMax * 4;
-      hipError_t e = hipExtLaunchKernel(reinterpret_cast<const void *>(&k_stream_cdf<E, G, PG>),
+      hipError_t e = hipExtLaunchKernel(kv.k_new ? reinterpret_cast<const void *>(&k_stream_cdf<E, G, PG, true>)
+                                                 : reinterpret_cast<const void *>(&k_stream_cdf<E, G, PG>),
                                         dim3(p.B * p.Hkv * p.T), dim3(kThreads), params, lds1, st,
                                         tm.start, nullptr, 0);
       if (e != hipSuccess) return e;
@@ -1690,9 +1702,14 @@ hipError_t launch_fused_sampled(const Plan &p, const KvView &kv, const void *q, 
       return hipExtLaunchKernel(fn2, dim3(p.B * p.Hq), dim3(kThreads), params2, lds2, st, nullptr,
                                 tm.stop, 0);
     }
-    const void *fn = mode == kStrat ? reinterpret_cast<const void *>(&k_fused_sampled<E, G, PG, kStrat>)
-                     : mode == kIid ? reinterpret_cast<const void *>(&k_fused_sampled<E, G, PG, kIid>)
-                                    : reinterpret_cast<const void *>(&k_fused_sampled<E, G, PG, kSys>);
+    const bool ap = kv.k_new != nullptr;
+    const void *fn =
+        mode == kStrat ? (ap ? reinterpret_cast<const void *>(&k_fused_sampled<E, G, PG, kStrat, true>)
+                             : reinterpret_cast<const void *>(&k_fused_sampled<E, G, PG, kStrat>))
+        : mode == kIid ? (ap ? reinterpret_cast<const void *>(&k_fused_sampled<E, G, PG, kIid, true>)
+                             : reinterpret_cast<const void *>(&k_fused_sampled<E, G, PG, kIid>))
+                       : (ap ? reinterpret_cast<const void *>(&k_fused_sampled<E, G, PG, kSys, true>)
+                             : reinterpret_cast<const void *>(&k_fused_sampled<E, G, PG, kSys>));
     // stage the group's uniforms in LDS when they are few (the host keeps the
     // i.i.d. ones within the limit; their sorted thresholds follow them)
     const size_t nu = (size_t)G * (mode == kIid ? p.S + 1 : (mode == kStrat ? p.S : 1));

@@ -65,6 +65,7 @@ struct KvView {
   int32_t ps_log2;      // log2(page_size)
   int32_t max_pages;
   int32_t n_k;
+  const void *k_new, *v_new;  // nullable: the current token's rows [B, Hkv, 128], appended in-launch
 };
 
 struct KtView {

@@ -468,6 +468,32 @@ __device__ __forceinline__ int ld_coherent(const int *p) {
 // compiler barrier for memory accesses.
 __device__ __forceinline__ void wait_stores() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// Fused current-token append (App. Decode-Step Kernel Microbenchmark Details,
+// note on KV-cache appends: the decode step stores the new token's key and
+// value before attending).  When kv.k_new is set, the workgroup whose split
+// [start, start + nrows) holds position L - 1 copies the rows (b, kvh) of
+// k_new / v_new ([B, Hkv, 128]) into the cache there and waits for the stores
+// before it reads its split.  No other workgroup of the launch reads that row
+// (every split reads and gathers only its own keys).  Called by every thread;
+// the condition is uniform over the workgroup.
+template <typename E, bool PAGED>
+__device__ __forceinline__ void append_current(const KvView &kv, int b, int kvh, int Hkv, int start,
+                                               int nrows, int L) {
+  if (!kv.k_new || L - 1 < start || L - 1 >= start + nrows) return;
+  constexpr int n16 = kHeadDim * (int)sizeof(E) / 16;  // 16-byte chunks per row
+  const int tid = threadIdx.x;
+  if (tid < 2 * n16) {
+    const bool isv = tid >= n16;
+    const int c = isv ? tid - n16 : tid;
+    const uint4 *src = reinterpret_cast<const uint4 *>(static_cast<const E *>(isv ? kv.v_new : kv.k_new) +
+                                                       ((int64_t)b * Hkv + kvh) * kHeadDim);
+    E *dst = const_cast<E *>(static_cast<const E *>(isv ? kv.v : kv.k)) + row_offset<PAGED>(kv, b, kvh, L - 1);
+    reinterpret_cast<uint4 *>(dst)[c] = src[c];
+  }
+  wait_stores();
+  __syncthreads();
+}
+
 // Per-split claim state of one head: the split owns thresholds tau with
 // lo <= tau < hi (global CDF units); a is exp2(m_t - m*), Z the row total.
 struct HeadClaim {

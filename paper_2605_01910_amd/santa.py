@@ -50,7 +50,8 @@ class santa_kv_t(ctypes.Structure):
                 ("stride_h", ctypes.c_int64),
                 ("ctx_len", ctypes.c_void_p), ("block_table", ctypes.c_void_p),
                 ("page_size", ctypes.c_int32), ("max_pages", ctypes.c_int32),
-                ("n_k", ctypes.c_int32)]
+                ("n_k", ctypes.c_int32),
+                ("k_new", ctypes.c_void_p), ("v_new", ctypes.c_void_p)]
 
 
 class santa_kt_t(ctypes.Structure):

@@ -45,6 +45,7 @@ class DeviceWorkload:
 
     def __init__(self, w, layout: str = "nhd", pass_ctx: bool = True):
         self.w = w
+        self.layout = layout
         self.q = dev_elems(w.q)
         self.ctx = torch.from_numpy(w.ctx_len.astype(np.int32)).cuda()
         self.u = None if w.u is None else torch.from_numpy(w.u).cuda()
@@ -203,3 +204,20 @@ def check_flash(w, out: np.ndarray, idx: np.ndarray, rows: Optional[Sequence[int
         worst = max(worst, e)
         assert e <= SAMPLED_MAX_ABS, f"row {r}: flash max abs error {e:.3e}"
     return {"band_accepted": band, "max_abs": worst, "rows": len(rows)}
+
+
+def current_rows(dw: DeviceWorkload, w):
+    """Views of the cache rows at position ctx_len[b] - 1 (the current token),
+    per batch: (K [Hkv, d], V [Hkv, d])."""
+    out = []
+    for b in range(w.B):
+        L = int(w.ctx_len[b])
+        if w.paged:
+            page = int(w.block_table[b, (L - 1) // w.page_size])
+            s = (L - 1) % w.page_size
+            out.append((dw.kp[page, :, s, :], dw.vp[page, :, s, :]))
+        elif dw.layout == "hnd":
+            out.append((dw.k[b, :, L - 1], dw.v[b, :, L - 1]))
+        else:
+            out.append((dw.k[b, L - 1], dw.v[b, L - 1]))
+    return out
