@@ -21,6 +21,7 @@ CASES = {
     "iid_one_launch": (2, "iid", dict(B=2, n=2000, S=96, ctx_len=[2000, 640]), "fused"),
     "sys_paged": (4, "systematic", dict(B=3, len_lo=700, len_hi=3000), "fused"),
     "sys_paged_two_launch": (4, "systematic", dict(B=3, len_lo=700, len_hi=3000), "split"),
+    "strat_work_queue": (2, "stratified", dict(B=4, n=2200, S=64, ctx_len=[2200, 3, 1500, 64]), "queue"),
     "dense": (2, "dense", dict(B=2, n=3000, ctx_len=[3000, 1234]), "fused"),
     "dense_paged": (4, "dense", dict(B=3, len_lo=900, len_hi=2600), "fused"),
     "flash": (2, "flash", dict(B=2, n=3000, ctx_len=[3000, 1500]), "fused"),
@@ -31,7 +32,8 @@ CASES = {
 @pytest.mark.parametrize("case", sorted(CASES))
 def test_fused_append(case, monkeypatch):
     cfg, kind, over, path = CASES[case]
-    monkeypatch.setenv("SANTA_SAMPLED", path)
+    monkeypatch.setenv("SANTA_SAMPLED", "split" if path == "queue" else path)
+    monkeypatch.setenv("SANTA_QUEUE", "1" if path == "queue" else "0")
     gen_kind = "systematic" if kind == "dense" else kind
     w = make_workload(cfg, seed=81, kind=gen_kind, **over)
     log(f"[append/{kind}/{path}] {case} cfg={cfg} {over}")
