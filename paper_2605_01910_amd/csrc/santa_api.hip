@@ -73,11 +73,12 @@ Tuning tuning() {
 
 // Splits per row of the fused path: enough that the whole batch of rows fills
 // about `target` workgroups, at least ceil(n_k / kSplitMax).  Sampled steps
-// with small budgets (S <= 256) take 256 (one per CU): at batch 1 and 32k keys
-// the stratified S = 256 step runs in 27.5 us against 28.3 us with 512, the
-// i.i.d. one in 29.4 against 29.8 us.  Larger budgets put more claims in each
-// split and take 512 (systematic S = 2048: 32.7 us against 34.2 us), and so
-// do the dense and flash steps (level either way).
+// with budgets up to S = 1024 take 256 (one per CU): at batch 1 and 32k keys
+// the stratified S = 256 step runs in 27.5 us against 28.3 us with 512,
+// systematic S = 512 in 27.7 against 29.1 us, S = 1024 in 29.4 against
+// 29.7 us, the i.i.d. S = 256 step in 29.4 against 29.8 us.  Larger budgets
+// put more claims in each split and take 512 (systematic S = 2048: 32.7 us
+// against 34.2 us), and so do the dense and flash steps (level either way).
 int fused_splits(int64_t rows_kv, int64_t n_k, int64_t target) {
   const int tmin = (int)((n_k + santa::kSplitMax - 1) / santa::kSplitMax);
   int fill = 128;
@@ -159,7 +160,7 @@ santa::Plan make_plan(const santa_shape_t *sh, const santa_kv_t *kv, int S, int 
   p.off_sync = take((size_t)santa::kSyncRowsMax * santa::kSyncStride * 4);
   const Tuning tune = tuning();
   const bool small_budget = (kind == SANTA_KIND_SYSTEMATIC || kind == SANTA_KIND_STRATIFIED ||
-                             kind == SANTA_KIND_IID) && S <= 256;
+                             kind == SANTA_KIND_IID) && S <= 1024;
   const int Tf = fused_splits((int64_t)p.B * p.Hkv, p.n_k, small_budget ? 256 : 512);
   if (kind != SANTA_KIND_BERNOULLI && tune.fused && Tf <= santa::kMaxSplits &&
       (int64_t)p.B * p.Hkv <= santa::kSyncRowsMax) {
