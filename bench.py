@@ -57,6 +57,16 @@ def parse():
     ap.add_argument("--S-tile", type=int, default=None,
                     help="flash: draws per tile (default: the budget rule S_tile ~ S / T)")
     ap.add_argument("--layout", default="nhd", choices=["nhd", "hnd"])
+    ap.add_argument("--path", default="auto", choices=["auto", "one", "two", "multi"],
+                    help="launch path (santa_set_options): by size, one persistent launch, "
+                         "key stream + per-head value stage, or the multi-kernel variant")
+    ap.add_argument("--splits", type=int, default=0, help="KV splits per row (0: by size)")
+    ap.add_argument("--mode", type=int, default=None,
+                    help="Bernoulli: 0 per-head ternary query, 1 mean group query")
+    ap.add_argument("--B-draws", type=int, default=None, help="Bernoulli: draws per feature")
+    ap.add_argument("--kv", default="bf16", choices=["bf16", "fp8"],
+                    help="cache element type: the query's (bf16) or OCP FP8 E4M3 codes with "
+                         "per-(batch, KV head) scales (queries and outputs stay bf16)")
     ap.add_argument("--flush-gib", type=float, default=1.0)
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--append", action="store_true",
@@ -91,24 +101,33 @@ def main():
         over["S"] = args.S
     if args.kind is not None:
         over["kind"] = args.kind
+    if args.mode is not None:
+        over["mode"] = args.mode
+    if args.B_draws is not None:
+        over["B_draws"] = args.B_draws
+    if args.kv == "fp8":
+        over["kv_dtype"] = "fp8"
     if args.kind == "flash":
         from workload.gen import CONFIGS
         n = CONFIGS[args.cfg]["n"]
         over["tile"] = args.tile
-        over["S_tile"] = args.S_tile or S.flash_tile_budget(over.get("S", CONFIGS[args.cfg]["S"]),
-                                                            (n + args.tile - 1) // args.tile)
+        over["S_tile"] = args.S_tile or flash_tile_budget(over.get("S", CONFIGS[args.cfg]["S"]),
+                                                          (n + args.tile - 1) // args.tile)
+    S.santa_set_options(S.PATHS[args.path], args.splits)
     t0 = time.time()
     w = make_workload(args.cfg, seed=0, **over)
     print(f"[bench] workload cfg={args.cfg} B={w.B} Hq={w.Hq} Hkv={w.Hkv} n={w.n_max} "
           f"kind={w.kind} S={w.S} built in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
 
-    from tests.gpu_util import DeviceWorkload, KIND_CODE
+    from workload.device import DeviceWorkload, current_rows
+    KIND_CODE = {"dense": S.SANTA_KIND_DENSE, "systematic": S.SANTA_KIND_SYSTEMATIC,
+                 "stratified": S.SANTA_KIND_STRATIFIED, "bernoulli": S.SANTA_KIND_BERNOULLI,
+                 "flash": S.SANTA_KIND_FLASH, "iid": S.SANTA_KIND_IID}
     dw = DeviceWorkload(w, layout=args.layout)
     kind = w.kind
     if args.append:
         if kind == "bernoulli":
             sys.exit("--append is not available with Bernoulli scores")
-        from tests.gpu_util import current_rows
         rows = current_rows(dw, w)
         k_new = torch.stack([k.clone() for k, _ in rows]).contiguous()
         v_new = torch.stack([v.clone() for _, v in rows]).contiguous()
@@ -116,6 +135,8 @@ def main():
     out = torch.empty_like(dw.q)
     ws = S.alloc_workspace(dw.shape, dw.kv, max(w.S, 1), KIND_CODE[kind])
     ws_dense = S.alloc_workspace(dw.shape, dw.kv, 1, S.SANTA_KIND_DENSE)
+    plan = S.santa_plan_info(dw.shape, dw.kv, max(w.S, 1), KIND_CODE[kind])
+    plan["path_name"] = {v: k for k, v in S.PATHS.items()}[plan["path"]]
     stream = torch.cuda.current_stream()
     mask = None
     if kind == "bernoulli":
@@ -143,7 +164,8 @@ def main():
         S.santa_decode_dense(dw.q, dw.kv, dw.shape, w.scale, out, ws_dense, stream)
 
     # ---- algorithmic bytes (untimed call with idx_out) ----
-    esz = 2 if w.dtype == "bf16" else 4
+    qsz = 2 if w.dtype == "bf16" else 4            # q and out elements
+    esz = 1 if w.kv_dtype == "fp8" else qsz        # cache elements
     L = w.ctx_len.astype(np.int64)
     k_bytes = int(L.sum()) * w.Hkv * w.d * esz
     uniq_rows = 0
@@ -161,11 +183,13 @@ def main():
             feat_frac = float(m.mean())
             k_bytes = int(sum(int(m[b].sum()) * int(L[b]) for b in range(w.B))) * esz
     v_bytes = (uniq_rows if kind != "dense" else int(L.sum()) * w.Hkv) * w.d * esz
-    io_bytes = 2 * w.B * w.Hq * w.d * esz + (w.u.nbytes if w.u is not None else 0)
+    io_bytes = 2 * w.B * w.Hq * w.d * qsz + (w.u.nbytes if w.u is not None else 0)
+    if w.kv_dtype == "fp8":
+        io_bytes += w.k_scale.nbytes + w.v_scale.nbytes
     if kind == "bernoulli":
         io_bytes += w.u_q.nbytes
     alg_bytes = k_bytes + v_bytes + io_bytes
-    dense_bytes = 2 * int(L.sum()) * w.Hkv * w.d * esz + 2 * w.B * w.Hq * w.d * esz
+    dense_bytes = 2 * int(L.sum()) * w.Hkv * w.d * esz + 2 * w.B * w.Hq * w.d * qsz
 
     # ---- timing ----
     flush = torch.empty(int(args.flush_gib * (1 << 30)) // 4, dtype=torch.float32, device=dev)
@@ -215,11 +239,13 @@ def main():
     wall0 = time.time()
     us, kus = timed(step, args.steps, args.warmup)
     wall = time.time() - wall0
+    S.check_workspace(ws)  # every timed call's bounded waits completed
     print(f"[bench] {kind}: call mean {us.mean():.2f} us  median {np.median(us):.2f}  "
           f"min {us.min():.2f} | kernel mean {kus.mean():.2f} us", file=sys.stderr, flush=True)
     res = {}
     if not args.no_dense and kind != "dense":
         dus, dkus = timed(dense_step, args.steps, args.warmup)
+        S.check_workspace(ws_dense)
         res["dense_us_per_step"] = round(float(dus.mean()), 3)
         res["dense_kernel_us"] = round(float(dkus.mean()), 3)
         res["dense_gbs"] = round(dense_bytes / (dus.mean() * 1e-6) / 1e9, 1)
@@ -250,6 +276,8 @@ def main():
         cache_desc = f"{args.layout} cache"
     if args.append:
         cache_desc += ", fused current-token append"
+    if w.kv_dtype == "fp8":
+        cache_desc += ", FP8 E4M3 K/V with per-(batch, KV head) scales"
     kgbs = alg_bytes / (kus.mean() * 1e-6) / 1e9
     line = {
         "metric": METRIC,
@@ -270,7 +298,7 @@ def main():
                          f"B={w.B}, Hq={w.Hq}, Hkv={w.Hkv}, d={w.d}, "
                          f"n_k={w.n_max}, {w.dtype}, {cache_desc}, cold cache "
                          f"({args.flush_gib:g} GiB update + {2 * args.flush_gib:g} GiB read per step)"),
-            "variant": os.environ.get("SANTA_VARIANT", "fused"),
+            "path": plan["path_name"], "kernels": plan["kernels"],
             "batch": w.B, "n_k": w.n_max, "S": w.S, "kind": w.kind,
         },
         "us_per_step": round(float(us.mean()), 3),
@@ -285,7 +313,7 @@ def main():
         **res,
         "roofline": {
             "bound": "hbm",
-            "kernel": kernel_label(w, kind),
+            "kernel": plan["kernels"],
             "timing": ("HIP events the library attaches to its kernel dispatch "
                        "(santa_time_next_call), mean over the timed cold-cache steps"),
             "kernel_us": round(float(kus.mean()), 3),
@@ -309,7 +337,7 @@ def main():
 
     # counter-based traffic exists for the default workload only
     if (args.cfg == 2 and args.B is None and args.S is None and args.kind is None
-            and args.layout == "nhd" and line["roofline"]["kernel"].startswith("k_fused_")):
+            and args.layout == "nhd" and args.path == "auto" and args.splits == 0):
         line["roofline"]["traffic"] = measured_traffic(line["roofline"]["kernel"],
                                                        "traffic_llama8b_32k_b1.json")
     if not args.no_cpu and not args.profile:
@@ -317,25 +345,10 @@ def main():
     print(json.dumps(line), flush=True)
 
 
-def kernel_label(w, kind: str) -> str:
-    """Name of the kernel(s) one call launches, following the library's path
-    choice: the sampled step takes two launches when its rows exceed one
-    resident round of ~1024 workgroups (splits per row: at least n_k / 1024,
-    and 128 halved while splits x rows > 512)."""
-    if os.environ.get("SANTA_VARIANT", "fused") == "multi" or kind == "bernoulli":
-        return "all kernels of one santa_decode_* call"
-    if kind == "dense":
-        return "k_fused_dense"
-    if kind == "flash":
-        return "k_fused_dense (flash mode)"
-    rows = w.B * w.Hkv
-    fill = 128
-    while fill > 1 and fill * rows > 512:
-        fill //= 2
-    T = max((w.n_max + 1023) // 1024, fill)
-    forced = os.environ.get("SANTA_SAMPLED", "")
-    two = forced == "split" or (forced != "fused" and rows * T > 1024)
-    return "k_stream_cdf + k_value_heads" if two else "k_fused_sampled"
+def flash_tile_budget(S_total: int, n_tiles: int) -> int:
+    """Draws per tile for a total budget S spread over T tiles (S_tile ~ S/T,
+    Sec. 3.3), rounded half up, at least one."""
+    return max(1, (2 * int(S_total) + int(n_tiles)) // (2 * int(n_tiles)))
 
 
 def kernel_source_hash() -> str:

@@ -41,7 +41,9 @@
  *   byte 0 of the workspace to nonzero; that call's outputs are then not
  *   valid and the workspace needs santa_workspace_init() again.  The library
  *   never reads the flag back (it does not synchronise); callers may.
- * - The library is stateless apart from the thread-local error message.
+ * - Per-thread state: the last error message, a pending call timer
+ *   (santa_time_next_call) and the launch options (santa_set_options).
+ *   Nothing else persists between calls outside the caller's workspace.
  */
 #ifndef SANTA_H
 #define SANTA_H
@@ -123,7 +125,26 @@ typedef struct {
    * SANTA_ERR_UNSUPPORTED. */
   const void *k_new;
   const void *v_new;
+  /* Element type of K and V (a santa_kv_dtype_t).  SANTA_KV_AS_Q (0, the
+   * default): shape->dtype.  SANTA_KV_FP8_E4M3 (1): one byte per element, an
+   * OCP FP8 E4M3 code (1 sign bit, 4 exponent bits with bias 7, 3 mantissa
+   * bits; exponent field 0 encodes the subnormals m/8 * 2^-6; S.1111.111 is
+   * NaN; no infinities), scaled per (batch, KV head): element (b, j, k, i) of
+   * K is k_scale[b*num_kv_heads + k] * e4m3(code), and likewise for V with
+   * v_scale (device float32 arrays [batch, num_kv_heads]).  Quantising the
+   * cache is complementary to SANTA (Sec. 1; Related Work on KV-cache
+   * compression): keys and values are read at one byte each.  Needs
+   * shape->dtype == SANTA_BF16 (q and out stay bfloat16); strides are in
+   * elements (= bytes) and must keep rows 16-byte aligned.  Supported by the
+   * dense, flash, systematic, stratified and i.i.d. calls on their fused
+   * paths; the Bernoulli call, the multi-kernel path and the fused append
+   * return SANTA_ERR_UNSUPPORTED. */
+  int32_t kv_dtype;
+  const float *k_scale;
+  const float *v_scale;
 } santa_kv_t;
+
+typedef enum { SANTA_KV_AS_Q = 0, SANTA_KV_FP8_E4M3 = 1 } santa_kv_dtype_t;
 
 /* Feature-major key cache for the Bernoulli score stage: element (b, k, i, j)
  * (feature i of key j) at k_t + b*stride_b + k*stride_h + i*stride_d + j; keys
@@ -176,8 +197,9 @@ santa_status_t santa_decode_stratified(const void *q, const santa_kv_t *kv,
  * C_m = sum_{i<=m} E_i (the normalised partial sums of S + 1 unit
  * exponentials are the order statistics of S uniforms); out = (1/S)
  * sum_m V_{J_m}.  Requires G*(2S + 1) <= 4096 (G = num_q_heads /
- * num_kv_heads); workspace as SANTA_KIND_IID.  Not available under
- * SANTA_VARIANT=multi (returns SANTA_ERR_UNSUPPORTED). */
+ * num_kv_heads; S <= 511 at G = 4); workspace as SANTA_KIND_IID.  Needs the
+ * fused launch layout: returns SANTA_ERR_UNSUPPORTED under SANTA_PATH_MULTI
+ * and when batch * num_kv_heads exceeds 4096. */
 santa_status_t santa_decode_iid(const void *q, const santa_kv_t *kv, const santa_shape_t *shape,
                                 float scale, int32_t S, const float *u, int32_t *idx_out,
                                 void *out, void *ws, size_t ws_bytes, void *stream);
@@ -224,8 +246,9 @@ santa_status_t santa_decode_bernoulli_qk(const void *q, const santa_kt_t *kt,
  *          (logical positions) tile by tile, -1 for tiles at or past the row's
  *          length.
  * The workspace is sized by santa_workspace_size(..., SANTA_KIND_FLASH) (the
- * dense step's workspace).  Contiguous and paged caches; not available under
- * SANTA_VARIANT=multi (returns SANTA_ERR_UNSUPPORTED). */
+ * dense step's workspace).  Contiguous and paged caches.  Needs the fused
+ * launch layout: returns SANTA_ERR_UNSUPPORTED under SANTA_PATH_MULTI and
+ * when batch * num_kv_heads exceeds 4096. */
 santa_status_t santa_decode_flash(const void *q, const santa_kv_t *kv, const santa_shape_t *shape,
                                   float scale, int32_t tile, int32_t S_tile, const float *u,
                                   int32_t *idx_out, void *out, void *ws, size_t ws_bytes,
@@ -259,6 +282,58 @@ santa_status_t santa_time_next_call(void *start_event, void *stop_event);
  * bytes can be read at. */
 #define SANTA_STREAM_READ_GROUPS 4096
 santa_status_t santa_stream_read(const void *buf, size_t bytes, uint32_t *sink, void *stream);
+
+/* Launch options (not part of the method): which kernels a call runs.  They
+ * exist for tuning sweeps and for tests that cover every path; the defaults
+ * choose by problem size.
+ *   SANTA_PATH_AUTO        by size: sampled steps whose rows fit one resident
+ *                          round of about 1024 workgroups take one persistent
+ *                          launch, larger ones the two-launch path;
+ *   SANTA_PATH_ONE_LAUNCH  sampled steps: one persistent launch (k_fused_sampled);
+ *   SANTA_PATH_TWO_LAUNCH  sampled steps: key stream with a CDF stash, then one
+ *                          workgroup per query head (k_stream_cdf, k_value_heads);
+ *   SANTA_PATH_MULTI       every step: the multi-kernel variant (score/CDF,
+ *                          offsets, sampling and merge kernels).
+ * splits: KV splits per row of the fused paths (0 = by size; at least
+ * ceil(n_k / 1024)).  The options apply to every later call made on the
+ * calling thread (santa_workspace_size and santa_plan_info included) until
+ * they are set again; opts = NULL restores the defaults {AUTO, 0}.  A
+ * workspace must be sized under the options of the calls that use it.
+ * Returns SANTA_ERR_INVALID_ARG for an unknown path or splits outside
+ * [0, 256]. */
+typedef enum {
+  SANTA_PATH_AUTO = 0,
+  SANTA_PATH_ONE_LAUNCH = 1,
+  SANTA_PATH_TWO_LAUNCH = 2,
+  SANTA_PATH_MULTI = 3
+} santa_path_t;
+
+typedef struct {
+  int32_t path;   /* santa_path_t */
+  int32_t splits; /* 0 = by size */
+} santa_options_t;
+
+santa_status_t santa_set_options(const santa_options_t *opts);
+
+/* The calling thread's current options (written to *opts). */
+santa_status_t santa_get_options(santa_options_t *opts);
+
+/* What a call with these arguments would launch under the calling thread's
+ * options, without launching anything: the path taken (a santa_path_t other
+ * than AUTO), the KV splits per row, the longest split in keys, the
+ * workspace bytes (as santa_workspace_size) and the names of the kernels.
+ * kernels points to a static string.  Same argument rules as
+ * santa_workspace_size (S is ignored for dense and flash). */
+typedef struct {
+  int32_t path;
+  int32_t splits;
+  int32_t split_len;
+  size_t workspace;
+  const char *kernels;
+} santa_plan_info_t;
+
+santa_status_t santa_plan_info(const santa_shape_t *shape, const santa_kv_t *kv, int32_t S,
+                               int32_t kind, santa_plan_info_t *info);
 
 /* Human-readable name of a status code. */
 const char *santa_status_string(santa_status_t status);

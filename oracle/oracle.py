@@ -41,7 +41,9 @@ class _Problem(ctypes.Structure):
                 ("d", ctypes.c_int32), ("n_max", ctypes.c_int32), ("is_f32", ctypes.c_int32),
                 ("q", ctypes.c_void_p), ("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
                 ("sb", ctypes.c_int64), ("sn", ctypes.c_int64), ("sh", ctypes.c_int64),
-                ("ctx_len", ctypes.c_void_p), ("scale", ctypes.c_double)]
+                ("ctx_len", ctypes.c_void_p), ("scale", ctypes.c_double),
+                ("kv_fp8", ctypes.c_int32), ("k_scale", ctypes.c_void_p),
+                ("v_scale", ctypes.c_void_p)]
 
 
 _lib = None
@@ -75,6 +77,7 @@ def lib():
         L.orc_decode_flash.argtypes = [ctypes.POINTER(_Problem), ctypes.c_int, ctypes.c_int, P,
                                        ctypes.c_int, P, P, P, P, P]
         L.orc_decode_flash.restype = ctypes.c_int
+        L.orc_fp8_e4m3_decode.argtypes = [P, ctypes.c_int64, P]
         _lib = L
     return _lib
 
@@ -84,10 +87,21 @@ def _p(a: Optional[np.ndarray]):
 
 
 def _elem(a: np.ndarray):
-    """(contiguous array, is_f32) for bfloat16 bits (uint16) or float32 input."""
+    """(contiguous array, element kind) for bfloat16 bits (uint16, 0), float32
+    (1) or float64 (2) input."""
     if a.dtype == np.uint16:
         return np.ascontiguousarray(a), 0
+    if a.dtype == np.float64:
+        return np.ascontiguousarray(a), 2
     return np.ascontiguousarray(a, dtype=np.float32), 1
+
+
+def fp8_e4m3_decode(codes: np.ndarray) -> np.ndarray:
+    """OCP FP8 E4M3 codes (uint8) -> float64 values, elementwise."""
+    c = np.ascontiguousarray(codes, dtype=np.uint8)
+    out = np.empty(c.shape, dtype=np.float64)
+    lib().orc_fp8_e4m3_decode(_p(c), c.size, _p(out))
+    return out
 
 
 # --------------------------------------------------------------------------
@@ -197,22 +211,46 @@ class Result:
         self.rows, self.threads = rows, threads
 
 
+def _problem(q, k, v, ctx_len, scale, k_scale, v_scale):
+    """The C problem struct (and the arrays it points to, kept alive by the
+    caller).  k and v hold q's element type, or FP8 E4M3 codes (uint8) with
+    k_scale / v_scale float32 [B, Hkv]."""
+    q, f = _elem(q)
+    B, Hq, d = q.shape
+    if k.dtype == np.uint8:
+        assert v.dtype == np.uint8 and k_scale is not None and v_scale is not None
+        k, v = np.ascontiguousarray(k), np.ascontiguousarray(v)
+        ks = np.ascontiguousarray(k_scale, dtype=np.float32).reshape(-1)
+        vs = np.ascontiguousarray(v_scale, dtype=np.float32).reshape(-1)
+        fp8 = 1
+    else:
+        k, fk = _elem(k)
+        v, fv = _elem(v)
+        assert f == fk == fv, "q, k and v must share one element type"
+        ks = vs = None
+        fp8 = 0
+    _, n, Hkv, _ = k.shape
+    assert ks is None or ks.size == B * Hkv
+    ctx = np.ascontiguousarray(ctx_len, dtype=np.int32)
+    P = _Problem(B, Hq, Hkv, d, n, f, q.ctypes.data, k.ctypes.data, v.ctypes.data,
+                 n * Hkv * d, Hkv * d, d, ctx.ctypes.data, float(scale), fp8,
+                 None if ks is None else ks.ctypes.data, None if vs is None else vs.ctypes.data)
+    return P, (q, k, v, ctx, ks, vs)
+
+
 def decode(kind: str, q: np.ndarray, k: np.ndarray, v: np.ndarray, ctx_len: np.ndarray,
            scale: float, S: int = 0, u: Optional[np.ndarray] = None,
            u_q: Optional[np.ndarray] = None, B_draws: int = 1, mode: int = 0,
            iid_draws: bool = False, rows: Optional[Sequence[int]] = None,
-           want_cdf: bool = False, want_weights: bool = False) -> Result:
+           want_cdf: bool = False, want_weights: bool = False,
+           k_scale: Optional[np.ndarray] = None, v_scale: Optional[np.ndarray] = None) -> Result:
     """One decode step over logical caches ``k``/``v`` of shape [B, n, Hkv, d]
-    for the rows ``b*Hq + h`` listed in ``rows`` (all rows if None)."""
-    q, f = _elem(q)
-    k, fk = _elem(k)
-    v, fv = _elem(v)
-    assert f == fk == fv, "q, k and v must share one element type"
+    for the rows ``b*Hq + h`` listed in ``rows`` (all rows if None).  An FP8
+    cache holds uint8 E4M3 codes with scales ``k_scale``/``v_scale`` [B, Hkv]."""
+    P, keep = _problem(q, k, v, ctx_len, scale, k_scale, v_scale)
+    q = keep[0]
     B, Hq, d = q.shape
-    _, n, Hkv, _ = k.shape
-    ctx = np.ascontiguousarray(ctx_len, dtype=np.int32)
-    P = _Problem(B, Hq, Hkv, d, n, f, q.ctypes.data, k.ctypes.data, v.ctypes.data,
-                 n * Hkv * d, Hkv * d, d, ctx.ctypes.data, float(scale))
+    n = keep[1].shape[1]
     rows_a = None if rows is None else np.ascontiguousarray(rows, dtype=np.int32)
     nr = B * Hq if rows_a is None else rows_a.size
     out = np.empty((nr, d), dtype=np.float64)
@@ -240,52 +278,52 @@ def decode_workload(wl, kind: Optional[str] = None, rows: Optional[Sequence[int]
     if kind == "iid":  # the workload's i.i.d. uniforms are S + 1 per row (spacings)
         kind = "iid_spacings"
     S = wl.S if kind != "dense" else 0
+    ks, vs = getattr(wl, "k_scale", None), getattr(wl, "v_scale", None)
     if not wl.paged:
         return decode(kind, wl.q, wl.k, wl.v, wl.ctx_len, wl.scale, S, wl.u, wl.u_q, wl.B_draws,
-                      wl.mode, False, rows, want_cdf, want_weights)
-    # paged: one sequence at a time through its logical arrays
+                      wl.mode, False, rows, want_cdf, want_weights, ks, vs)
+    # paged: one sequence at a time through its logical arrays, all of its
+    # listed rows in one call
     all_rows = list(range(wl.B * wl.Hq)) if rows is None else list(rows)
-    outs, idxs, cdfs, threads = [], [], [], 1
-    for r in all_rows:
-        b, h = divmod(r, wl.Hq)
+    by_b = {}
+    for i, r in enumerate(all_rows):
+        by_b.setdefault(r // wl.Hq, []).append(i)
+    nr = len(all_rows)
+    out = np.empty((nr, wl.d))
+    idx = np.empty((nr, max(S, 1)), np.int32) if kind != "dense" else None
+    cdf = np.full((nr, wl.n_max), np.nan) if want_cdf and kind != "dense" else None
+    threads = 1
+    for b, pos in by_b.items():
         kb, vb = wl.logical_kv(b)
         L = int(wl.ctx_len[b])
         kk = kb.reshape(1, L, wl.Hkv, wl.d)
         vv = vb.reshape(1, L, wl.Hkv, wl.d)
-        ub = None
-        if wl.u is not None:
-            ub = wl.u[b:b + 1]
+        ub = None if wl.u is None else wl.u[b:b + 1]
+        heads = [all_rows[i] % wl.Hq for i in pos]
         res = decode(kind, wl.q[b:b + 1], kk, vv, np.array([L], np.int32), wl.scale, S, ub, None,
-                     wl.B_draws, wl.mode, False, [h], want_cdf, False)
+                     wl.B_draws, wl.mode, False, heads, want_cdf, False,
+                     None if ks is None else ks[b:b + 1], None if vs is None else vs[b:b + 1])
         threads = max(threads, res.threads)
-        outs.append(res.out[0])
-        if res.idx is not None:
-            idxs.append(res.idx[0])
-        if res.cdf is not None:
-            c = np.full(wl.n_max, np.nan)
-            c[:L] = res.cdf[0]
-            cdfs.append(c)
-    return Result(np.array(outs), np.array(idxs) if idxs else None,
-                  np.array(cdfs) if cdfs else None, None, None,
-                  np.asarray(all_rows, np.int32), threads)
+        out[pos] = res.out
+        if idx is not None:
+            idx[pos] = res.idx
+        if cdf is not None:
+            cdf[pos, :L] = res.cdf
+    return Result(out, idx, cdf, None, None, np.asarray(all_rows, np.int32), threads)
 
 
 def decode_flash(q: np.ndarray, k: np.ndarray, v: np.ndarray, ctx_len: np.ndarray, scale: float,
                  tile: int, S_tile: int, u: np.ndarray, rows: Optional[Sequence[int]] = None,
-                 want_cdf: bool = False) -> Result:
+                 want_cdf: bool = False, k_scale: Optional[np.ndarray] = None,
+                 v_scale: Optional[np.ndarray] = None) -> Result:
     """S2ANTA-flash over logical caches [B, n, Hkv, d]; ``u`` is [B, Hq,
     ceil(n/tile)].  Result.idx is [rows, T_max*S_tile] (-1 past a row's tiles),
     Result.w the tile weights [rows, T_max]."""
-    q, f = _elem(q)
-    k, fk = _elem(k)
-    v, fv = _elem(v)
-    assert f == fk == fv, "q, k and v must share one element type"
+    P, keep = _problem(q, k, v, ctx_len, scale, k_scale, v_scale)
+    q = keep[0]
     B, Hq, d = q.shape
-    _, n, Hkv, _ = k.shape
+    n = keep[1].shape[1]
     Tm = (n + tile - 1) // tile
-    ctx = np.ascontiguousarray(ctx_len, dtype=np.int32)
-    P = _Problem(B, Hq, Hkv, d, n, f, q.ctypes.data, k.ctypes.data, v.ctypes.data,
-                 n * Hkv * d, Hkv * d, d, ctx.ctypes.data, float(scale))
     rows_a = None if rows is None else np.ascontiguousarray(rows, dtype=np.int32)
     nr = B * Hq if rows_a is None else rows_a.size
     uu = np.ascontiguousarray(u, dtype=np.float32).reshape(-1)
@@ -303,9 +341,10 @@ def decode_flash(q: np.ndarray, k: np.ndarray, v: np.ndarray, ctx_len: np.ndarra
 def _decode_workload_flash(wl, rows, want_cdf) -> Result:
     """decode_workload for kind="flash": contiguous workloads in one batch
     call, paged ones one sequence at a time through their logical arrays."""
+    ks, vs = getattr(wl, "k_scale", None), getattr(wl, "v_scale", None)
     if not wl.paged:
         return decode_flash(wl.q, wl.k, wl.v, wl.ctx_len, wl.scale, wl.tile, wl.S_tile, wl.u,
-                            rows, want_cdf)
+                            rows, want_cdf, ks, vs)
     all_rows = list(range(wl.B * wl.Hq)) if rows is None else list(rows)
     Tm = (wl.n_max + wl.tile - 1) // wl.tile
     outs, idxs, threads = [], [], 1
@@ -316,7 +355,9 @@ def _decode_workload_flash(wl, rows, want_cdf) -> Result:
         T = (L + wl.tile - 1) // wl.tile
         res = decode_flash(wl.q[b:b + 1], kb.reshape(1, L, wl.Hkv, wl.d),
                            vb.reshape(1, L, wl.Hkv, wl.d), np.array([L], np.int32), wl.scale,
-                           wl.tile, wl.S_tile, np.ascontiguousarray(wl.u[b:b + 1, :, :T]), [h])
+                           wl.tile, wl.S_tile, np.ascontiguousarray(wl.u[b:b + 1, :, :T]), [h],
+                           False, None if ks is None else ks[b:b + 1],
+                           None if vs is None else vs[b:b + 1])
         threads = max(threads, res.threads)
         ix = np.full(Tm * wl.S_tile, -1, np.int32)
         ix[:T * wl.S_tile] = res.idx[0][:T * wl.S_tile]

@@ -23,6 +23,8 @@
  *   orc_gather_mean       (1/S) sum_m v_{J_m}                     (Sec. 2, Eq. "stochastic-add-only-attn")
  *   orc_bernoulli_weights ternary / mean-group query weights      (Sec. 5, Eq. "qk_estimator";
  *                                                                  App. C, Eq. "mean_group_query")
+ *   orc_fp8_e4m3          OCP FP8 E4M3 code -> value (a quantised cache; Sec. 1,
+ *                         Related Work: complementary to SANTA)
  *   orc_flash             S2ANTA-flash: per-tile systematic sampling with a
  *                         fixed budget, tiles merged by their softmax mass
  *                                                                  (Sec. 3.3; App. "S2ANTA-Flash
@@ -44,8 +46,10 @@
  *   - A row with zero context length has no attention distribution: its
  *     output is zero and its indices are -1.
  *
- * Element arrays hold bfloat16 bit patterns (uint16, is_f32 = 0) or float32
- * values (is_f32 = 1); both widen to double exactly.
+ * Element arrays hold bfloat16 bit patterns (uint16, kind 0), float32 values
+ * (kind 1) or float64 values (kind 2); all widen to double exactly.  A cache
+ * of OCP FP8 E4M3 codes with per-(batch, KV head) scales is decoded to
+ * float64 first (orc_fp8_e4m3), one (batch, KV head) slab per row.
  */
 #include <math.h>
 #include <stdint.h>
@@ -55,14 +59,19 @@
 #include <omp.h>
 #endif
 
-/* Exact widening of one stored element to double. */
+/* Exact widening of one stored element to double (kind: 0 bfloat16 bits,
+ * 1 float32, 2 float64). */
 static double elem(const void *base, int is_f32, int64_t i) {
+  if (is_f32 == 2) return ((const double *)base)[i];
   if (is_f32) return (double)((const float *)base)[i];
   uint32_t w = (uint32_t)((const uint16_t *)base)[i] << 16;
   float f;
   memcpy(&f, &w, sizeof f);
   return (double)f;
 }
+
+/* Bytes per element of kind 0, 1, 2. */
+static size_t esize(int kind) { return kind == 2 ? 8 : kind == 1 ? 4 : 2; }
 
 /* Same widening, but to float (used where a decision is taken in float32). */
 static float elemf(const void *base, int is_f32, int64_t i) {
@@ -71,6 +80,29 @@ static float elemf(const void *base, int is_f32, int64_t i) {
   float f;
   memcpy(&f, &w, sizeof f);
   return f;
+}
+
+/* OCP FP8 E4M3 ("E4M3FN") code -> value, from the format's definition: bit 7
+ * the sign, bits 6..3 the exponent field e (bias 7), bits 2..0 the mantissa
+ * field m.  e = 0: subnormal, m/8 * 2^-6; e = 15 and m = 7: NaN (the format
+ * has no infinities); otherwise (1 + m/8) * 2^(e - 7).  Largest finite value
+ * 448, smallest subnormal 2^-9.  Keys and values stored this way are a
+ * quantised KV cache, which the paper treats as complementary to SANTA
+ * (Sec. 1; Related Work). */
+double orc_fp8_e4m3(uint8_t code) {
+  const int sign = code >> 7, e = (code >> 3) & 15, m = code & 7;
+  double v;
+  if (e == 15 && m == 7)
+    v = NAN;
+  else if (e == 0)
+    v = ldexp((double)m / 8.0, -6);
+  else
+    v = ldexp(1.0 + (double)m / 8.0, e - 7);
+  return sign ? -v : v;
+}
+
+void orc_fp8_e4m3_decode(const uint8_t *codes, int64_t n, double *out) {
+  for (int64_t i = 0; i < n; ++i) out[i] = orc_fp8_e4m3(codes[i]);
 }
 
 /* Score stage (Sec. 2, SDPA equation): s_j = scale * sum_i w_i k_{j,i} for j < L, with
@@ -283,7 +315,7 @@ void orc_flash(const double *s, const void *v, int v_f32, int64_t row_stride, in
     /* systematic draws inside the tile and the tile estimate */
     orc_thresholds(0, a + t, S_tile, thr);
     orc_inverse_cdf(C, n, thr, S_tile, ix);
-    orc_gather_mean((const char *)v + (int64_t)j0 * row_stride * (v_f32 ? 4 : 2), v_f32, row_stride,
+    orc_gather_mean((const char *)v + (int64_t)j0 * row_stride * (int64_t)esize(v_f32), v_f32, row_stride,
                     d, ix, S_tile, ot + (int64_t)t * d);
     if (idx)
       for (int i = 0; i < S_tile; ++i) idx[(int64_t)t * S_tile + i] = j0 + ix[i];
@@ -316,14 +348,46 @@ void orc_flash(const double *s, const void *v, int v_f32, int64_t row_stride, in
 
 typedef struct {
   int32_t B, Hq, Hkv, d, n_max;
-  int32_t is_f32;        /* element type of q, k, v */
+  int32_t is_f32;        /* element type of q (and of k, v when kv_fp8 is 0) */
   const void *q;         /* [B, Hq, d] */
   const void *k;         /* logical keys: element (b, j, kv, i) at b*sb + j*sn + kv*sh + i */
   const void *v;         /* logical values, same strides */
   int64_t sb, sn, sh;
   const int32_t *ctx_len; /* [B] */
   double scale;
+  int32_t kv_fp8;        /* 1: k, v hold FP8 E4M3 codes scaled by k_scale / v_scale */
+  const float *k_scale;  /* [B, Hkv] */
+  const float *v_scale;  /* [B, Hkv] */
 } orc_problem_t;
+
+/* The keys and values of row (b, kv) as arrays the step functions read: the
+ * stored arrays themselves (kind is_f32, row stride sn), or, for an FP8
+ * cache, their decoded values times the row's scales in kd / vd (float64,
+ * row stride d). */
+static void kv_rows(const orc_problem_t *P, int b, int kv, int L, double *kd, double *vd,
+                    const void **k_out, const void **v_out, int *kind, int64_t *stride) {
+  const int64_t base = (int64_t)b * P->sb + (int64_t)kv * P->sh;
+  if (!P->kv_fp8) {
+    const size_t esz = P->is_f32 ? 4 : 2;
+    *k_out = (const char *)P->k + base * (int64_t)esz;
+    *v_out = (const char *)P->v + base * (int64_t)esz;
+    *kind = P->is_f32;
+    *stride = P->sn;
+    return;
+  }
+  const double ks = (double)P->k_scale[(int64_t)b * P->Hkv + kv];
+  const double vs = (double)P->v_scale[(int64_t)b * P->Hkv + kv];
+  const uint8_t *kc = (const uint8_t *)P->k + base, *vc = (const uint8_t *)P->v + base;
+  for (int j = 0; j < L; ++j)
+    for (int i = 0; i < P->d; ++i) {
+      kd[(int64_t)j * P->d + i] = ks * orc_fp8_e4m3(kc[(int64_t)j * P->sn + i]);
+      vd[(int64_t)j * P->d + i] = vs * orc_fp8_e4m3(vc[(int64_t)j * P->sn + i]);
+    }
+  *k_out = kd;
+  *v_out = vd;
+  *kind = 2;
+  *stride = P->d;
+}
 
 enum { ORC_DENSE = 0, ORC_SYSTEMATIC = 1, ORC_STRATIFIED = 2, ORC_IID = 3, ORC_BERNOULLI_SYS = 4,
        ORC_IID_SPACINGS = 5 };
@@ -358,13 +422,15 @@ int orc_decode(const orc_problem_t *P, int kind, int S, const float *u, const fl
     double *p = (double *)malloc(sizeof(double) * (size_t)(P->n_max > 0 ? P->n_max : 1));
     double *C = (double *)malloc(sizeof(double) * (size_t)(P->n_max > 0 ? P->n_max : 1));
     double *T = (double *)malloc(sizeof(double) * (size_t)(S > 0 ? S : 1));
+    const size_t slab = P->kv_fp8 ? (size_t)(P->n_max > 0 ? P->n_max : 1) * (size_t)P->d : 1;
+    double *kd = (double *)malloc(sizeof(double) * slab);
+    double *vd = (double *)malloc(sizeof(double) * slab);
 #pragma omp for schedule(dynamic, 1)
     for (int r = 0; r < total; ++r) {
       const int row = rows ? rows[r] : r;
       const int b = row / P->Hq, h = row % P->Hq, kv = h / G;
       const int L = P->ctx_len[b];
       double *o = out + (int64_t)r * P->d;
-      const int64_t base = (int64_t)b * P->sb + (int64_t)kv * P->sh;
       if (L <= 0) {
         for (int i = 0; i < P->d; ++i) o[i] = 0.0;
         if (idx && kind != ORC_DENSE)
@@ -388,13 +454,14 @@ int orc_decode(const orc_problem_t *P, int kind, int S, const float *u, const fl
       } else {
         for (int i = 0; i < P->d; ++i) qd[i] = elem(P->q, P->is_f32, ((int64_t)b * P->Hq + h) * P->d + i);
       }
-      const size_t esz = P->is_f32 ? 4 : 2;
-      const void *kb = (const char *)P->k + base * (int64_t)esz;
-      const void *vb = (const char *)P->v + base * (int64_t)esz;
-      orc_scores(wq, P->d, kb, P->is_f32, P->sn, L, P->scale, s);
+      const void *kb, *vb;
+      int kvk;
+      int64_t rs;
+      kv_rows(P, b, kv, L, kd, vd, &kb, &vb, &kvk, &rs);
+      orc_scores(wq, P->d, kb, kvk, rs, L, P->scale, s);
       orc_softmax(s, L, p);
       if (kind == ORC_DENSE) {
-        orc_weighted_sum(p, vb, P->is_f32, P->sn, L, P->d, o);
+        orc_weighted_sum(p, vb, kvk, rs, L, P->d, o);
         continue;
       }
       orc_cdf(p, L, C);
@@ -408,8 +475,10 @@ int orc_decode(const orc_problem_t *P, int kind, int S, const float *u, const fl
         orc_thresholds(kind == ORC_STRATIFIED ? 1 : 2, u + (int64_t)row * S, S, T);
       int32_t *ix = idx + (int64_t)r * S;
       orc_inverse_cdf(C, L, T, S, ix);
-      orc_gather_mean(vb, P->is_f32, P->sn, P->d, ix, S, o);
+      orc_gather_mean(vb, kvk, rs, P->d, ix, S, o);
     }
+    free(kd);
+    free(vd);
     free(qd);
     free(wg);
     free(mk);
@@ -440,6 +509,9 @@ int orc_decode_flash(const orc_problem_t *P, int tile, int S_tile, const float *
 #endif
     double *qd = (double *)malloc(sizeof(double) * (size_t)P->d);
     double *s = (double *)malloc(sizeof(double) * (size_t)(P->n_max > 0 ? P->n_max : 1));
+    const size_t slab = P->kv_fp8 ? (size_t)(P->n_max > 0 ? P->n_max : 1) * (size_t)P->d : 1;
+    double *kd = (double *)malloc(sizeof(double) * slab);
+    double *vd = (double *)malloc(sizeof(double) * slab);
 #pragma omp for schedule(dynamic, 1)
     for (int r = 0; r < total; ++r) {
       const int row = rows ? rows[r] : r;
@@ -456,13 +528,17 @@ int orc_decode_flash(const orc_problem_t *P, int tile, int S_tile, const float *
         for (int i = 0; i < P->d; ++i) o[i] = 0.0;
         continue;
       }
-      const int64_t base = (int64_t)b * P->sb + (int64_t)kv * P->sh;
-      const size_t esz = P->is_f32 ? 4 : 2;
       for (int i = 0; i < P->d; ++i) qd[i] = elem(P->q, P->is_f32, ((int64_t)b * P->Hq + h) * P->d + i);
-      orc_scores(qd, P->d, (const char *)P->k + base * (int64_t)esz, P->is_f32, P->sn, L, P->scale, s);
-      orc_flash(s, (const char *)P->v + base * (int64_t)esz, P->is_f32, P->sn, L, P->d, tile, S_tile,
-                u + (int64_t)row * Tm, ix, o, w, NULL, cdf ? cdf + (int64_t)r * P->n_max : NULL);
+      const void *kb, *vb;
+      int kvk;
+      int64_t rs;
+      kv_rows(P, b, kv, L, kd, vd, &kb, &vb, &kvk, &rs);
+      orc_scores(qd, P->d, kb, kvk, rs, L, P->scale, s);
+      orc_flash(s, vb, kvk, rs, L, P->d, tile, S_tile, u + (int64_t)row * Tm, ix, o, w, NULL,
+                cdf ? cdf + (int64_t)r * P->n_max : NULL);
     }
+    free(kd);
+    free(vd);
     free(qd);
     free(s);
   }

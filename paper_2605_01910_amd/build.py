@@ -2,6 +2,7 @@
 
 from __future__ import annotations
 
+import glob
 import os
 import shutil
 import subprocess
@@ -13,7 +14,10 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libsanta.so")
-SOURCES = ["santa_api.hip", "santa_kernels.hip", "santa_fused.hip", "santa_measure.hip"]
+# every translation unit of the library: the C ABI, the launch dispatch, the
+# multi-kernel variant, the calibration read, and one unit per kernel family
+# and element type (so that hipcc compiles the kernel instantiations in parallel)
+SOURCES = sorted(os.path.basename(f) for f in glob.glob(os.path.join(CSRC, "*.hip")))
 ARCH = "gfx950"
 
 
@@ -46,7 +50,7 @@ def build(verbose: bool = False) -> str:
             raise RuntimeError("hipcc failed for " + src)
         return obj
 
-    with ThreadPoolExecutor(len(SOURCES)) as ex:
+    with ThreadPoolExecutor(min(len(SOURCES), max(1, os.cpu_count() or 1))) as ex:
         objs = list(ex.map(compile_one, SOURCES))
     tmp = LIB + ".tmp"
     cmd = [cc, "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp, *objs]

@@ -47,29 +47,10 @@ int choose_split(int64_t rows, int64_t n_k) {
   return p;
 }
 
-// Tuning knobs read from the environment on every call (measurement sweeps and
-// tests of both paths; a workspace must be sized under the same settings):
-//   SANTA_VARIANT=multi  use the multi-kernel path instead of the fused launch
-//   SANTA_SPLITS=T       splits per row of the fused path
-//   SANTA_QUEUE=1        large batches: stream and value stage in one launch with
-//                        per-XCD work queues (k_stream_value) instead of two
-struct Tuning {
-  int fused, splits;
-  int sampled_path;  // 0: by size, 1: one persistent launch, 2: stream + value stage
-  int queue;         // stream + value stage in one launch (per-XCD work queues)
-};
-
-Tuning tuning() {
-  Tuning r{1, 0, 0, 0};
-  if (const char *v = std::getenv("SANTA_QUEUE")) r.queue = std::atoi(v) != 0;
-  if (const char *v = std::getenv("SANTA_VARIANT")) r.fused = std::string(v) != "multi";
-  if (const char *v = std::getenv("SANTA_SPLITS")) r.splits = std::atoi(v);
-  if (const char *v = std::getenv("SANTA_SAMPLED")) {
-    const std::string s(v);
-    r.sampled_path = s == "fused" ? 1 : s == "split" ? 2 : 0;
-  }
-  return r;
-}
+// The calling thread's launch options (santa_set_options).  They select a
+// launch path for tuning and for tests of every path; a workspace must be
+// sized under the options of the calls that use it.
+thread_local santa_options_t g_opts{SANTA_PATH_AUTO, 0};
 
 // Splits per row of the fused path: enough that the whole batch of rows fills
 // about `target` workgroups, at least ceil(n_k / kSplitMax).  Sampled steps
@@ -84,7 +65,7 @@ int fused_splits(int64_t rows_kv, int64_t n_k, int64_t target) {
   int fill = 128;
   while (fill > 1 && (int64_t)fill * rows_kv > target) fill >>= 1;
   int T = std::max(tmin, fill);
-  if (tuning().splits > 0) T = std::max(tmin, tuning().splits);
+  if (g_opts.splits > 0) T = std::max(tmin, (int)g_opts.splits);
   return T;
 }
 
@@ -107,7 +88,20 @@ santa_status_t check_kv(const santa_kv_t *kv, const santa_shape_t *sh, bool need
   if (!kv) return fail(SANTA_ERR_INVALID_ARG, "kv is NULL");
   if ((need_k && !kv->k) || !kv->v) return fail(SANTA_ERR_INVALID_ARG, "kv->k or kv->v is NULL");
   if (kv->n_k < 1) return fail(SANTA_ERR_INVALID_ARG, "n_k must be >= 1");
-  const int64_t esz = sh->dtype == SANTA_BF16 ? 2 : 4;
+  if (kv->kv_dtype != SANTA_KV_AS_Q && kv->kv_dtype != SANTA_KV_FP8_E4M3)
+    return fail(SANTA_ERR_INVALID_ARG, "kv_dtype must be SANTA_KV_AS_Q or SANTA_KV_FP8_E4M3");
+  const bool fp8 = kv->kv_dtype == SANTA_KV_FP8_E4M3;
+  if (fp8) {
+    if (sh->dtype != SANTA_BF16)
+      return fail(SANTA_ERR_UNSUPPORTED, "an FP8 cache needs bfloat16 queries (shape->dtype)");
+    if (!kv->k_scale || !kv->v_scale)
+      return fail(SANTA_ERR_INVALID_ARG, "an FP8 cache needs k_scale and v_scale");
+    if (kv->k_new || kv->v_new)
+      return fail(SANTA_ERR_UNSUPPORTED, "the fused append is not available with an FP8 cache");
+    if (g_opts.path == SANTA_PATH_MULTI)
+      return fail(SANTA_ERR_UNSUPPORTED, "an FP8 cache needs the fused launch layout");
+  }
+  const int64_t esz = fp8 ? 1 : sh->dtype == SANTA_BF16 ? 2 : 4;
   const int64_t a = 16 / esz;  // elements per 16 bytes
   if (kv->stride_b < 0 || kv->stride_n < 0 || kv->stride_h < 0)
     return fail(SANTA_ERR_INVALID_ARG, "strides must be non-negative");
@@ -138,6 +132,7 @@ santa::Plan make_plan(const santa_shape_t *sh, const santa_kv_t *kv, int S, int 
   p.Hkv = sh->num_kv_heads;
   p.G = p.Hq / p.Hkv;
   p.dtype = sh->dtype;
+  p.elem = kv->kv_dtype == SANTA_KV_FP8_E4M3 ? 2 : sh->dtype == SANTA_BF16 ? 0 : 1;
   p.n_k = kv->n_k;
   p.Ls = choose_split((int64_t)p.B * p.Hkv, p.n_k);
   p.T = (int)((p.n_k + p.Ls - 1) / p.Ls);
@@ -151,18 +146,18 @@ santa::Plan make_plan(const santa_shape_t *sh, const santa_kv_t *kv, int S, int 
     off = align256(off + bytes);
     return o;
   };
-  // Every layout, fused or not, starts with the error flag (with the
-  // work-queue tickets) and the fused paths' counter area, at the same offsets
+  // Every layout, fused or not, starts with the error flag and the fused
+  // paths' counter area, at the same offsets
   // and of the same size, so that calls of any kind and shape can share one
   // workspace in any order: no layout puts data where another keeps counters.
   // The counters must start at zero (santa_workspace_init).
   p.off_err = take(santa::kErrBytes);
   p.off_sync = take((size_t)santa::kSyncRowsMax * santa::kSyncStride * 4);
-  const Tuning tune = tuning();
+  const bool fused = g_opts.path != SANTA_PATH_MULTI;
   const bool small_budget = (kind == SANTA_KIND_SYSTEMATIC || kind == SANTA_KIND_STRATIFIED ||
                              kind == SANTA_KIND_IID) && S <= 1024;
   const int Tf = fused_splits((int64_t)p.B * p.Hkv, p.n_k, small_budget ? 256 : 512);
-  if (kind != SANTA_KIND_BERNOULLI && tune.fused && Tf <= santa::kMaxSplits &&
+  if (kind != SANTA_KIND_BERNOULLI && fused && Tf <= santa::kMaxSplits &&
       (int64_t)p.B * p.Hkv <= santa::kSyncRowsMax) {
     p.fused = 1;
     p.T = Tf;
@@ -171,10 +166,9 @@ santa::Plan make_plan(const santa_shape_t *sh, const santa_kv_t *kv, int S, int 
     const bool sampled = kind != SANTA_KIND_DENSE;
     // sampled steps whose rows do not fit in one resident round of about 1024
     // workgroups take the two-launch path
-    p.split2 = sampled && (tune.sampled_path == 2 ||
-                           (tune.sampled_path == 0 && (int64_t)p.B * p.Hkv * p.T > 1024));
+    p.split2 = sampled && (g_opts.path == SANTA_PATH_TWO_LAUNCH ||
+                           (g_opts.path == SANTA_PATH_AUTO && (int64_t)p.B * p.Hkv * p.T > 1024));
     if (p.split2) {
-      p.queue = tune.queue;
       p.npitch = ((int64_t)p.n_k + 63) & ~int64_t(63);
       p.off_stats = take(rows * p.T * 8);
       p.off_stash = take(rows * (size_t)p.npitch * 2);   // 16-bit in-block CDF
@@ -186,7 +180,7 @@ santa::Plan make_plan(const santa_shape_t *sh, const santa_kv_t *kv, int S, int 
     p.total = off;
     return p;
   }
-  if (kind == SANTA_KIND_BERNOULLI && tune.fused && Tf <= santa::kMaxSplits) {
+  if (kind == SANTA_KIND_BERNOULLI && fused && Tf <= santa::kMaxSplits) {
     // Bernoulli scores from the feature-major cache, then the value stage of
     // the two-launch path (one workgroup per query head)
     p.fused = 1;
@@ -244,6 +238,8 @@ santa::KvView make_view(const santa_kv_t *kv) {
   v.n_k = kv->n_k;
   v.k_new = kv->k_new;
   v.v_new = kv->v_new;
+  v.ks = kv->kv_dtype == SANTA_KV_FP8_E4M3 ? kv->k_scale : nullptr;
+  v.vs = kv->kv_dtype == SANTA_KV_FP8_E4M3 ? kv->v_scale : nullptr;
   return v;
 }
 
@@ -279,6 +275,8 @@ santa_status_t sampled(const void *q, const santa_kv_t *kv, const santa_shape_t 
   s = check_ws(p, ws, ws_bytes);
   if (s == SANTA_OK && kv->k_new && !p.fused)
     s = fail(SANTA_ERR_UNSUPPORTED, "the fused append (k_new, v_new) needs the fused path");
+  if (s == SANTA_OK && kv->kv_dtype != SANTA_KV_AS_Q && !p.fused)
+    s = fail(SANTA_ERR_UNSUPPORTED, "an FP8 cache needs the fused launch layout");
   if (s != SANTA_OK) return s;
   if (p.fused)
     return hip_status(santa::launch_fused_sampled(p, make_view(kv), q, log2_scale(scale),
@@ -322,6 +320,8 @@ santa_status_t santa_decode_dense(const void *q, const santa_kv_t *kv, const san
   s = check_ws(p, ws, ws_bytes);
   if (s == SANTA_OK && kv->k_new && !p.fused)
     s = fail(SANTA_ERR_UNSUPPORTED, "the fused append (k_new, v_new) needs the fused path");
+  if (s == SANTA_OK && kv->kv_dtype != SANTA_KV_AS_Q && !p.fused)
+    s = fail(SANTA_ERR_UNSUPPORTED, "an FP8 cache needs the fused launch layout");
   if (s != SANTA_OK) return s;
   if (p.fused)
     return hip_status(santa::launch_fused_dense(p, make_view(kv), q, log2_scale(scale), out,
@@ -355,6 +355,8 @@ santa_status_t santa_decode_bernoulli_qk(const void *q, const santa_kt_t *kt,
   santa_status_t s = common_checks(q, kv, shape, scale, out, false);
   if (s != SANTA_OK) return s;
   if (kv->block_table) return fail(SANTA_ERR_UNSUPPORTED, "Bernoulli scores need a contiguous cache");
+  if (kv->kv_dtype != SANTA_KV_AS_Q)
+    return fail(SANTA_ERR_UNSUPPORTED, "Bernoulli scores need a cache in the query's dtype");
   if (!kt || !kt->k_t) return fail(SANTA_ERR_INVALID_ARG, "kt or kt->k_t is NULL");
   const int64_t a = shape->dtype == SANTA_BF16 ? 8 : 4;
   if (kt->stride_b < 0 || kt->stride_h < 0 || kt->stride_d < kv->n_k)
@@ -396,6 +398,8 @@ santa_status_t santa_decode_iid(const void *q, const santa_kv_t *kv, const santa
   s = check_ws(p, ws, ws_bytes);
   if (s == SANTA_OK && kv->k_new && !p.fused)
     s = fail(SANTA_ERR_UNSUPPORTED, "the fused append (k_new, v_new) needs the fused path");
+  if (s == SANTA_OK && kv->kv_dtype != SANTA_KV_AS_Q && !p.fused)
+    s = fail(SANTA_ERR_UNSUPPORTED, "an FP8 cache needs the fused launch layout");
   if (s != SANTA_OK) return s;
   if (!p.fused) return fail(SANTA_ERR_UNSUPPORTED, "the i.i.d. step needs the fused launch layout");
   return hip_status(santa::launch_fused_sampled(p, make_view(kv), q, log2_scale(scale), 2, u,
@@ -418,6 +422,8 @@ santa_status_t santa_decode_flash(const void *q, const santa_kv_t *kv, const san
   s = check_ws(p, ws, ws_bytes);
   if (s == SANTA_OK && kv->k_new && !p.fused)
     s = fail(SANTA_ERR_UNSUPPORTED, "the fused append (k_new, v_new) needs the fused path");
+  if (s == SANTA_OK && kv->kv_dtype != SANTA_KV_AS_Q && !p.fused)
+    s = fail(SANTA_ERR_UNSUPPORTED, "an FP8 cache needs the fused launch layout");
   if (s != SANTA_OK) return s;
   if (!p.fused) return fail(SANTA_ERR_UNSUPPORTED, "the flash step needs the fused launch layout");
   return hip_status(santa::launch_fused_flash(p, make_view(kv), q, log2_scale(scale), ilog2(tile),
@@ -435,6 +441,62 @@ santa_status_t santa_stream_read(const void *buf, size_t bytes, uint32_t *sink, 
   if (reinterpret_cast<uintptr_t>(buf) & 15) return fail(SANTA_ERR_INVALID_ARG, "buf must be 16-byte aligned");
   return hip_status(santa::launch_stream_read(buf, bytes, sink, SANTA_STREAM_READ_GROUPS,
                                               static_cast<hipStream_t>(stream)));
+}
+
+santa_status_t santa_set_options(const santa_options_t *opts) {
+  g_last_error.clear();
+  if (!opts) {
+    g_opts = santa_options_t{SANTA_PATH_AUTO, 0};
+    return SANTA_OK;
+  }
+  if (opts->path < SANTA_PATH_AUTO || opts->path > SANTA_PATH_MULTI)
+    return fail(SANTA_ERR_INVALID_ARG, "path must be a santa_path_t");
+  if (opts->splits < 0 || opts->splits > santa::kMaxSplits)
+    return fail(SANTA_ERR_INVALID_ARG, "splits must be in [0, 256]");
+  g_opts = *opts;
+  return SANTA_OK;
+}
+
+santa_status_t santa_get_options(santa_options_t *opts) {
+  g_last_error.clear();
+  if (!opts) return fail(SANTA_ERR_INVALID_ARG, "opts is NULL");
+  *opts = g_opts;
+  return SANTA_OK;
+}
+
+santa_status_t santa_plan_info(const santa_shape_t *shape, const santa_kv_t *kv, int32_t S,
+                               int32_t kind, santa_plan_info_t *info) {
+  g_last_error.clear();
+  if (!info) return fail(SANTA_ERR_INVALID_ARG, "info is NULL");
+  santa_status_t s = check_shape(shape);
+  if (s != SANTA_OK) return s;
+  if (!kv || kv->n_k < 1) return fail(SANTA_ERR_INVALID_ARG, "kv is NULL or n_k < 1");
+  if (kind < SANTA_KIND_DENSE || kind > SANTA_KIND_IID) return fail(SANTA_ERR_INVALID_ARG, "bad kind");
+  const int32_t plan_kind = kind == SANTA_KIND_FLASH ? SANTA_KIND_DENSE : kind;
+  if (plan_kind != SANTA_KIND_DENSE && (S < 1 || S > (1 << 24)))
+    return fail(SANTA_ERR_INVALID_ARG, "S must be in [1, 2^24]");
+  const santa::Plan p = make_plan(shape, kv, S, plan_kind);
+  info->splits = p.T;
+  info->split_len = p.Ls;
+  info->workspace = p.total;
+  if (!p.fused) {
+    info->path = SANTA_PATH_MULTI;
+    info->kernels = "multi-kernel variant (k_score_cdf / k_dense_split / k_bern_score, k_offsets, "
+                    "k_sample, k_merge_*)";
+  } else if (kind == SANTA_KIND_BERNOULLI) {
+    info->path = SANTA_PATH_TWO_LAUNCH;
+    info->kernels = "k_bern_stream + k_value_heads";
+  } else if (kind == SANTA_KIND_DENSE || kind == SANTA_KIND_FLASH) {
+    info->path = SANTA_PATH_ONE_LAUNCH;
+    info->kernels = kind == SANTA_KIND_DENSE ? "k_fused_dense" : "k_fused_dense (flash mode)";
+  } else if (p.split2) {
+    info->path = SANTA_PATH_TWO_LAUNCH;
+    info->kernels = "k_stream_cdf + k_value_heads";
+  } else {
+    info->path = SANTA_PATH_ONE_LAUNCH;
+    info->kernels = "k_fused_sampled";
+  }
+  return SANTA_OK;
 }
 
 santa_status_t santa_time_next_call(void *start_event, void *stop_event) {

@@ -90,6 +90,66 @@ struct Chunk<float> {
   }
 };
 
+// 8 consecutive features of one row of an OCP FP8 E4M3 cache (one byte per
+// feature), loaded with one 64-bit load.  The codes widen exactly: to float32
+// with v_cvt_pk_f32_fp8 (two codes per instruction) and to packed bfloat16
+// with v_cvt_scalef32_pk_bf16_fp8 at scale 1 (every E4M3 value, subnormals
+// included, is a bfloat16 value).  The per-(batch, KV head) dequantisation
+// scale is applied by the caller, outside the feature loops.
+typedef unsigned int nt_u32x2 __attribute__((ext_vector_type(2)));
+
+template <>
+struct Chunk<uint8_t> {
+  uint2 w;
+  __device__ __forceinline__ static Chunk zero() { return Chunk{make_uint2(0, 0)}; }
+  __device__ __forceinline__ static Chunk load(const uint8_t *p) {
+    return Chunk{*reinterpret_cast<const uint2 *>(p)};
+  }
+  __device__ __forceinline__ static Chunk load_nt(const uint8_t *p) {
+    const nt_u32x2 v = __builtin_nontemporal_load(reinterpret_cast<const nt_u32x2 *>(p));
+    return Chunk{make_uint2(v[0], v[1])};
+  }
+  __device__ __forceinline__ void to_float(float (&f)[8]) const {
+    typedef float f32x2_t __attribute__((ext_vector_type(2)));
+    const f32x2_t a = __builtin_amdgcn_cvt_pk_f32_fp8(w.x, false);
+    const f32x2_t b = __builtin_amdgcn_cvt_pk_f32_fp8(w.x, true);
+    const f32x2_t c = __builtin_amdgcn_cvt_pk_f32_fp8(w.y, false);
+    const f32x2_t d = __builtin_amdgcn_cvt_pk_f32_fp8(w.y, true);
+    f[0] = a[0]; f[1] = a[1]; f[2] = b[0]; f[3] = b[1];
+    f[4] = c[0]; f[5] = c[1]; f[6] = d[0]; f[7] = d[1];
+  }
+  __device__ __forceinline__ void require() const { asm volatile("" ::"v"(w.x), "v"(w.y)); }
+  // the 8 codes as 4 packed bfloat16 pairs (features 2i, 2i+1 in word i)
+  __device__ __forceinline__ uint4 to_bf16() const {
+    return make_uint4(
+        __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w.x, 1.0f, false)),
+        __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w.x, 1.0f, true)),
+        __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w.y, 1.0f, false)),
+        __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w.y, 1.0f, true)));
+  }
+  // <this, q> over the 8 features with a bfloat16 query
+  __device__ __forceinline__ float dot(const Chunk<uint16_t> &q) const {
+    const uint4 k = to_bf16();
+    float a = dot2_bf16(k.x, q.w.x, 0.0f);
+    a = dot2_bf16(k.y, q.w.y, a);
+    a = dot2_bf16(k.z, q.w.z, a);
+    return dot2_bf16(k.w, q.w.w, a);
+  }
+};
+
+// Element type of q and out for a cache of element type E: the cache's own
+// type, except bfloat16 queries and outputs for an FP8 cache.
+template <typename E>
+struct QElemOf {
+  using type = E;
+};
+template <>
+struct QElemOf<uint8_t> {
+  using type = uint16_t;
+};
+template <typename E>
+using QE = typename QElemOf<E>::type;
+
 // ---------------------------------------------------------------------------
 // Cross-lane helpers.  DPP controls (gfx9 encoding): quad_perm [1,0,3,2] = 0xB1,
 // quad_perm [2,3,0,1] = 0x4E, row_half_mirror = 0x141, row_mirror = 0x140.
@@ -181,6 +241,17 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 // ---------------------------------------------------------------------------
 // KV addressing
 // ---------------------------------------------------------------------------
+// Dequantisation scales of row (b, kvh) of an FP8 cache (K, V); 1 for other
+// element types, whose stored values are the values.
+template <typename E>
+__device__ __forceinline__ float2 kv_scales(const KvView &kv, int b, int kvh, int Hkv) {
+  if constexpr (sizeof(E) == 1) {
+    const int64_t r = (int64_t)b * Hkv + kvh;
+    return make_float2(kv.ks[r], kv.vs[r]);
+  } else {
+    return make_float2(1.0f, 1.0f);
+  }
+}
 __device__ __forceinline__ int seq_len(const KvView &kv, int b) {
   if (!kv.ctx) return kv.n_k;
   int L = kv.ctx[b];

@@ -14,8 +14,7 @@ constexpr int kSplitMax = 1024; // largest KV split (keys) handled by one workgr
 constexpr int kMaxSplits = 256; // largest number of splits per row in the fused kernels
 constexpr int kSyncStride = 64; // ints per row of fused-path counters (256 B apart)
 constexpr int kSyncRowsMax = 4096; // KV rows (batch * kv heads) of the fused paths' counter area
-constexpr int kTicketOffset = 64; // bytes from the error flag to the 8 per-XCD ticket counters
-constexpr int kErrBytes = 128;    // error flag and ticket counters
+constexpr int kErrBytes = 128;    // the error flag's section
 
 // Per-call launch plan.  The KV sequence of every (batch, kv head) row is cut
 // into T splits of Ls keys; each split is one workgroup.  All sizes below are
@@ -23,6 +22,7 @@ constexpr int kErrBytes = 128;    // error flag and ticket counters
 // decode calls agree on the layout.
 struct Plan {
   int B, Hq, Hkv, G, dtype;
+  int elem;     // element type of K and V: 0 bfloat16, 1 float32, 2 FP8 E4M3 (q, out bfloat16)
   int n_k;      // max context length
   int Ls;       // keys per split (multi-kernel: multiple of 16; fused: longest split of
                 // any row, multiple of 64; <= kSplitMax)
@@ -32,8 +32,6 @@ struct Plan {
   int fused;    // 1: single persistent launch (per-row split lengths), 0: multi-kernel
   int split2;   // fused sampled: 1 = stream + CDF stash, then one workgroup per
                 // query head; 0 = one persistent launch
-  int queue;    // split2: 1 = both stages in one launch (per-XCD work queues),
-                // 0 = two launches
   int64_t npitch;  // two-launch sampled: stash entries per query head (n_k rounded up to 64)
   // workspace carve-up (byte offsets, 256-aligned)
   size_t off_stats;  // float2 [B*Hq*T]     per-split (max, sum) in log2 units
@@ -48,8 +46,7 @@ struct Plan {
   size_t off_bw;     // float  [B*Hq*128]   Bernoulli query weights
   size_t off_blist;  // int    [B*Hkv*128]  Bernoulli feature list
   size_t off_bn;     // int    [B*Hkv]      Bernoulli feature count
-  size_t off_err;    // int    [1]          fused: a wait gave up; at +kTicketOffset
-                     // uint [8] per-XCD ticket counters of the one-launch split2 path
+  size_t off_err;    // int    [1]          fused: a wait gave up
   size_t off_sync;   // u64    [kSyncRowsMax*kSyncStride/2] fused: per-row counters; the area
                      // has the same offset and size in every layout, so calls of any kind
                      // and shape find their counters where earlier calls left them
@@ -66,6 +63,7 @@ struct KvView {
   int32_t max_pages;
   int32_t n_k;
   const void *k_new, *v_new;  // nullable: the current token's rows [B, Hkv, 128], appended in-launch
+  const float *ks, *vs;       // FP8 cache: dequantisation scales [B*Hkv] of K and V (else null)
 };
 
 struct KtView {

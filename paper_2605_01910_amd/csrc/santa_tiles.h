@@ -12,9 +12,11 @@ namespace santa {
 // ---------------------------------------------------------------------------
 // shared device pieces
 // ---------------------------------------------------------------------------
+// The G query rows of a KV group, 8 features per lane, in the query element
+// type QE<E> (bfloat16 for an FP8 cache).
 template <typename E, int G>
 struct QRegs {
-  Chunk<E> h[G];
+  Chunk<QE<E>> h[G];
   // Makes every register available (the compiler waits for their loads here).
   __device__ __forceinline__ void require() const {
 #pragma unroll
@@ -31,12 +33,12 @@ __device__ __forceinline__ int quarter_gray(int c) {
 }
 
 template <typename E, int G>
-__device__ __forceinline__ QRegs<E, G> load_q(const E *q, int b, int Hq, int kvh, int c) {
+__device__ __forceinline__ QRegs<E, G> load_q(const QE<E> *q, int b, int Hq, int kvh, int c) {
   QRegs<E, G> r;
   const int perm = G == 4 ? quarter_gray(c) : 0;
 #pragma unroll
   for (int h = 0; h < G; ++h)
-    r.h[h] = Chunk<E>::load(q + ((int64_t)b * Hq + kvh * G + (h ^ perm)) * kHeadDim + c * 8);
+    r.h[h] = Chunk<QE<E>>::load(q + ((int64_t)b * Hq + kvh * G + (h ^ perm)) * kHeadDim + c * 8);
   return r;
 }
 
@@ -54,12 +56,13 @@ __device__ __forceinline__ void store_out(uint16_t *p, float x) {
 }
 __device__ __forceinline__ void store_out(float *p, float x) { *p = x; }
 
-// Key rows per lane and batch of the score tile (U 16-byte loads per lane in
-// flight, twice that while a batch is scored): 8 for bf16 with G <= 4, 4 for
-// the wider register sets of fp32 rows or G = 8.
+// Key rows per lane and batch of the score tile (U loads per lane in flight,
+// twice that while a batch is scored): 8 for bf16 with G <= 4, 4 for the
+// wider register sets of fp32 rows or G = 8; FP8 rows take half the bytes and
+// registers per load, so twice as many.
 template <typename E, int G>
 constexpr int score_unroll() {
-  return (sizeof(E) == 2 && G <= 4) ? 8 : 4;
+  return sizeof(E) == 1 ? (G <= 4 ? 16 : 8) : (sizeof(E) == 2 && G <= 4) ? 8 : 4;
 }
 
 // Block-table entries of the pages one split covers, one per lane: lane l of
@@ -115,6 +118,14 @@ __device__ __forceinline__ uint4 buffer_load16(const void *p, uint32_t lb) {
   return make_uint4(v[0], v[1], v[2], v[3]);
 }
 
+// 8 bytes at byte offset lb from p, as buffer_load16 (FP8 rows: 8 features).
+__device__ __forceinline__ uint2 buffer_load8(const void *p, uint32_t lb) {
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), 0, 0x7fffffff, 0x00020000);
+  const auto v = __builtin_amdgcn_raw_buffer_load_b64(rs, lb, 0, 2);
+  return make_uint2(v[0], v[1]);
+}
+
 // Features 8c..8c+7 of key row (row0 + slot); lb = (slot*stride_n + 8c) *
 // sizeof(E) is the lane's byte offset (32 bits; the host bounds the stride).
 template <typename E, bool PAGED>
@@ -125,7 +136,9 @@ __device__ __forceinline__ Chunk<E> load_key_row(const E *base, const KvView &kv
     if (kv.ps_log2 < 4) return Chunk<E>::load_nt(base + row_offset<true>(kv, b, kvh, row0 + slot) + c * 8);
   }
   const E *p = base + row16_offset<PAGED>(kv, pw, b, kvh, row0);
-  if constexpr (sizeof(E) == 2) {
+  if constexpr (sizeof(E) == 1) {
+    return Chunk<E>{buffer_load8(p, lb)};
+  } else if constexpr (sizeof(E) == 2) {
     return Chunk<E>{buffer_load16(p, lb)};
   } else {
     const uint4 x = buffer_load16(p, lb), y = buffer_load16(p, lb + 16);
@@ -424,8 +437,15 @@ __device__ __forceinline__ void reduce_slots(float (&acc)[G][8], float *red /* [
   __syncthreads();
 }
 
+// Threshold r of a row in global CDF units, ((r + u_r)/S) Z (Sec. 2.1,
+// "Construction"), kept strictly below Z.  In float32, r + u rounds up to
+// r + 1 when u lies within half an ulp of 1 (u = 1 - 2^-24 with r >= 1), and
+// (r + u) * fl(1/S) can round up to 1 when S is not a power of two; at r =
+// S - 1 either would put the threshold at Z, past every key's CDF interval.
+// The fraction is capped at the largest float below 1, whose product with a
+// normal Z rounds below Z.  The cap keeps tau non-decreasing in r.
 __device__ __forceinline__ float threshold(int r, float ur, float invS, float Z) {
-  return ((float)r + ur) * invS * Z;
+  return fminf(((float)r + ur) * invS, 0x1.fffffep-1f) * Z;
 }
 
 // Number of j < n with a * P[j] <= x (P non-decreasing): branch-free binary lifting.

@@ -9,6 +9,7 @@ fallback path.  PyTorch provides device memory and streams.
 
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
 from typing import Optional
@@ -20,13 +21,18 @@ LIB_PATH = os.path.join(_HERE, "libsanta.so")
 
 SANTA_OK, SANTA_ERR_INVALID_ARG, SANTA_ERR_UNSUPPORTED, SANTA_ERR_WORKSPACE, SANTA_ERR_HIP = range(5)
 SANTA_BF16, SANTA_F32 = 0, 1
+SANTA_KV_AS_Q, SANTA_KV_FP8_E4M3 = 0, 1
 (SANTA_KIND_DENSE, SANTA_KIND_SYSTEMATIC, SANTA_KIND_STRATIFIED, SANTA_KIND_BERNOULLI,
  SANTA_KIND_FLASH, SANTA_KIND_IID) = range(6)
+SANTA_PATH_AUTO, SANTA_PATH_ONE_LAUNCH, SANTA_PATH_TWO_LAUNCH, SANTA_PATH_MULTI = range(4)
+PATHS = {"auto": SANTA_PATH_AUTO, "one": SANTA_PATH_ONE_LAUNCH, "two": SANTA_PATH_TWO_LAUNCH,
+         "multi": SANTA_PATH_MULTI}
 
 # every symbol include/santa.h declares
 EXPORTS = ("santa_workspace_size", "santa_workspace_init", "santa_decode_dense",
            "santa_decode_systematic", "santa_decode_stratified", "santa_decode_bernoulli_qk",
            "santa_decode_iid", "santa_decode_flash", "santa_stream_read", "santa_time_next_call",
+           "santa_set_options", "santa_get_options", "santa_plan_info",
            "santa_status_string", "santa_last_error")
 
 STREAM_READ_GROUPS = 4096  # SANTA_STREAM_READ_GROUPS: uint32 words of the sink
@@ -51,12 +57,24 @@ class santa_kv_t(ctypes.Structure):
                 ("ctx_len", ctypes.c_void_p), ("block_table", ctypes.c_void_p),
                 ("page_size", ctypes.c_int32), ("max_pages", ctypes.c_int32),
                 ("n_k", ctypes.c_int32),
-                ("k_new", ctypes.c_void_p), ("v_new", ctypes.c_void_p)]
+                ("k_new", ctypes.c_void_p), ("v_new", ctypes.c_void_p),
+                ("kv_dtype", ctypes.c_int32), ("k_scale", ctypes.c_void_p),
+                ("v_scale", ctypes.c_void_p)]
 
 
 class santa_kt_t(ctypes.Structure):
     _fields_ = [("k_t", ctypes.c_void_p), ("stride_b", ctypes.c_int64),
                 ("stride_h", ctypes.c_int64), ("stride_d", ctypes.c_int64)]
+
+
+class santa_options_t(ctypes.Structure):
+    _fields_ = [("path", ctypes.c_int32), ("splits", ctypes.c_int32)]
+
+
+class santa_plan_info_t(ctypes.Structure):
+    _fields_ = [("path", ctypes.c_int32), ("splits", ctypes.c_int32),
+                ("split_len", ctypes.c_int32), ("workspace", ctypes.c_size_t),
+                ("kernels", ctypes.c_char_p)]
 
 
 _lib: Optional[ctypes.CDLL] = None
@@ -85,12 +103,17 @@ def load() -> ctypes.CDLL:
     L.santa_decode_iid.argtypes = [P, KP, SP, ctypes.c_float, I32, P, P, P, P, SZ, P]
     L.santa_stream_read.argtypes = [P, SZ, P, P]
     L.santa_time_next_call.argtypes = [P, P]
+    OP = ctypes.POINTER(santa_options_t)
+    L.santa_set_options.argtypes = [OP]
+    L.santa_get_options.argtypes = [OP]
+    L.santa_plan_info.argtypes = [SP, KP, I32, I32, ctypes.POINTER(santa_plan_info_t)]
     L.santa_status_string.argtypes = [ctypes.c_int]
     L.santa_status_string.restype = ctypes.c_char_p
     L.santa_last_error.restype = ctypes.c_char_p
     for name in ("santa_workspace_init", "santa_decode_dense", "santa_decode_systematic",
                  "santa_decode_stratified", "santa_decode_bernoulli_qk", "santa_decode_flash",
-                 "santa_decode_iid", "santa_stream_read", "santa_time_next_call"):
+                 "santa_decode_iid", "santa_stream_read", "santa_time_next_call",
+                 "santa_set_options", "santa_get_options", "santa_plan_info"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -161,6 +184,17 @@ def kv_paged(k_pages: torch.Tensor, v_pages: torch.Tensor, block_table: torch.Te
                       block_table.data_ptr(), ps, block_table.shape[1], int(n_k))
 
 
+def set_fp8_cache(kv: santa_kv_t, k_scale: torch.Tensor, v_scale: torch.Tensor) -> santa_kv_t:
+    """Mark the cache of ``kv`` as OCP FP8 E4M3 codes (uint8 tensors) with
+    float32 dequantisation scales [batch, num_kv_heads] for K and V."""
+    assert k_scale.dtype == torch.float32 and v_scale.dtype == torch.float32
+    assert k_scale.is_contiguous() and v_scale.is_contiguous()
+    kv.kv_dtype = SANTA_KV_FP8_E4M3
+    kv.k_scale = k_scale.data_ptr()
+    kv.v_scale = v_scale.data_ptr()
+    return kv
+
+
 def kt_feature_major(k_t: torch.Tensor) -> santa_kt_t:
     """k_t: [B, Hkv, d, n] with keys contiguous."""
     assert k_t.stride(-1) == 1
@@ -180,6 +214,22 @@ def santa_workspace_size(shape: santa_shape_t, kv: santa_kv_t, S: int, kind: int
 
 def santa_workspace_init(ws: torch.Tensor, stream=None) -> None:
     _check(load().santa_workspace_init(_ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def workspace_error(ws: torch.Tensor) -> int:
+    """The int32 at byte 0 of a workspace: nonzero when a bounded wait of a
+    single-launch path gave up, which makes that call's outputs invalid.
+    Reading it synchronises with the device."""
+    return int(ws[:4].view(torch.int32).item())
+
+
+def check_workspace(ws: torch.Tensor) -> None:
+    """Raise SantaError if a bounded wait gave up in a call on this workspace."""
+    flag = workspace_error(ws)
+    if flag:
+        raise SantaError(SANTA_ERR_HIP, f"a bounded wait gave up (workspace flag {flag}); "
+                                        "the outputs of the calls since the last "
+                                        "santa_workspace_init are not valid")
 
 
 def alloc_workspace(shape: santa_shape_t, kv: santa_kv_t, S: int, kind: int,
@@ -248,10 +298,36 @@ def santa_decode_flash(q: torch.Tensor, kv: santa_kv_t, shape: santa_shape_t, sc
                                      _stream(stream)))
 
 
-def flash_tile_budget(S: int, n_tiles: int) -> int:
-    """The flash budget rule S_tile ~ S / T (Sec. 3.3): S total draws spread
-    uniformly over T tiles, rounded half up, at least one draw per tile."""
-    return max(1, (2 * int(S) + int(n_tiles)) // (2 * int(n_tiles)))
+def santa_set_options(path: int = SANTA_PATH_AUTO, splits: int = 0) -> None:
+    """Launch options of the calling thread (see santa_options_t)."""
+    _check(load().santa_set_options(ctypes.byref(santa_options_t(int(path), int(splits)))))
+
+
+def santa_get_options() -> tuple:
+    o = santa_options_t()
+    _check(load().santa_get_options(ctypes.byref(o)))
+    return o.path, o.splits
+
+
+@contextlib.contextmanager
+def options(path="auto", splits: int = 0):
+    """Context manager: run the body under launch options (path: a
+    SANTA_PATH_* code or one of "auto", "one", "two", "multi"), restoring the
+    thread's previous options afterwards."""
+    prev = santa_get_options()
+    santa_set_options(PATHS[path] if isinstance(path, str) else path, splits)
+    try:
+        yield
+    finally:
+        santa_set_options(*prev)
+
+
+def santa_plan_info(shape: santa_shape_t, kv: santa_kv_t, S: int, kind: int) -> dict:
+    info = santa_plan_info_t()
+    _check(load().santa_plan_info(ctypes.byref(shape), ctypes.byref(kv), int(S), int(kind),
+                                  ctypes.byref(info)))
+    return {"path": info.path, "splits": info.splits, "split_len": info.split_len,
+            "workspace": int(info.workspace), "kernels": info.kernels.decode()}
 
 
 def santa_stream_read(buf, sink, stream=None) -> None:

@@ -18,7 +18,7 @@ import torch
 
 from oracle import oracle as O
 from paper_2605_01910_amd import santa as S
-from workload import bf16_bits_to_f32
+from workload.device import DeviceWorkload, current_rows, dev_elems  # noqa: F401
 
 BAND = 1e-5
 DENSE_MAX_ABS, DENSE_REL_L2, SAMPLED_MAX_ABS = 2e-2, 5e-3, 2e-2
@@ -30,40 +30,6 @@ KIND_CODE = {"dense": S.SANTA_KIND_DENSE, "systematic": S.SANTA_KIND_SYSTEMATIC,
 def log(msg: str) -> None:
     print(msg, flush=True)
     sys.stdout.flush()
-
-
-def dev_elems(a: np.ndarray) -> torch.Tensor:
-    """numpy bf16 bits (uint16) or float32 -> device tensor of bfloat16 / float32."""
-    a = np.ascontiguousarray(a)
-    if a.dtype == np.uint16:
-        return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
-    return torch.from_numpy(a).cuda()
-
-
-class DeviceWorkload:
-    """Device copies of a workload plus the C descriptors that point at them."""
-
-    def __init__(self, w, layout: str = "nhd", pass_ctx: bool = True):
-        self.w = w
-        self.layout = layout
-        self.q = dev_elems(w.q)
-        self.ctx = torch.from_numpy(w.ctx_len.astype(np.int32)).cuda()
-        self.u = None if w.u is None else torch.from_numpy(w.u).cuda()
-        if w.paged:
-            self.kp, self.vp = dev_elems(w.k_pages), dev_elems(w.v_pages)
-            self.bt = torch.from_numpy(w.block_table).cuda()
-            self.kv = S.kv_paged(self.kp, self.vp, self.bt, self.ctx, w.n_max)
-        else:
-            k, v = dev_elems(w.k), dev_elems(w.v)
-            if layout == "hnd":
-                k, v = k.transpose(1, 2).contiguous(), v.transpose(1, 2).contiguous()
-            self.k, self.v = k, v
-            self.kv = S.kv_contiguous(k, v, self.ctx if pass_ctx else None, layout)
-        if w.kind == "bernoulli":
-            self.kt_t = dev_elems(w.k_t)
-            self.kt = S.kt_feature_major(self.kt_t)
-            self.u_q = torch.from_numpy(w.u_q).cuda()
-        self.shape = S.shape_of(self.q, w.Hkv)
 
 
 def run(w, kind: Optional[str] = None, layout: str = "nhd", want_idx: bool = True,
@@ -98,10 +64,22 @@ def run(w, kind: Optional[str] = None, layout: str = "nhd", want_idx: bool = Tru
         S.santa_decode_bernoulli_qk(dw.q, dw.kt, dw.kv, dw.shape, w.scale, w.B_draws, w.mode,
                                     dw.u_q, Sn, dw.u, idx, mask, out, ws)
     torch.cuda.synchronize()
+    S.check_workspace(ws)  # no bounded wait of the call gave up
     o = out.float().cpu().numpy().astype(np.float64).reshape(w.B * w.Hq, w.d)
     ix = None if idx is None else idx.cpu().numpy().reshape(w.B * w.Hq, Sn)
     mk = None if mask is None else mask.cpu().numpy()
     return o, ix, mk
+
+
+def value_rows(w, b: int, kvh: int) -> np.ndarray:
+    """V rows of sequence b, KV head kvh as the oracle reads them: the stored
+    elements, or for an FP8 cache their decoded values times the head's scale
+    (float64)."""
+    _, vb = w.logical_kv(b)
+    v = np.ascontiguousarray(vb[:, kvh, :])
+    if getattr(w, "kv_dtype", "") == "fp8":
+        return O.fp8_e4m3_decode(v) * np.float64(w.v_scale[b, kvh])
+    return v
 
 
 def check_dense(w, out: np.ndarray, rows: Optional[Sequence[int]] = None) -> dict:
@@ -124,8 +102,9 @@ def _thresholds(w, kind: str, row: int) -> np.ndarray:
 
 
 def check_sampled(w, out: np.ndarray, idx: np.ndarray, kind: Optional[str] = None,
-                  rows: Optional[Sequence[int]] = None) -> dict:
-    """Band-rule check of every index and gather check of every output row."""
+                  rows: Optional[Sequence[int]] = None, exact: bool = False) -> dict:
+    """Band-rule check of every index (exact: every index equal to the
+    oracle's, no band) and gather check of every output row."""
     kind = kind or w.kind
     rows = list(range(w.B * w.Hq)) if rows is None else list(rows)
     res = O.decode_workload(w, kind, rows=rows, want_cdf=True)
@@ -142,15 +121,17 @@ def check_sampled(w, out: np.ndarray, idx: np.ndarray, kind: Optional[str] = Non
         C = res.cdf[i, :L]
         T = _thresholds(w, kind if kind in ("stratified", "iid") else "systematic", r)
         diff = np.nonzero(g != o_idx)[0]
+        if exact:
+            assert diff.size == 0, (f"row {r}: {diff.size} indices differ from the oracle, first "
+                                    f"sample {diff[0] if diff.size else -1}")
         for m in diff:
             gm = int(g[m])
             lo = C[gm - 1] if gm > 0 else 0.0
-            ok = (lo - BAND <= T[m] < C[gm] + BAND) or (gm == L - 1 and T[m] >= C[gm] - BAND)
+            ok = lo - BAND <= T[m] < C[gm] + BAND
             assert ok, (f"row {r} sample {m}: GPU index {gm}, oracle {o_idx[m]}, T={T[m]!r}, "
                         f"F(g-1)={lo!r}, F(g)={C[gm]!r}")
         band += len(diff)
-        _, vb = w.logical_kv(b)
-        ref = O.gather_mean(np.ascontiguousarray(vb[:, h // w.G, :]), g)
+        ref = O.gather_mean(value_rows(w, b, h // w.G), g)
         e = float(np.abs(out[r] - ref).max())
         worst = max(worst, e)
         assert e <= SAMPLED_MAX_ABS, f"row {r}: sampled max abs error {e:.3e}"
@@ -177,10 +158,13 @@ def check_flash(w, out: np.ndarray, idx: np.ndarray, rows: Optional[Sequence[int
         kb, vb = w.logical_kv(b)
         T = (L + tile - 1) // tile
         assert np.all(g[T:] == -1), f"row {r}: draws past the row's tiles"
+        fp8 = getattr(w, "kv_dtype", "") == "fp8"
         res = O.decode_flash(w.q[b:b + 1], kb.reshape(1, L, w.Hkv, w.d), vb.reshape(1, L, w.Hkv, w.d),
                              np.array([L], np.int32), w.scale, tile, St,
                              w.u[b:b + 1, :, :T].copy() if w.u.shape[2] != T else w.u[b:b + 1],
-                             rows=[h], want_cdf=True)
+                             rows=[h], want_cdf=True,
+                             k_scale=w.k_scale[b:b + 1] if fp8 else None,
+                             v_scale=w.v_scale[b:b + 1] if fp8 else None)
         o_idx = res.idx[0].reshape(-1, St)[:T]
         C = res.cdf[0]
         wt = res.w[0][:T]
@@ -193,31 +177,14 @@ def check_flash(w, out: np.ndarray, idx: np.ndarray, rows: Optional[Sequence[int
                 j = int(gt[i]) - t0
                 x = (i + float(w.u[b, h, t])) / St
                 lo = C[t0 + j - 1] if j > 0 else 0.0
-                ok = (lo - BAND <= x < C[t0 + j] + BAND) or (j == n - 1 and x >= C[t0 + j] - BAND)
+                ok = lo - BAND <= x < C[t0 + j] + BAND
                 assert ok, f"row {r} tile {t} draw {i}: GPU {gt[i]}, oracle {o_idx[t][i]}, x={x!r}"
                 band += 1
         ref = np.zeros(w.d)
-        vk = vb[:, h // w.G, :]
+        vk = value_rows(w, b, h // w.G)
         for t in range(T):
             ref += wt[t] * O.gather_mean(np.ascontiguousarray(vk), g[t])
         e = float(np.abs(out[r] - ref).max())
         worst = max(worst, e)
         assert e <= SAMPLED_MAX_ABS, f"row {r}: flash max abs error {e:.3e}"
     return {"band_accepted": band, "max_abs": worst, "rows": len(rows)}
-
-
-def current_rows(dw: DeviceWorkload, w):
-    """Views of the cache rows at position ctx_len[b] - 1 (the current token),
-    per batch: (K [Hkv, d], V [Hkv, d])."""
-    out = []
-    for b in range(w.B):
-        L = int(w.ctx_len[b])
-        if w.paged:
-            page = int(w.block_table[b, (L - 1) // w.page_size])
-            s = (L - 1) % w.page_size
-            out.append((dw.kp[page, :, s, :], dw.vp[page, :, s, :]))
-        elif dw.layout == "hnd":
-            out.append((dw.k[b, :, L - 1], dw.v[b, :, L - 1]))
-        else:
-            out.append((dw.k[b, L - 1], dw.v[b, L - 1]))
-    return out

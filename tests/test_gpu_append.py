@@ -9,6 +9,7 @@ import numpy as np
 import pytest
 import torch
 
+from paper_2605_01910_amd import santa as S
 from tests.gpu_util import (KIND_CODE, DeviceWorkload, check_dense, check_flash, check_sampled,
                             current_rows, log, run)
 from workload import make_workload
@@ -16,24 +17,21 @@ from workload import make_workload
 pytestmark = pytest.mark.gpu
 
 CASES = {
-    "sys_one_launch": (2, "systematic", dict(B=2, n=3000, S=128, ctx_len=[3000, 1777]), "fused"),
-    "strat_two_launch": (2, "stratified", dict(B=3, n=2500, S=64, ctx_len=[2500, 1, 999]), "split"),
-    "iid_one_launch": (2, "iid", dict(B=2, n=2000, S=96, ctx_len=[2000, 640]), "fused"),
-    "sys_paged": (4, "systematic", dict(B=3, len_lo=700, len_hi=3000), "fused"),
-    "sys_paged_two_launch": (4, "systematic", dict(B=3, len_lo=700, len_hi=3000), "split"),
-    "strat_work_queue": (2, "stratified", dict(B=4, n=2200, S=64, ctx_len=[2200, 3, 1500, 64]), "queue"),
-    "dense": (2, "dense", dict(B=2, n=3000, ctx_len=[3000, 1234]), "fused"),
-    "dense_paged": (4, "dense", dict(B=3, len_lo=900, len_hi=2600), "fused"),
-    "flash": (2, "flash", dict(B=2, n=3000, ctx_len=[3000, 1500]), "fused"),
-    "sys_f32_no_ctx": (1, "systematic", {}, "fused"),
+    "sys_one_launch": (2, "systematic", dict(B=2, n=3000, S=128, ctx_len=[3000, 1777]), "one"),
+    "strat_two_launch": (2, "stratified", dict(B=3, n=2500, S=64, ctx_len=[2500, 1, 999]), "two"),
+    "iid_one_launch": (2, "iid", dict(B=2, n=2000, S=96, ctx_len=[2000, 640]), "one"),
+    "sys_paged": (4, "systematic", dict(B=3, len_lo=700, len_hi=3000), "one"),
+    "sys_paged_two_launch": (4, "systematic", dict(B=3, len_lo=700, len_hi=3000), "two"),
+    "dense": (2, "dense", dict(B=2, n=3000, ctx_len=[3000, 1234]), "one"),
+    "dense_paged": (4, "dense", dict(B=3, len_lo=900, len_hi=2600), "one"),
+    "flash": (2, "flash", dict(B=2, n=3000, ctx_len=[3000, 1500]), "one"),
+    "sys_f32_no_ctx": (1, "systematic", {}, "one"),
 }
 
 
 @pytest.mark.parametrize("case", sorted(CASES))
-def test_fused_append(case, monkeypatch):
+def test_fused_append(case):
     cfg, kind, over, path = CASES[case]
-    monkeypatch.setenv("SANTA_SAMPLED", "split" if path == "queue" else path)
-    monkeypatch.setenv("SANTA_QUEUE", "1" if path == "queue" else "0")
     gen_kind = "systematic" if kind == "dense" else kind
     w = make_workload(cfg, seed=81, kind=gen_kind, **over)
     log(f"[append/{kind}/{path}] {case} cfg={cfg} {over}")
@@ -49,7 +47,8 @@ def test_fused_append(case, monkeypatch):
         k.copy_(4.0 * torch.sign(qg[b]))
         v.fill_(-2.0)
     dw.kv.k_new, dw.kv.v_new = k_new.data_ptr(), v_new.data_ptr()
-    out, idx, _ = run(w, kind, dw=dw)
+    with S.options(path if kind not in ("dense", "flash") else "auto"):
+        out, idx, _ = run(w, kind, dw=dw)
     torch.cuda.synchronize()
     for b, (k, v) in enumerate(rows):
         assert torch.equal(k, k_new[b]) and torch.equal(v, v_new[b]), f"cache row of batch {b}"
@@ -61,21 +60,19 @@ def test_fused_append(case, monkeypatch):
         log(f"  {check_sampled(w, out, idx, kind)}")
 
 
-def test_append_rejected_where_unsupported(monkeypatch):
+def test_append_rejected_where_unsupported():
     """The multi-kernel path refuses the append, and k_new without v_new is
     an invalid argument; neither launches anything."""
-    from paper_2605_01910_amd import santa as S
     w = make_workload(2, B=1, n=700, kind="systematic", S=32, seed=82)
     dw = DeviceWorkload(w)
     z = torch.zeros(w.B, w.Hkv, 128, dtype=dw.k.dtype, device="cuda")
     dw.kv.k_new, dw.kv.v_new = z.data_ptr(), z.data_ptr()
-    monkeypatch.setenv("SANTA_VARIANT", "multi")
-    ws = S.alloc_workspace(dw.shape, dw.kv, w.S, KIND_CODE["systematic"])
     out = torch.empty_like(dw.q)
-    with pytest.raises(S.SantaError) as e:
-        S.santa_decode_systematic(dw.q, dw.kv, dw.shape, w.scale, w.S, dw.u, None, out, ws)
+    with S.options("multi"):
+        ws = S.alloc_workspace(dw.shape, dw.kv, w.S, KIND_CODE["systematic"])
+        with pytest.raises(S.SantaError) as e:
+            S.santa_decode_systematic(dw.q, dw.kv, dw.shape, w.scale, w.S, dw.u, None, out, ws)
     assert e.value.status == S.SANTA_ERR_UNSUPPORTED
-    monkeypatch.setenv("SANTA_VARIANT", "fused")
     dw.kv.v_new = None
     with pytest.raises(S.SantaError) as e:
         S.santa_decode_systematic(dw.q, dw.kv, dw.shape, w.scale, w.S, dw.u, None, out, ws)

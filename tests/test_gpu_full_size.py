@@ -1,10 +1,8 @@
 """GPU parity at the full benchmark shapes, in the launch configuration the
 benchmark times (default split counts and path choice, seed 0 as in bench.py).
 
-Configurations 2, 3 and 5 are checked on every row: the oracle finishes a
-full 32k-context step in milliseconds.  Configuration 4 (paged, 64 sequences
-of up to 64k keys) is checked on a sample of rows that includes the shortest
-and the longest sequence and rows of every KV head."""
+Every configuration is checked on every row, configuration 4 (paged, 64
+sequences of 4k..64k keys) included."""
 
 import numpy as np
 import pytest
@@ -24,7 +22,8 @@ def test_cfg2_full_every_row():
     log(f"  dense {check_dense(w, d)}")
 
 
-@pytest.mark.parametrize("kind,S", [("systematic", 128), ("systematic", 2048)])
+@pytest.mark.parametrize("kind,S", [("systematic", 128), ("systematic", 512), ("systematic", 1024),
+                                    ("stratified", 1024), ("systematic", 2048)])
 def test_cfg2_shape_paper_budgets_every_row(kind, S):
     """The batch-1 32k shape at the paper's two operating budgets."""
     w = make_workload(2, seed=0, kind=kind, S=S)
@@ -45,18 +44,15 @@ def test_cfg3_full_every_row(S):
         log(f"  dense {check_dense(w, d)}")
 
 
-@pytest.mark.timeout(600)
-def test_cfg4_paged_full_sampled_rows():
+@pytest.mark.timeout(900)
+def test_cfg4_paged_full_every_row():
     w = make_workload(4, seed=0)
-    order = np.argsort(w.ctx_len)
-    bs = sorted({int(order[0]), int(order[-1]), int(order[len(order) // 2]), 5, 37})
-    rows = [b * w.Hq + h for b in bs for h in range(0, w.Hq, 3)]
     log(f"[full cfg4] B={w.B} n_max={w.n_max} ctx {w.ctx_len.min()}..{w.ctx_len.max()} "
-        f"rows={len(rows)} of {w.B * w.Hq}")
+        f"rows={w.B * w.Hq}")
     out, idx, _ = run(w)
-    log(f"  sampled {check_sampled(w, out, idx, rows=rows)}")
+    log(f"  sampled {check_sampled(w, out, idx)}")
     d, _, _ = run(w, "dense")
-    log(f"  dense {check_dense(w, d, rows=rows)}")
+    log(f"  dense {check_dense(w, d)}")
 
 
 @pytest.mark.timeout(300)

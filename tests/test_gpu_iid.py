@@ -8,6 +8,7 @@ the paged cache, and the full Llama-3.1-8B 32k shape."""
 import numpy as np
 import pytest
 
+from paper_2605_01910_amd import santa as S
 from tests.gpu_util import DeviceWorkload, check_sampled, log, run
 from workload import make_workload
 
@@ -23,14 +24,14 @@ CASES = {
 }
 
 
-@pytest.mark.parametrize("path", ["fused", "split"])
+@pytest.mark.parametrize("path", ["one", "two"])
 @pytest.mark.parametrize("case", sorted(CASES))
-def test_iid_parity(case, path, monkeypatch):
-    monkeypatch.setenv("SANTA_SAMPLED", path)
+def test_iid_parity(case, path):
     cfg, over = CASES[case]
     log(f"[iid/{path}] {case} cfg={cfg} {over}")
     w = make_workload(cfg, seed=71, kind="iid", **over)
-    out, idx, _ = run(w, "iid")
+    with S.options(path):
+        out, idx, _ = run(w, "iid")
     log(f"  {check_sampled(w, out, idx, 'iid')}")
 
 

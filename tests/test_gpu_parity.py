@@ -8,6 +8,7 @@ import numpy as np
 import pytest
 import torch
 
+from paper_2605_01910_amd import santa as S
 from tests.gpu_util import (KIND_CODE, DeviceWorkload, check_dense, check_sampled, log, run)
 from workload import make_workload
 
@@ -140,13 +141,13 @@ MULTI_CASES = {
 
 
 @pytest.mark.parametrize("case", sorted(MULTI_CASES))
-def test_multi_kernel_variant_parity(case, monkeypatch):
+def test_multi_kernel_variant_parity(case):
     """The multi-kernel path (score/CDF stash, offsets, sample, merge launches)."""
-    monkeypatch.setenv("SANTA_VARIANT", "multi")
     cfg, kind, over = MULTI_CASES[case]
     log(f"[multi/{kind}] {case} cfg={cfg} {over}")
     w = make_workload(cfg, seed=51, kind=kind if kind != "dense" else "systematic", **over)
-    out, idx, _ = run(w, kind)
+    with S.options("multi"):
+        out, idx, _ = run(w, kind)
     if kind == "dense":
         check_dense(w, out)
     else:
@@ -154,165 +155,119 @@ def test_multi_kernel_variant_parity(case, monkeypatch):
 
 
 @pytest.mark.parametrize("splits", [16, 64, 200])
-def test_fused_split_counts(splits, monkeypatch):
+def test_fused_split_counts(splits):
     """Fused path at other split counts."""
-    monkeypatch.setenv("SANTA_SPLITS", str(splits))
     w = make_workload(2, B=3, n=5000, kind="stratified", S=128, ctx_len=[5000, 2222, 17], seed=52)
     log(f"[fused splits={splits}]")
-    out, idx, _ = run(w)
-    check_sampled(w, out, idx)
-    d, _, _ = run(w, "dense")
-    check_dense(w, d)
+    with S.options("auto", splits):
+        out, idx, _ = run(w)
+        check_sampled(w, out, idx)
+        d, _, _ = run(w, "dense")
+        check_dense(w, d)
 
 
 def test_fused_barrier_flag_stays_clear():
     """The fused path's bounded barrier wait never gives up on these inputs."""
-    from paper_2605_01910_amd import santa as S
     w = make_workload(2, B=16, n=1024, kind="systematic", S=64, seed=53)
     dw = DeviceWorkload(w)
     ws = S.alloc_workspace(dw.shape, dw.kv, w.S, S.SANTA_KIND_SYSTEMATIC)
     for _ in range(3):
         out, idx, _ = run(w, dw=dw, ws=ws)
     check_sampled(w, out, idx)
-    assert int(ws[:4].view(torch.int32).item()) == 0
+    assert S.workspace_error(ws) == 0
 
 
-@pytest.mark.parametrize("queue", [1, 0])
 @pytest.mark.parametrize("case", sorted(SAMPLED_CASES))
-def test_two_launch_sampled_parity(case, queue, monkeypatch):
+def test_two_launch_sampled_parity(case):
     """The large-batch sampled path (key stream with CDF stash, then one
-    workgroup per query head) on every sampled case, in both forms: two
-    launches (queue=0, the default) and one launch with per-XCD work queues."""
-    monkeypatch.setenv("SANTA_SAMPLED", "split")
-    monkeypatch.setenv("SANTA_QUEUE", str(queue))
+    workgroup per query head) forced on every sampled case."""
     cfg, kind, over = SAMPLED_CASES[case]
-    log(f"[two-launch/{kind} queue={queue}] {case} cfg={cfg} {over}")
+    log(f"[two-launch/{kind}] {case} cfg={cfg} {over}")
     w = make_workload(cfg, seed=23, kind=kind, **over)
-    out, idx, _ = run(w, kind)
+    with S.options("two"):
+        out, idx, _ = run(w, kind)
     log(f"  {check_sampled(w, out, idx, kind)}")
 
 
 @pytest.mark.parametrize("case", sorted(SAMPLED_CASES))
-def test_one_launch_sampled_parity(case, monkeypatch):
+def test_one_launch_sampled_parity(case):
     """The small-batch sampled path forced on every sampled case."""
-    monkeypatch.setenv("SANTA_SAMPLED", "fused")
     cfg, kind, over = SAMPLED_CASES[case]
     log(f"[one-launch/{kind}] {case} cfg={cfg} {over}")
     w = make_workload(cfg, seed=24, kind=kind, **over)
-    out, idx, _ = run(w, kind)
+    with S.options("one"):
+        out, idx, _ = run(w, kind)
     log(f"  {check_sampled(w, out, idx, kind)}")
 
 
-def test_one_launch_many_rounds(monkeypatch):
+def test_one_launch_many_rounds():
     """One launch over far more rows than one resident round holds: every
     workgroup handles a split of several rows, rows have ragged lengths (one
     empty), and three calls in a row reuse the row counters."""
-    from paper_2605_01910_amd import santa as S
-    monkeypatch.setenv("SANTA_SAMPLED", "fused")
     lens = [(37 * i * i + 11 * i) % 9000 for i in range(24)]
     lens[3] = 0
     lens[7] = 9000
     w = make_workload(3, B=24, n=9000, kind="systematic", S=64, ctx_len=lens, seed=54)
     dw = DeviceWorkload(w)
-    ws = max((S.alloc_workspace(dw.shape, dw.kv, w.S, k)
-              for k in (S.SANTA_KIND_SYSTEMATIC, S.SANTA_KIND_DENSE)), key=lambda x: x.numel())
-    log(f"[rounds] B={w.B} n={w.n_max} rows={w.B * w.Hkv}")
-    for _ in range(3):
-        out, idx, _ = run(w, dw=dw, ws=ws)
-        check_sampled(w, out, idx)
-        d, _, _ = run(w, "dense", dw=dw, ws=ws)
-        check_dense(w, d)
-    assert int(ws[:4].view(torch.int32).item()) == 0
+    with S.options("one"):
+        ws = max((S.alloc_workspace(dw.shape, dw.kv, w.S, k)
+                  for k in (S.SANTA_KIND_SYSTEMATIC, S.SANTA_KIND_DENSE)), key=lambda x: x.numel())
+        log(f"[rounds] B={w.B} n={w.n_max} rows={w.B * w.Hkv}")
+        for _ in range(3):
+            out, idx, _ = run(w, dw=dw, ws=ws)
+            check_sampled(w, out, idx)
+            d, _, _ = run(w, "dense", dw=dw, ws=ws)
+            check_dense(w, d)
+    assert S.workspace_error(ws) == 0
 
 
-def test_workspace_shared_by_both_sampled_paths(monkeypatch):
+def test_workspace_shared_by_both_sampled_paths():
     """The counters keep their place in every fused layout: one workspace
     serves the one-launch path, the two-launch path and the dense step in any
     order."""
-    from paper_2605_01910_amd import santa as S
     w = make_workload(2, B=4, n=3000, kind="stratified", S=128, seed=55)
     dw = DeviceWorkload(w)
     spaces = [S.alloc_workspace(dw.shape, dw.kv, 1, S.SANTA_KIND_DENSE)]
-    for path in ("fused", "split"):
-        monkeypatch.setenv("SANTA_SAMPLED", path)
-        spaces.append(S.alloc_workspace(dw.shape, dw.kv, w.S, S.SANTA_KIND_STRATIFIED))
+    for path in ("one", "two"):
+        with S.options(path):
+            spaces.append(S.alloc_workspace(dw.shape, dw.kv, w.S, S.SANTA_KIND_STRATIFIED))
     ws = max(spaces, key=lambda x: x.numel())
-    log("[workspace] fused, split, dense, fused")
-    for path in ("fused", "split", "dense", "fused"):
+    log("[workspace] one, two, dense, one")
+    for path in ("one", "two", "dense", "one"):
         if path == "dense":
             d, _, _ = run(w, "dense", dw=dw, ws=ws)
             check_dense(w, d)
             continue
-        monkeypatch.setenv("SANTA_SAMPLED", path)
-        out, idx, _ = run(w, dw=dw, ws=ws)
+        with S.options(path):
+            out, idx, _ = run(w, dw=dw, ws=ws)
         check_sampled(w, out, idx)
 
 
-def test_stream_value_queue_matches_two_launches(monkeypatch):
-    """The one-launch work-queue form of the large-batch path gives bitwise the
-    two-launch result on the same inputs, leaves its per-XCD tickets and its
-    per-row counters at zero after every call (calls of other shapes follow on
-    the same workspace) and never sets the wait flag."""
-    from paper_2605_01910_amd import santa as S
-    monkeypatch.setenv("SANTA_SAMPLED", "split")
-    cases = [(3, "systematic", dict(B=16, n=3000, S=256)),           # 128 KV rows
-             (2, "stratified", dict(B=3, n=1100, S=64, ctx_len=[1100, 5, 700])),  # 24 rows
-             (2, "systematic", dict(B=9, Hq=16, Hkv=2, n=2048, S=128)),           # 18 rows, G = 8
-             (2, "iid", dict(B=5, n=1500, S=96, ctx_len=[1500, 1, 0, 999, 64]))]
-    works = [make_workload(c, seed=61 + i, kind=k, **o) for i, (c, k, o) in enumerate(cases)]
-    dws = [DeviceWorkload(w) for w in works]
-    ws = max((S.alloc_workspace(d.shape, d.kv, w.S, KIND_CODE[w.kind]) for w, d in zip(works, dws)),
-             key=lambda x: x.numel())
-    off_sync = 256  # the error flag and the ticket counters take the first 256 bytes
-    # shapes grow and shrink in turn: 128, 24, 18, 40 KV rows (the counter
-    # area has one size in every layout, so no call sees another's data there)
-    for rep in range(2):
-        for w, d in zip(works, dws):
-            rows = w.B * w.Hkv
-            log(f"[queue rep={rep}] {w.kind} B={w.B} Hq={w.Hq} Hkv={w.Hkv} n={w.n_max} S={w.S}")
-            monkeypatch.setenv("SANTA_QUEUE", "1")
-            out1, idx1, _ = run(w, dw=d, ws=ws)
-            torch.cuda.synchronize()
-            assert int(ws[:4].view(torch.int32).item()) == 0
-            assert int(ws[64:96].view(torch.int32).abs().sum().item()) == 0
-            cnt = ws[off_sync:off_sync + rows * 256].view(torch.int64).view(rows, 32)[:, 4:6]
-            assert int(cnt.abs().sum().item()) == 0
-            check_sampled(w, out1, idx1)
-            monkeypatch.setenv("SANTA_QUEUE", "0")
-            out0, idx0, _ = run(w, dw=d, ws=ws)
-            assert np.array_equal(idx0, idx1)
-            assert np.array_equal(out0, out1)
-
-
-def test_workspace_shared_by_every_kind(monkeypatch):
+def test_workspace_shared_by_every_kind():
     """Every layout keeps the error flag and the counter area at the front, so
     one workspace serves Bernoulli, multi-kernel, one-launch, two-launch and
     dense calls interleaved in any order."""
-    from paper_2605_01910_amd import santa as S
     ws_ = make_workload(2, B=2, n=3000, kind="systematic", S=128, seed=71)
     wb = make_workload(5, B=2, n=1500, mode=1, B_draws=1, seed=72)
     ds, db = DeviceWorkload(ws_), DeviceWorkload(wb)
     spaces = [S.alloc_workspace(db.shape, db.kv, wb.S, S.SANTA_KIND_BERNOULLI),
               S.alloc_workspace(ds.shape, ds.kv, 1, S.SANTA_KIND_DENSE)]
-    for var, path in (("fused", "fused"), ("fused", "split"), ("multi", "fused")):
-        monkeypatch.setenv("SANTA_VARIANT", var)
-        monkeypatch.setenv("SANTA_SAMPLED", path)
-        spaces.append(S.alloc_workspace(ds.shape, ds.kv, ws_.S, S.SANTA_KIND_SYSTEMATIC))
+    for path in ("one", "two", "multi"):
+        with S.options(path):
+            spaces.append(S.alloc_workspace(ds.shape, ds.kv, ws_.S, S.SANTA_KIND_SYSTEMATIC))
     ws = max(spaces, key=lambda x: x.numel())
-    order = ["fused", "bernoulli", "fused", "multi", "fused", "split", "bernoulli", "split",
-             "dense", "multi", "fused"]
+    order = ["one", "bernoulli", "one", "multi", "one", "two", "bernoulli", "two",
+             "dense", "multi", "one"]
     log(f"[workspace] {' '.join(order)}")
     for step in order:
-        monkeypatch.setenv("SANTA_VARIANT", "multi" if step == "multi" else "fused")
-        monkeypatch.setenv("SANTA_SAMPLED", "split" if step == "split" else "fused")
-        if step == "bernoulli":
-            out, idx, _ = run(wb, "bernoulli", dw=db, ws=ws)
-            check_sampled(wb, out, idx, "bernoulli")
-        elif step == "dense":
-            d, _, _ = run(ws_, "dense", dw=ds, ws=ws)
-            check_dense(ws_, d)
-        else:
-            out, idx, _ = run(ws_, dw=ds, ws=ws)
-            check_sampled(ws_, out, idx)
-        torch.cuda.synchronize()
-        assert int(ws[:4].view(torch.int32).item()) == 0, step
+        with S.options(step if step in ("one", "two", "multi") else "auto"):
+            if step == "bernoulli":
+                out, idx, _ = run(wb, "bernoulli", dw=db, ws=ws)
+                check_sampled(wb, out, idx, "bernoulli")
+            elif step == "dense":
+                d, _, _ = run(ws_, "dense", dw=ds, ws=ws)
+                check_dense(ws_, d)
+            else:
+                out, idx, _ = run(ws_, dw=ds, ws=ws)
+                check_sampled(ws_, out, idx)
+        assert S.workspace_error(ws) == 0, step

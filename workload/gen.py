@@ -10,7 +10,10 @@ function of ``(cfg, seed, overrides)``:
     stream 3  planted key positions           stream 7  Bernoulli-query uniforms
 
 Gaussians are drawn in float32, planted in float32 and then rounded to
-bfloat16 (round to nearest even).  Uniforms are ``rng.random(dtype=float32)``,
+bfloat16 (round to nearest even).  An FP8 cache (``kv_dtype="fp8"``) instead
+holds OCP FP8 E4M3 codes of the keys and values divided by a per-(batch, KV
+head) scale, max |x| / 448 over that slab, rounded to nearest even (torch's
+float8_e4m3fn cast); queries stay bfloat16.  Uniforms are ``rng.random(dtype=float32)``,
 which lies on the 2^-24 grid of [0, 1).
 
 The paper's decode microbenchmark feeds i.i.d. Gaussian q/K/V (Appendix
@@ -124,6 +127,11 @@ class Workload:
     B_draws: int = 0
     mode: int = 0
     heavy_pos: Optional[np.ndarray] = None    # [B, Hkv, heavy] planted positions
+    # FP8 E4M3 cache: k, v (or the pools) hold uint8 codes; element value =
+    # scale[b, kv head] * e4m3(code)
+    kv_dtype: str = ""
+    k_scale: Optional[np.ndarray] = None      # float32 [B, Hkv]
+    v_scale: Optional[np.ndarray] = None
 
     @property
     def G(self) -> int:
@@ -146,6 +154,22 @@ class Workload:
 
 def _cast(x32: np.ndarray, dtype: str) -> np.ndarray:
     return f32_to_bf16_bits(x32) if dtype == "bf16" else np.ascontiguousarray(x32, dtype=np.float32)
+
+
+FP8_E4M3_MAX = 448.0
+
+
+def _quant_fp8(x32: np.ndarray):
+    """Per-KV-head FP8 E4M3 quantisation of one sequence's keys or values
+    [L, Hkv, d]: scale = max |x| / 448 over the head's slab (1 if it is all
+    zero), codes = the E4M3 rounding of x / scale.  Returns (codes uint8,
+    scales float32 [Hkv])."""
+    import torch
+    amax = np.abs(x32).max(axis=(0, 2)) if x32.shape[0] else np.zeros(x32.shape[1], np.float32)
+    sc = np.where(amax > 0, amax / np.float32(FP8_E4M3_MAX), np.float32(1.0)).astype(np.float32)
+    y = np.ascontiguousarray(x32 / sc[None, :, None], dtype=np.float32)
+    codes = torch.from_numpy(y).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    return codes, sc
 
 
 def _plant(keys32: np.ndarray, qf: np.ndarray, G: int, scale: float, sink: float,
@@ -171,8 +195,8 @@ def _plant(keys32: np.ndarray, qf: np.ndarray, G: int, scale: float, sink: float
 def make_workload(cfg: int, seed: int = 0, **over) -> Workload:
     """Build configuration ``cfg`` (1..5), optionally with overrides of its
     parameters (``B, Hq, Hkv, n, S, kind, dtype, sink, heavy, len_lo, len_hi,
-    B_draws, mode, paged, page_size, ctx_len``, and ``tile, S_tile`` for
-    kind="flash") for smaller test cases."""
+    B_draws, mode, paged, page_size, ctx_len, kv_dtype``, and ``tile, S_tile``
+    for kind="flash") for smaller test cases."""
     p = dict(CONFIGS[cfg])
     p.update(over)
     B, Hq, Hkv, d, n = p["B"], p["Hq"], p["Hkv"], p["d"], p["n"]
@@ -182,6 +206,9 @@ def make_workload(cfg: int, seed: int = 0, **over) -> Workload:
     G = Hq // Hkv
     scale = float(p.get("scale", 1.0 / math.sqrt(d)))
     paged = bool(p.get("paged", False))
+    kv_fp8 = p.get("kv_dtype", "") == "fp8"
+    if kv_fp8 and (dtype != "bf16" or kind == "bernoulli"):
+        raise ValueError("an FP8 cache goes with bfloat16 queries and no Bernoulli scores")
 
     # query
     qf = _rng(cfg, STREAM_Q, seed).standard_normal((B, Hq, d), dtype=np.float32)
@@ -212,20 +239,30 @@ def make_workload(cfg: int, seed: int = 0, **over) -> Workload:
                 pos = np.sort(r.choice(np.arange(1, max(L, 2)), size=m, replace=False)) if m else []
                 heavy_pos[b, kv, :m] = pos
 
-    edt = np.uint16 if dtype == "bf16" else np.float32
+    edt = np.uint8 if kv_fp8 else np.uint16 if dtype == "bf16" else np.float32
     k_seq, v_seq = [], []
+    k_sc = np.ones((B, Hkv), np.float32)
+    v_sc = np.ones((B, Hkv), np.float32)
     for b in range(B):
         L = int(ctx[b])
         kb = _rng(cfg, STREAM_K, seed, b).standard_normal((L, Hkv, d), dtype=np.float32)
         _plant(kb, qf[b], G, scale, float(p.get("sink", 0.0)), heavy_pos[b] if nh else None,
                float(p.get("heavy_boost", 0.0)))
         vb = _rng(cfg, STREAM_V, seed, b).standard_normal((L, Hkv, d), dtype=np.float32)
-        k_seq.append(_cast(kb, dtype))
-        v_seq.append(_cast(vb, dtype))
+        if kv_fp8:
+            kc, k_sc[b] = _quant_fp8(kb)
+            vc, v_sc[b] = _quant_fp8(vb)
+            k_seq.append(kc)
+            v_seq.append(vc)
+        else:
+            k_seq.append(_cast(kb, dtype))
+            v_seq.append(_cast(vb, dtype))
         del kb, vb
 
     w = Workload(cfg=cfg, seed=seed, B=B, Hq=Hq, Hkv=Hkv, d=d, n_max=n_max, dtype=dtype,
                  kind=kind, S=S, scale=scale, q=q, ctx_len=ctx, u=None, heavy_pos=heavy_pos)
+    if kv_fp8:
+        w.kv_dtype, w.k_scale, w.v_scale = "fp8", k_sc, v_sc
 
     if paged:
         ps = int(p["page_size"])
