@@ -192,7 +192,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(PERSIS
     const QRegs<E, G> qr = load_q<E, G>(static_cast<const QE<E> *>(a.q), b, a.Hq, kvh, c);
     const float2 sc = kv_scales<E>(a.kv, b, kvh, a.Hkv);  // FP8 cache: K and V scales
     float mx[G];
-    constexpr int U = PERSIST ? score_unroll<E, G>() : (sizeof(E) == 1 ? 8 : 4);
+    constexpr int U = PERSIST ? score_unroll<E, G>() : (sizeof(E) == 1 && G <= 4 ? 8 : 4);
     score_tile<E, G, PAGED, U>(a.kv, b, kvh, start, nrows, qr, a.scale_log2 * sc.x, s, pitch, mx);
     block_max_heads<G>(mx, mtmp, mh);
     if constexpr (FLASH) {

@@ -61,7 +61,8 @@ __device__ __forceinline__ void write_split_stash(const FusedArgs &a, const floa
 // stream's loads in flight (64 VGPRs for bf16 rows with G <= 4).
 template <typename E, int G, bool PAGED>
 constexpr int stream_waves() {
-  return sizeof(E) <= 2 && G <= 4 && !PAGED ? 8 : (G <= 4 ? 4 : 2);
+  if constexpr (sizeof(E) == 1) return G <= 4 ? 5 : 2;  // 8 FP8 rows per lane and batch
+  return sizeof(E) == 2 && G <= 4 && !PAGED ? 8 : (G <= 4 ? 4 : 2);
 }
 
 // Split t of KV row rowkv (= b * Hkv + kvh): scores, CDF, then the stash, the

@@ -59,10 +59,11 @@ __device__ __forceinline__ void store_out(float *p, float x) { *p = x; }
 // Key rows per lane and batch of the score tile (U loads per lane in flight,
 // twice that while a batch is scored): 8 for bf16 with G <= 4, 4 for the
 // wider register sets of fp32 rows or G = 8; FP8 rows take half the bytes and
-// registers per load, so twice as many.
+// registers per load, so twice as many for G <= 4 (G = 8 keeps 4: its query
+// registers and the bf16 conversions leave no room for more).
 template <typename E, int G>
 constexpr int score_unroll() {
-  return sizeof(E) == 1 ? (G <= 4 ? 16 : 8) : (sizeof(E) == 2 && G <= 4) ? 8 : 4;
+  return sizeof(E) == 1 ? (G <= 4 ? 16 : 4) : (sizeof(E) == 2 && G <= 4) ? 8 : 4;
 }
 
 // Block-table entries of the pages one split covers, one per lane: lane l of
