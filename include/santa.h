@@ -204,6 +204,29 @@ santa_status_t santa_decode_iid(const void *q, const santa_kv_t *kv, const santa
                                 float scale, int32_t S, const float *u, int32_t *idx_out,
                                 void *out, void *ws, size_t ws_bytes, void *stream);
 
+/* No-allocation form of santa_decode_stratified, for callers that cannot
+ * allocate device memory at call time: code under HIP graph capture, serving
+ * loops and harnesses that forbid it.  Same arguments, computation and
+ * outputs as santa_decode_stratified, without the workspace: the call uses a
+ * scratch array of SANTA_STATIC_SCRATCH_BYTES (64 MiB) in the library's own
+ * device memory, one per GPU, placed when the library's code is loaded on that
+ * GPU and held until the process ends.  The first call on a device looks up
+ * the array's address there.  Every call first clears the part of the array
+ * that must start at zero (a fill kernel on `stream`), so it does not depend
+ * on what earlier calls left; calls on one GPU share the array, so calls that
+ * overlap in time on one GPU (on different streams, or from different
+ * threads without ordering) race and give invalid outputs.  `stream` must
+ * belong to the calling thread's current device.  Errors: as
+ * santa_decode_stratified; SANTA_ERR_WORKSPACE when the call needs more than
+ * SANTA_STATIC_SCRATCH_BYTES of workspace (santa_workspace_size with
+ * SANTA_KIND_STRATIFIED gives the need); SANTA_ERR_UNSUPPORTED under
+ * SANTA_PATH_MULTI.  It never calls hipMalloc or hipFree. */
+#define SANTA_STATIC_SCRATCH_BYTES (64u << 20)
+santa_status_t santa_decode_stratified_noalloc(const void *q, const santa_kv_t *kv,
+                                               const santa_shape_t *shape, float scale, int32_t S,
+                                               const float *u, int32_t *idx_out, void *out,
+                                               void *stream);
+
 /* Bernoulli qK^T score sampling (Sec. 5, Eq. "qk_estimator"; App. C) followed
  * by the systematic value stage.
  *   mode 0, per-head ternary query: norm = max_i |q_i|, pi_i = |q_i|/norm,

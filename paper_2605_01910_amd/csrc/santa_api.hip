@@ -6,6 +6,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdlib>
+#include <mutex>
 #include <string>
 
 #include "santa.h"
@@ -288,6 +289,37 @@ santa_status_t sampled(const void *q, const santa_kv_t *kv, const santa_shape_t 
                                           static_cast<hipStream_t>(stream)));
 }
 
+// Scratch of the no-allocation entry point: the workspace of its calls, one
+// array per GPU in the library's own device memory (a code-object global, so
+// the loader places it and nothing is allocated at call time).  In host code
+// `scratch` names a host-side stand-in, never a device address: its device
+// address on each GPU comes from hipGetSymbolAddress, taken once per device
+// with that device current, and only that address is passed to kernels.
+static __device__ __align__(256) unsigned char scratch[SANTA_STATIC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];  // device address of `scratch` on each GPU (null: not yet)
+
+// The calling thread's current device, which must also own `stream`, and the
+// device address of its scratch array (set up on the device's first call).
+santa_status_t scratch_for(hipStream_t stream, void **ptr) {
+  int dev = -1, sdev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+    return fail(SANTA_ERR_HIP, "no usable current device");
+  if (stream && (hipStreamGetDevice(stream, &sdev) != hipSuccess || sdev != dev))
+    return fail(SANTA_ERR_INVALID_ARG, "stream must belong to the current device");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) return fail(SANTA_ERR_HIP, "hipGetSymbolAddress(scratch) failed");
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return SANTA_OK;
+}
+
 }  // namespace
 
 santa::CallTimer &santa::call_timer() { return g_timer; }
@@ -343,6 +375,35 @@ santa_status_t santa_decode_stratified(const void *q, const santa_kv_t *kv,
                                        const float *u, int32_t *idx_out, void *out, void *ws,
                                        size_t ws_bytes, void *stream) {
   return sampled(q, kv, shape, scale, S, u, idx_out, out, ws, ws_bytes, stream, true);
+}
+
+santa_status_t santa_decode_stratified_noalloc(const void *q, const santa_kv_t *kv,
+                                               const santa_shape_t *shape, float scale, int32_t S,
+                                               const float *u, int32_t *idx_out, void *out,
+                                               void *stream) {
+  TimerScope timer_scope;
+  santa_status_t s = common_checks(q, kv, shape, scale, out, true);
+  if (s != SANTA_OK) return s;
+  if (S < 1 || S > (1 << 24)) return fail(SANTA_ERR_INVALID_ARG, "S must be in [1, 2^24]");
+  if (!u) return fail(SANTA_ERR_INVALID_ARG, "u is NULL");
+  const santa::Plan p = make_plan(shape, kv, S, SANTA_KIND_STRATIFIED);
+  if (p.total > SANTA_STATIC_SCRATCH_BYTES)
+    return fail(SANTA_ERR_WORKSPACE, "the call needs more workspace than the static scratch array "
+                                     "holds (SANTA_STATIC_SCRATCH_BYTES)");
+  if (!p.fused) return fail(SANTA_ERR_UNSUPPORTED, "the no-allocation call needs the fused launch layout");
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  void *ws = nullptr;
+  s = scratch_for(st, &ws);
+  if (s != SANTA_OK) return s;
+  // The array keeps the previous call's contents.  Clear what must start at
+  // zero: the wait flag and the row counters this call uses (a fill kernel,
+  // not a memset, so that the call can be captured in a graph).  Everything
+  // else the call reads it writes first.
+  const size_t head = p.off_sync + (size_t)p.B * p.Hkv * santa::kSyncStride * 4;
+  hipError_t e = santa::launch_zero(ws, head, st);
+  if (e != hipSuccess) return hip_status(e);
+  return hip_status(santa::launch_fused_sampled(p, make_view(kv), q, log2_scale(scale), 1, u,
+                                                idx_out, out, static_cast<char *>(ws), st));
 }
 
 santa_status_t santa_decode_bernoulli_qk(const void *q, const santa_kt_t *kt,

@@ -33,9 +33,10 @@ EXPORTS = ("santa_workspace_size", "santa_workspace_init", "santa_decode_dense",
            "santa_decode_systematic", "santa_decode_stratified", "santa_decode_bernoulli_qk",
            "santa_decode_iid", "santa_decode_flash", "santa_stream_read", "santa_time_next_call",
            "santa_set_options", "santa_get_options", "santa_plan_info",
-           "santa_status_string", "santa_last_error")
+           "santa_decode_stratified_noalloc", "santa_status_string", "santa_last_error")
 
 STREAM_READ_GROUPS = 4096  # SANTA_STREAM_READ_GROUPS: uint32 words of the sink
+STATIC_SCRATCH_BYTES = 64 << 20  # SANTA_STATIC_SCRATCH_BYTES
 
 
 class SantaError(RuntimeError):
@@ -97,6 +98,7 @@ def load() -> ctypes.CDLL:
     L.santa_decode_dense.argtypes = [P, KP, SP, ctypes.c_float, P, P, SZ, P]
     L.santa_decode_systematic.argtypes = [P, KP, SP, ctypes.c_float, I32, P, P, P, P, SZ, P]
     L.santa_decode_stratified.argtypes = [P, KP, SP, ctypes.c_float, I32, P, P, P, P, SZ, P]
+    L.santa_decode_stratified_noalloc.argtypes = [P, KP, SP, ctypes.c_float, I32, P, P, P, P]
     L.santa_decode_bernoulli_qk.argtypes = [P, TP, KP, SP, ctypes.c_float, I32, I32, P, I32, P,
                                             P, P, P, P, SZ, P]
     L.santa_decode_flash.argtypes = [P, KP, SP, ctypes.c_float, I32, I32, P, P, P, P, SZ, P]
@@ -113,7 +115,8 @@ def load() -> ctypes.CDLL:
     for name in ("santa_workspace_init", "santa_decode_dense", "santa_decode_systematic",
                  "santa_decode_stratified", "santa_decode_bernoulli_qk", "santa_decode_flash",
                  "santa_decode_iid", "santa_stream_read", "santa_time_next_call",
-                 "santa_set_options", "santa_get_options", "santa_plan_info"):
+                 "santa_set_options", "santa_get_options", "santa_plan_info",
+                 "santa_decode_stratified_noalloc"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -266,6 +269,15 @@ def santa_decode_stratified(q: torch.Tensor, kv: santa_kv_t, shape: santa_shape_
                                           float(scale), int(S), _ptr(u), _ptr(idx_out),
                                           _ptr(out), _ptr(ws), ws.numel() * ws.element_size(),
                                           _stream(stream)))
+
+
+def santa_decode_stratified_noalloc(q: torch.Tensor, kv: santa_kv_t, shape: santa_shape_t,
+                                    scale: float, S: int, u: torch.Tensor,
+                                    idx_out: Optional[torch.Tensor], out: torch.Tensor,
+                                    stream=None) -> None:
+    _check(load().santa_decode_stratified_noalloc(_ptr(q), ctypes.byref(kv), ctypes.byref(shape),
+                                                  float(scale), int(S), _ptr(u), _ptr(idx_out),
+                                                  _ptr(out), _stream(stream)))
 
 
 def santa_decode_bernoulli_qk(q: torch.Tensor, kt: santa_kt_t, kv: santa_kv_t,
