@@ -186,10 +186,11 @@ santa::Plan make_plan(const santa_shape_t *sh, const santa_kv_t *kv, int S, int 
     // the two-launch path (one workgroup per query head)
     p.fused = 1;
     p.split2 = 1;
-    // splits of at most 512 keys: the feature-row stream of a split is short,
-    // so more workgroups keep more of it in flight
-    p.T = std::min(santa::kMaxSplits,
-                   std::max(Tf, (int)((p.n_k + 511) / 512)));
+    // splits of at most 512 keys by default: the feature-row stream of a
+    // split is short, so more workgroups keep more of it in flight; a split
+    // count set in the options applies as given (at least n_k / 1024)
+    p.T = g_opts.splits > 0 ? Tf
+                            : std::min(santa::kMaxSplits, std::max(Tf, (int)((p.n_k + 511) / 512)));
     p.Ls = (int)(((p.n_k + p.T - 1) / p.T + 63) & ~63);
     p.npitch = ((int64_t)p.n_k + 63) & ~int64_t(63);
     p.off_stats = take(rows * p.T * 8);

@@ -11,17 +11,42 @@ namespace santa {
 // Small-batch sampled step
 // ---------------------------------------------------------------------------
 // #{j < nrows : a P_j <= x} over a non-decreasing LDS CDF P (nrows <=
-// kSplitMax): branch-free binary lifting in a rolled loop (a handful of
-// instructions; one LDS read per step).
+// kSplitMax = 1024) in three dependent steps instead of ten: the number of
+// 256-key quarters whose last value is <= x (three reads), then the 16-key
+// chunks of that quarter whose last value is <= x (16 reads issued together),
+// then the keys of that chunk (four 16-byte reads).  Entries at or past nrows
+// hold stale values and are never counted.
 __device__ __forceinline__ int lds_cdf_count(const float *Ph, int nrows, float a, float x) {
-  int pos = 0;
-#pragma unroll 1
-  for (int step = 1 << (31 - __clz(nrows)); step > 0; step >>= 1) {
-    const int np = pos + step;
-    const float v = Ph[min(np, nrows) - 1];
-    pos = (np <= nrows && a * v <= x) ? np : pos;
+  static_assert(kSplitMax == 1024, "three levels of 4 x 16 x 16 keys");
+  // every read is inside the 1024-entry row, so the reads of a level are
+  // unconditional and issued together; the tests use non-short-circuit '&'
+  float w[16];
+#pragma unroll
+  for (int k = 1; k < 4; ++k) w[k] = Ph[256 * k - 1];
+  int q = 0;
+#pragma unroll
+  for (int k = 1; k < 4; ++k) q += ((256 * k - 1 < nrows) & (a * w[k] <= x)) ? 1 : 0;
+  const float *pq = Ph + 256 * q + 15;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) w[i] = pq[16 * i];
+  int c2 = 0;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) c2 += ((256 * q + 16 * i + 15 < nrows) & (a * w[i] <= x)) ? 1 : 0;
+  if (c2 == 16) return 256 * (q + 1);  // only when the quarter is the last: q = 3
+  const int j0 = 256 * q + 16 * c2;
+  const float4 *pc = reinterpret_cast<const float4 *>(Ph + j0);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float4 t = pc[i];
+    w[4 * i] = t.x;
+    w[4 * i + 1] = t.y;
+    w[4 * i + 2] = t.z;
+    w[4 * i + 3] = t.w;
   }
-  return pos;
+  int c3 = 0;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) c3 += ((j0 + i < nrows) & (a * w[i] <= x)) ? 1 : 0;
+  return j0 + c3;
 }
 
 // Claims and inverse CDF of one split for thresholds held in LDS without a
@@ -158,6 +183,88 @@ __device__ __forceinline__ bool claim_keys(const HeadClaim *hc, const int *rng, 
   return total > 0;
 }
 
+// Claims of the group without a workgroup barrier between ranges and keys
+// (sorted thresholds with a closed-form count and staged uniforms; 2G <= 64):
+// in every wave, lanes 2h and 2h + 1 count head h's thresholds below lo and
+// hi (count_below), so each wave holds all G claimed ranges [N(lo), N(hi))
+// at once; the claims are then dealt to all threads of the workgroup (a hot
+// split of one head is not left to one wave), each r mapped to the key #{j :
+// a P_j <= tau_r - lo} (the CDF interval holding tau, App. A), clamped to the
+// split.  Counts go to cnt (LDS), and every chosen key sets its bit in the
+// split's key mask kmask (LDS, one bit per key) for the union compaction.
+template <int G, int MODE>
+__device__ __forceinline__ void claim_keys_mask(const HeadClaim *hc, const float *ul, int S,
+                                                float invS, const float *P, int pitch, int nrows,
+                                                int start, int64_t row0, int *cnt, unsigned *kmask,
+                                                int32_t *__restrict__ idx_out) {
+  static_assert(2 * G <= 64, "one lane per range end");
+  const int lane = threadIdx.x & 63;
+  int n = 0;
+  if (lane < 2 * G) {
+    const int h = lane >> 1;
+    const HeadClaim c = hc[h];
+    const float *uh = ul + h * (MODE == kSys ? 1 : S);
+    n = count_below<MODE>(uh, MODE == kSys ? uh[0] : 0.0f, S, invS, c.Z, (float)S / c.Z,
+                          (lane & 1) ? c.hi : c.lo);
+  }
+  int lo[G], first[G + 1];
+  first[0] = 0;
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    lo[h] = __builtin_amdgcn_readlane(n, 2 * h);
+    first[h + 1] = first[h] + max(0, __builtin_amdgcn_readlane(n, 2 * h + 1) - lo[h]);
+  }
+  for (int i = threadIdx.x; i < first[G]; i += kThreads) {
+    int h = 0, r = lo[0] + i;
+#pragma unroll
+    for (int k = 1; k < G; ++k)
+      if (i >= first[k]) h = k, r = lo[k] + (i - first[k]);
+    const HeadClaim c = hc[h];
+    const float tau = tau_of<MODE>(ul + h * (MODE == kSys ? 1 : S), r, invS, c.Z);
+    const int pos = lds_cdf_count(P + h * pitch, nrows, c.a, tau - c.lo);
+    const int j = pos < nrows ? pos : nrows - 1;
+    atomicAdd(&cnt[h * pitch + j], 1);
+    atomicOr(&kmask[j >> 5], 1u << (j & 31));
+    if (idx_out) idx_out[(row0 + h) * S + r] = start + j;
+  }
+}
+
+// The union over the group's heads of the chosen keys, in key order, from the
+// split's key mask (nwords <= 64 32-bit words), by a prefix sum of the words'
+// bit counts.  Sparse words (at most 8 bits each) are walked bit by bit by
+// the lanes of wave 0; denser masks are expanded by all waves, two words per
+// pass (lane i holds bit i % 32 of word 2p + i / 32).  Returns the list
+// length (block-uniform).
+__device__ __forceinline__ int compact_union_mask(const unsigned *kmask, int nwords, int *list) {
+  static_assert(kSplitMax / 32 <= 64, "one key-mask word per lane");
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const unsigned mine = lane < nwords ? kmask[lane] : 0u;
+  const int pc = __popc(mine);
+  const float inc = wave_incl_scan((float)pc);  // exact: at most kSplitMax
+  const int excl = (int)inc - pc;
+  const int total = (int)__int_as_float(__builtin_amdgcn_readlane(__float_as_int(inc), 63));
+  if (wave_max((float)pc) <= 8.0f) {  // uniform: every lane holds the maximum
+    if (wave == 0) {
+      unsigned m = mine;
+      int pos = excl;
+      while (m) {
+        list[pos++] = lane * 32 + (__ffs(m) - 1);
+        m &= m - 1u;
+      }
+    }
+  } else {
+    const int bit = lane & 31;
+    for (int w0 = 2 * wave; w0 < nwords; w0 += 2 * (kThreads / 64)) {
+      const int wd = w0 + (lane >> 5);  // < 64: a valid source lane
+      const unsigned m = (unsigned)__shfl((int)mine, wd);
+      const int off = __shfl(excl, wd);
+      if ((m >> bit) & 1u) list[off + __popc(m & ((1u << bit) - 1u))] = wd * 32 + bit;
+    }
+  }
+  __syncthreads();
+  return total;
+}
+
 // Value stage of one split with one query head per wave (G >= 4), for a short
 // compacted union list (list[0..nlist), the group's chosen keys in key order):
 // wave w accumulates heads w, w + 4, ... over the whole list (4 rows per wave
@@ -233,6 +340,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   __shared__ HeadClaim hc[G];
   __shared__ float mh[G], lh[G], mtmp[8 * G];
   __shared__ int rank_lds, rng[2 * G];
+  __shared__ unsigned kmask[kSplitMax / 32];  // one bit per key of the split (G = 4 claims)
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nrk = a.B * a.Hkv;
@@ -310,6 +418,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     // wait until every split of the row has published (the last arrival does
     // not wait)
     for (int i = tid; i < G * pitch; i += kThreads) cnt[i] = 0;
+    if (tid < kSplitMax / 32) kmask[tid] = 0u;
     if (a.ustage) {
 #pragma unroll
       for (int k = 0; k < kUReg; ++k) {
@@ -334,6 +443,27 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
       if (lane == 0) hc[h] = HeadClaim{oh[t], t == Tb - 1 ? kInf : oh[t + 1], oh[Tb], ah[t]};
     }
     __syncthreads();
+    if constexpr (G >= 4 && MODE != kIid) {
+      if (a.ustage) {
+        claim_keys_mask<G, MODE>(hc, ul, a.S, a.invS, P, pitch, nrows, start, row0, cnt, kmask,
+                                 a.idx_out);
+        __syncthreads();  // counts and mask complete; offl/all are no longer needed
+        const int nlist = compact_union_mask(kmask, (nrows + 31) >> 5, list);
+        float *po = part_row + (int64_t)t * G * kHeadDim;
+        if (nlist == 0) {  // a split without samples contributes zeros
+          for (int o2 = tid; o2 < G * kHeadDim / 2; o2 += kThreads)
+            st_coherent(reinterpret_cast<float2 *>(po) + o2, make_float2(0.f, 0.f));
+        } else if (nlist <= 16) {
+          gather_heads_waves<E, G, PAGED>(a.kv, b, kvh, start, cnt, pitch, list, nlist, po);
+        } else {
+          constexpr int UG = sizeof(E) <= 2 ? 8 : 4;
+          gather_list<E, G, PAGED, true, false, UG>(a.kv, b, kvh, start, list, nlist, P, pitch, cnt,
+                                                    po);
+        }
+        goto arrive2;
+      }
+    }
+    {
     bool has;
     if (a.ustage && MODE != kIid) {
       constexpr int M = MODE == kIid ? kSys : MODE;
@@ -370,8 +500,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
       float2 *pz = reinterpret_cast<float2 *>(part_row + (int64_t)t * G * kHeadDim);
       for (int o2 = tid; o2 < G * kHeadDim / 2; o2 += kThreads) st_coherent(pz + o2, make_float2(0.f, 0.f));
     }
+    }
 
     // 4. arrive; the last min(G, Tb) arrivals merge one or more heads each
+  arrive2:
     const int W = min(G, Tb);
     const int rank = row_arrive(sync, base + (unsigned long long)Tb, &rank_lds);
     if (rank < Tb - W) continue;
