@@ -335,11 +335,13 @@ def main():
         "timed_wall_s": round(wall, 3),
     }
 
-    # counter-based traffic exists for the default workload only
-    if (args.cfg == 2 and args.B is None and args.S is None and args.kind is None
-            and args.layout == "nhd" and args.path == "auto" and args.splits == 0):
+    # counter-based traffic exists for each configuration's default workload
+    if (args.cfg in TRAFFIC_FILES and args.B is None and args.S is None and args.kind is None
+            and args.layout == "nhd" and args.path == "auto" and args.splits == 0
+            and args.mode is None and args.B_draws is None and args.kv == "bf16"
+            and not args.append):
         line["roofline"]["traffic"] = measured_traffic(line["roofline"]["kernel"],
-                                                       "traffic_llama8b_32k_b1.json")
+                                                       TRAFFIC_FILES[args.cfg])
     if not args.no_cpu and not args.profile:
         line["cpu_baseline"] = cpu_baseline(w, kind, alg_bytes, args.cpu_seconds)
     print(json.dumps(line), flush=True)
@@ -351,36 +353,54 @@ def flash_tile_budget(S_total: int, n_tiles: int) -> int:
     return max(1, (2 * int(S_total) + int(n_tiles)) // (2 * int(n_tiles)))
 
 
-def kernel_source_hash() -> str:
-    """Hash of the decode kernels' HIP sources (file names and contents), as
-    recorded with the counter runs under profiles/ (the streaming-read
-    calibration kernel's file is not part of it)."""
+# Sources of each kernel family (the files its code is compiled from) for the
+# hash recorded with the counter runs under profiles/: the shared headers, the
+# launcher and the plan, plus the family's own header and instantiation units.
+COMMON_SOURCES = ["include/santa.h", "csrc/santa_plan.h", "csrc/santa_device.h",
+                  "csrc/santa_tiles.h", "csrc/santa_kernels.h", "csrc/santa_fused.h",
+                  "csrc/santa_launch.hip", "csrc/santa_api.hip"]
+FAMILY_SOURCES = {
+    "k_fused_sampled": ["csrc/santa_sampled.h", "csrc/santa_sampled_*.hip"],
+    "k_fused_dense": ["csrc/santa_dense.h", "csrc/santa_dense_*.hip"],
+    "k_stream_cdf + k_value_heads": ["csrc/santa_stream.h", "csrc/santa_stream_*.hip"],
+    "k_bern_stream + k_value_heads": ["csrc/santa_stream.h", "csrc/santa_stream_*.hip"],
+}
+# counter runs per workload: (cfg, file under profiles/)
+TRAFFIC_FILES = {2: "traffic_llama8b_32k_b1.json", 3: "traffic_llama8b_32k_b16.json",
+                 4: "traffic_llama8b_paged_b64.json", 5: "traffic_llama8b_32k_b8_bernoulli.json"}
+
+
+def kernel_source_hash(kernels: str) -> str:
+    """Hash of the HIP sources of one kernel family (file names and contents),
+    as recorded with the counter runs under profiles/."""
     import glob
     import hashlib
     h = hashlib.sha256()
-    csrc = os.path.join(ROOT, "paper_2605_01910_amd", "csrc")
-    for f in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.h"))):
-        if os.path.basename(f) == "santa_measure.hip":
-            continue
-        h.update(os.path.basename(f).encode())
+    pkg = os.path.join(ROOT, "paper_2605_01910_amd")
+    files = []
+    for pat in COMMON_SOURCES + FAMILY_SOURCES[kernels]:
+        base = ROOT if pat.startswith("include/") else pkg
+        files += sorted(glob.glob(os.path.join(base, pat)))
+    for f in files:
+        h.update(os.path.relpath(f, ROOT).encode())
         with open(f, "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kernel: str, workload_file: str):
-    """HBM bytes per launch of `kernel` from the committed FETCH_SIZE /
-    WRITE_SIZE runs, or None if there are none for this workload or the
-    kernel sources changed since they were taken."""
+def measured_traffic(kernels: str, workload_file: str):
+    """HBM bytes per call of the kernels `kernels` (one launch each) from the
+    committed FETCH_SIZE / WRITE_SIZE runs, or None if there are none for this
+    workload or the family's sources changed since they were taken."""
     path = os.path.join(ROOT, "profiles", workload_file)
     if not os.path.exists(path):
         return None
     with open(path) as fh:
         rec = json.load(fh)
-    if rec.get("source_hash") != kernel_source_hash():
+    fam = rec.get("families", {}).get(kernels)
+    if fam is None or fam.get("source_hash") != kernel_source_hash(kernels):
         return None
-    k = rec.get("kernels", {}).get(kernel)
-    return None if k is None else int(k["bytes"])
+    return int(fam["bytes"])
 
 
 def cpu_baseline(w, kind, alg_bytes, seconds):
