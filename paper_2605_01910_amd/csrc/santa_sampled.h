@@ -265,6 +265,33 @@ __device__ __forceinline__ int compact_union_mask(const unsigned *kmask, int nwo
   return total;
 }
 
+// Merge of the four heads of a group (G = 4) by one workgroup, the row's last
+// arrival: thread (h, c) sums columns 2c and 2c + 1 of head h over the row's Tb
+// split partials in split order, O = (1/S) sum_t o_t (Sec. 3.1), with up to 32
+// partials in flight per thread.
+template <typename OE>
+__device__ __forceinline__ void merge_group4(const float *part_row, int Tb, float scale,
+                                             OE *out_row0) {
+  constexpr int G = 4;
+  const int tid = threadIdx.x, h = tid >> 6, o = (tid & 63) * 2;
+  const float2 *ph = reinterpret_cast<const float2 *>(part_row + h * kHeadDim + o);
+  float sx = 0.0f, sy = 0.0f;
+  for (int t0 = 0; t0 < Tb; t0 += 32) {
+    float2 v[32];
+#pragma unroll
+    for (int i = 0; i < 32; ++i)
+      v[i] = t0 + i < Tb ? ld_coherent(ph + (int64_t)(t0 + i) * (G * kHeadDim / 2))
+                         : make_float2(0.0f, 0.0f);
+#pragma unroll
+    for (int i = 0; i < 32; ++i) {
+      sx += v[i].x;
+      sy += v[i].y;
+    }
+  }
+  store_out(out_row0 + h * kHeadDim + o, sx * scale);
+  store_out(out_row0 + h * kHeadDim + o + 1, sy * scale);
+}
+
 // Value stage of one split with one query head per wave (G >= 4), for a short
 // compacted union list (list[0..nlist), the group's chosen keys in key order):
 // wave w accumulates heads w, w + 4, ... over the whole list (4 rows per wave
@@ -504,7 +531,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 
     // 4. arrive; the last min(G, Tb) arrivals merge one or more heads each
   arrive2:
-    const int W = min(G, Tb);
+    const int W = G == 4 ? 1 : min(G, Tb);  // G = 4: the last arrival merges the group
     const int rank = row_arrive(sync, base + (unsigned long long)Tb, &rank_lds);
     if (rank < Tb - W) continue;
     if (rank == Tb - 1) {
@@ -513,9 +540,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     } else {
       row_wait(sync, base + 2ull * Tb, a.err);
     }
-    for (int h = rank - (Tb - W); h < G; h += W)
-      merge_head<QE<E>, G>(part_row, h, Tb, nullptr, nullptr, a.invS * sc.y, P,
-                           out + (row0 + h) * kHeadDim);
+    if constexpr (G == 4) {
+      merge_group4(part_row, Tb, a.invS * sc.y, out + row0 * kHeadDim);
+    } else {
+      for (int h = rank - (Tb - W); h < G; h += W)
+        merge_head<QE<E>, G>(part_row, h, Tb, nullptr, nullptr, a.invS * sc.y, P,
+                             out + (row0 + h) * kHeadDim);
+    }
   }
 }
 

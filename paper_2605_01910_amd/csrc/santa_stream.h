@@ -118,29 +118,33 @@ template <typename E, int G>
 __device__ __forceinline__ int bern_group_weights(const E *__restrict__ q, int64_t row0, int64_t grp,
                                                   int Bd, int mode, const float *__restrict__ u_q,
                                                   float *wl, int *fl, uint8_t *mask) {
-  __shared__ float tmp[4];
+  __shared__ float tmp[2 * G];
   __shared__ int wc[2];
   const int i = threadIdx.x, lane = i & 63, wave = i >> 6;
   const bool act = i < kHeadDim;
-  auto max128 = [&](float v) -> float {  // max over the first 128 threads (values >= 0)
-    v = wave_max(act ? v : 0.0f);
-    if (lane == 0) tmp[wave] = v;
-    __syncthreads();
-    const float r = fmaxf(tmp[0], tmp[1]);
-    __syncthreads();
-    return r;
-  };
-  float qv[G];
+  // the query and the Bernoulli uniforms are loaded together, up front
+  float qv[G], uq[G];
 #pragma unroll
-  for (int g = 0; g < G; ++g) qv[g] = act ? to_f32(q[(row0 + g) * kHeadDim + i]) : 0.0f;
+  for (int g = 0; g < G; ++g) {
+    qv[g] = act ? to_f32(q[(row0 + g) * kHeadDim + i]) : 0.0f;
+    uq[g] = !act ? 1.0f : mode == 0 ? u_q[(row0 + g) * kHeadDim + i]
+                                    : (g == 0 ? u_q[grp * kHeadDim + i] : 1.0f);
+  }
   float w[G];
   const float fB = (float)Bd;
   if (mode == 0) {
+    // the G norms max_i |q_{g,i}| at once: one exchange of the two waves' maxima
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      const float norm = max128(fabsf(qv[g]));
+      const float v = wave_max(fabsf(qv[g]));
+      if (lane == 0 && wave < 2) tmp[2 * g + wave] = v;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const float norm = fmaxf(tmp[2 * g], tmp[2 * g + 1]);
       const float pi = norm > 0.0f ? fabsf(qv[g]) / norm : 0.0f;
-      const float ug = act ? u_q[(row0 + g) * kHeadDim + i] : 1.0f;
+      const float ug = uq[g];
       int cnt = 0;
       for (int n = 0; n < Bd; ++n) cnt += (((float)n + ug) / fB) < pi;
       const float sgn = qv[g] > 0.0f ? 1.0f : (qv[g] < 0.0f ? -1.0f : 0.0f);
@@ -151,9 +155,12 @@ __device__ __forceinline__ int bern_group_weights(const E *__restrict__ q, int64
 #pragma unroll
     for (int g = 0; g < G; ++g) m += fabsf(qv[g]);
     m = m / (float)G;
-    const float norm = max128(m);
+    const float wm = wave_max(m);
+    if (lane == 0 && wave < 2) tmp[wave] = wm;
+    __syncthreads();
+    const float norm = fmaxf(tmp[0], tmp[1]);
     const float pi = norm > 0.0f ? m / norm : 0.0f;
-    const float ug = act ? u_q[grp * kHeadDim + i] : 1.0f;
+    const float ug = uq[0];
     int cnt = 0;
     for (int n = 0; n < Bd; ++n) cnt += (((float)n + ug) / fB) < pi;
     const float mhat = (float)cnt * (norm / fB);
@@ -255,14 +262,20 @@ __global__ __launch_bounds__(kThreads) void k_bern_stream(FusedArgs a, KtView kt
       add(kf, i);
     }
   }
-  // slot partials added in slot order: slot 0 stores, slots 1.. add in turn
-  for (int r = 0; r < FS; ++r) {
-    if (fs == r) {
+  // slot partials in a fixed order: with room for two copies of the split
+  // (2 Ls <= kSplitMax), even slots accumulate in the first copy and odd
+  // slots in the second, FS/2 rounds, and the scale pass adds the two copies;
+  // otherwise slot 0 stores and slots 1.. add in turn
+  const bool two = 2 * Ls <= pitch && (FS & 1) == 0;
+  const int nr = two ? FS / 2 : FS;
+  for (int r = 0; r < nr; ++r) {
+    if ((two ? fs >> 1 : fs) == r) {
+      float *d0 = P + (two ? (fs & 1) * Ls : 0) + kc * 8;
 #pragma unroll
       for (int h = 0; h < G; ++h)
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          float *d = P + h * pitch + kc * 8 + e;
+          float *d = d0 + h * pitch + e;
           *d = r == 0 ? acc[h][e] : *d + acc[h][e];
         }
     }
@@ -270,7 +283,8 @@ __global__ __launch_bounds__(kThreads) void k_bern_stream(FusedArgs a, KtView kt
   }
   for (int o = tid; o < G * nrows; o += kThreads) {
     const int h = o / nrows, j = o - h * nrows;
-    P[h * pitch + j] *= a.scale_log2;
+    float *d = P + h * pitch + j;
+    *d = (two ? *d + d[Ls] : *d) * a.scale_log2;
   }
   __syncthreads();
   for (int h = wave; h < G; h += kThreads / 64) {
