@@ -57,7 +57,7 @@ def parse():
     ap.add_argument("--S-tile", type=int, default=None,
                     help="flash: draws per tile (default: the budget rule S_tile ~ S / T)")
     ap.add_argument("--layout", default="nhd", choices=["nhd", "hnd"])
-    ap.add_argument("--path", default="auto", choices=["auto", "one", "two", "multi"],
+    ap.add_argument("--path", default="auto", choices=["auto", "one", "two", "multi", "rows"],
                     help="launch path (santa_set_options): by size, one persistent launch, "
                          "key stream + per-head value stage, or the multi-kernel variant")
     ap.add_argument("--splits", type=int, default=0, help="KV splits per row (0: by size)")
@@ -364,6 +364,7 @@ FAMILY_SOURCES = {
     "k_fused_dense": ["csrc/santa_dense.h", "csrc/santa_dense_*.hip"],
     "k_stream_cdf + k_value_heads": ["csrc/santa_stream.h", "csrc/santa_stream_*.hip"],
     "k_bern_stream + k_value_heads": ["csrc/santa_stream.h", "csrc/santa_stream_*.hip"],
+    "k_row_sampled": ["csrc/santa_rows.h", "csrc/santa_rows_*.hip"],
 }
 # counter runs per workload: (cfg, file under profiles/)
 TRAFFIC_FILES = {2: "traffic_llama8b_32k_b1.json", 3: "traffic_llama8b_32k_b16.json",

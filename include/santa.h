@@ -309,14 +309,24 @@ santa_status_t santa_stream_read(const void *buf, size_t bytes, uint32_t *sink, 
 /* Launch options (not part of the method): which kernels a call runs.  They
  * exist for tuning sweeps and for tests that cover every path; the defaults
  * choose by problem size.
- *   SANTA_PATH_AUTO        by size: sampled steps whose rows fit one resident
- *                          round of about 1024 workgroups take one persistent
- *                          launch, larger ones the two-launch path;
+ *   SANTA_PATH_AUTO        by measured speed: systematic and stratified steps
+ *                          with at most 64 splits per row take the scheduled
+ *                          path for S <= 1024 on grids (KV rows x splits) above
+ *                          256 workgroups and for S <= 512 below that, paged
+ *                          caches up to 8192 workgroups, FP8 caches up to
+ *                          2048; other sampled steps whose rows fit one
+ *                          resident round of about 1024 workgroups take one
+ *                          persistent launch, larger ones the two-launch path;
  *   SANTA_PATH_ONE_LAUNCH  sampled steps: one persistent launch (k_fused_sampled);
  *   SANTA_PATH_TWO_LAUNCH  sampled steps: key stream with a CDF stash, then one
  *                          workgroup per query head (k_stream_cdf, k_value_heads);
  *   SANTA_PATH_MULTI       every step: the multi-kernel variant (score/CDF,
- *                          offsets, sampling and merge kernels).
+ *                          offsets, sampling and merge kernels);
+ *   SANTA_PATH_SCHEDULED   systematic and stratified steps with at most 64
+ *                          splits per row: one hardware-scheduled launch, a
+ *                          workgroup per split that keeps its CDF in LDS across
+ *                          a row barrier (k_row_sampled); other sampled steps
+ *                          as under AUTO.
  * splits: KV splits per row of the fused paths (0 = by size; at least
  * ceil(n_k / 1024)).  The options apply to every later call made on the
  * calling thread (santa_workspace_size and santa_plan_info included) until
@@ -328,7 +338,8 @@ typedef enum {
   SANTA_PATH_AUTO = 0,
   SANTA_PATH_ONE_LAUNCH = 1,
   SANTA_PATH_TWO_LAUNCH = 2,
-  SANTA_PATH_MULTI = 3
+  SANTA_PATH_MULTI = 3,
+  SANTA_PATH_SCHEDULED = 4
 } santa_path_t;
 
 typedef struct {

@@ -165,10 +165,25 @@ santa::Plan make_plan(const santa_shape_t *sh, const santa_kv_t *kv, int S, int 
     // rows use ceil(L_b / T) keys per split rounded up to 64; Ls is the longest
     p.Ls = (int)(((p.n_k + p.T - 1) / p.T + 63) & ~63);
     const bool sampled = kind != SANTA_KIND_DENSE;
-    // sampled steps whose rows do not fit in one resident round of about 1024
-    // workgroups take the two-launch path
-    p.split2 = sampled && (g_opts.path == SANTA_PATH_TWO_LAUNCH ||
-                           (g_opts.path == SANTA_PATH_AUTO && (int64_t)p.B * p.Hkv * p.T > 1024));
+    const bool big = (int64_t)p.B * p.Hkv * p.T > 1024;  // workgroups beyond one resident round
+    // systematic and stratified steps take the scheduled path (its row offsets
+    // live in LDS, so at most kRowTMax splits per row) when asked for, and by
+    // default where it measured faster than both other paths: budgets up to
+    // 1024 on grids of more than 256 workgroups, budgets up to 512 below that;
+    // paged caches up to 8192 workgroups and FP8 caches up to 2048 (beyond
+    // those the two-launch path was faster)
+    const bool rows_ok = (kind == SANTA_KIND_SYSTEMATIC || kind == SANTA_KIND_STRATIFIED) &&
+                         p.T <= santa::kRowTMax;
+    const int64_t grid = (int64_t)p.B * p.Hkv * p.T;
+    const bool rows_auto = rows_ok && S <= 1024 && (grid > 256 || S <= 512) &&
+                           (!kv->block_table || grid <= 8192) && (p.elem != 2 || grid <= 2048);
+    p.rows = g_opts.path == SANTA_PATH_SCHEDULED ? rows_ok
+                                                 : (g_opts.path == SANTA_PATH_AUTO && rows_auto);
+    // other sampled steps whose rows do not fit in one resident round of about
+    // 1024 workgroups take the two-launch path
+    p.split2 = sampled && !p.rows &&
+               (g_opts.path == SANTA_PATH_TWO_LAUNCH ||
+                ((g_opts.path == SANTA_PATH_AUTO || g_opts.path == SANTA_PATH_SCHEDULED) && big));
     if (p.split2) {
       p.npitch = ((int64_t)p.n_k + 63) & ~int64_t(63);
       p.off_stats = take(rows * p.T * 8);
@@ -511,7 +526,7 @@ santa_status_t santa_set_options(const santa_options_t *opts) {
     g_opts = santa_options_t{SANTA_PATH_AUTO, 0};
     return SANTA_OK;
   }
-  if (opts->path < SANTA_PATH_AUTO || opts->path > SANTA_PATH_MULTI)
+  if (opts->path < SANTA_PATH_AUTO || opts->path > SANTA_PATH_SCHEDULED)
     return fail(SANTA_ERR_INVALID_ARG, "path must be a santa_path_t");
   if (opts->splits < 0 || opts->splits > santa::kMaxSplits)
     return fail(SANTA_ERR_INVALID_ARG, "splits must be in [0, 256]");
@@ -551,6 +566,9 @@ santa_status_t santa_plan_info(const santa_shape_t *shape, const santa_kv_t *kv,
   } else if (kind == SANTA_KIND_DENSE || kind == SANTA_KIND_FLASH) {
     info->path = SANTA_PATH_ONE_LAUNCH;
     info->kernels = kind == SANTA_KIND_DENSE ? "k_fused_dense" : "k_fused_dense (flash mode)";
+  } else if (p.rows) {
+    info->path = SANTA_PATH_SCHEDULED;
+    info->kernels = "k_row_sampled";
   } else if (p.split2) {
     info->path = SANTA_PATH_TWO_LAUNCH;
     info->kernels = "k_stream_cdf + k_value_heads";

@@ -66,6 +66,7 @@ FusedArgs make_args(const Plan &p, const KvView &kv, const void *q, void *out, f
   a.Hq = p.Hq;
   a.Hkv = p.Hkv;
   a.T = p.T;
+  a.Ls = p.Ls;
   a.S = p.S;
   a.npitch = p.npitch;
   a.invS = p.S ? 1.0f / (float)p.S : 0.0f;
@@ -87,6 +88,7 @@ hipError_t launch_fused_sampled(const Plan &p, const KvView &kv, const void *q, 
                                 hipStream_t st) {
   return with_elem(p, [&](auto eptr) -> hipError_t {
     using E = std::remove_pointer_t<decltype(eptr)>;
+    if (p.rows) return launch_rows_e<E>(p, kv, q, scale_log2, mode, u, idx_out, out, ws, st);
     return p.split2 ? launch_two_launch_e<E>(p, kv, q, scale_log2, mode, u, idx_out, out, ws, st)
                     : launch_one_launch_e<E>(p, kv, q, scale_log2, mode, u, idx_out, out, ws, st);
   });

@@ -12,6 +12,7 @@ constexpr int kHeadDim = 128;   // supported head dimension
 constexpr int kThreads = 256;   // threads per workgroup (4 waves of 64)
 constexpr int kSplitMax = 1024; // largest KV split (keys) handled by one workgroup
 constexpr int kMaxSplits = 256; // largest number of splits per row in the fused kernels
+constexpr int kRowTMax = 64;    // largest number of splits per row of the scheduled sampled path
 constexpr int kSyncStride = 64; // ints per row of fused-path counters (256 B apart)
 constexpr int kSyncRowsMax = 4096; // KV rows (batch * kv heads) of the fused paths' counter area
 constexpr int kErrBytes = 128;    // the error flag's section
@@ -30,6 +31,8 @@ struct Plan {
   int S;        // samples per row (0 for dense)
   int kind;     // santa_kind_t
   int fused;    // 1: single persistent launch (per-row split lengths), 0: multi-kernel
+  int rows;     // fused systematic / stratified: 1 = one hardware-scheduled launch, a
+                // workgroup per split with row barriers (k_row_sampled)
   int split2;   // fused sampled: 1 = stream + CDF stash, then one workgroup per
                 // query head; 0 = one persistent launch
   int64_t npitch;  // two-launch sampled: stash entries per query head (n_k rounded up to 64)

@@ -1,0 +1,225 @@
+// santa_rows.h -- the scheduled sampled step (k_row_sampled): systematic and
+// stratified SANTA for batches whose rows do not fit one resident round.  One
+// workgroup per (row, split), scheduled by the hardware like the two-launch
+// key stream, but the split's CDF stays in LDS: the split publishes its
+// statistics, waits at its row's barrier, claims its thresholds, gathers
+// their V rows and publishes partial sums; the row's last arrival merges.
+// No CDF stash goes through HBM.  Shared pieces are in santa_fused.h.
+#pragma once
+
+#include "santa_fused.h"
+
+namespace santa {
+
+
+// Waves per SIMD: the key stream relies on many resident workgroups, as in
+// the two-launch stream (64 VGPRs for 16-bit rows with G <= 4).
+template <typename E, int G, bool PAGED>
+constexpr int row_waves() {
+  if constexpr (sizeof(E) == 1) return G <= 4 ? 8 : 2;
+  return sizeof(E) == 2 && G <= 4 && !PAGED ? 8 : (G <= 4 ? 4 : 2);
+}
+
+// Value stage of head h in split t, by one wave, for sorted thresholds with a
+// closed-form count (kSys, kStrat): lanes 0 and 1 count the head's thresholds
+// below lo and hi (count_below; uniforms read from global memory), so the
+// split claims r in [N(lo), N(hi)).  The claims are taken 64 at a time: lane
+// l inverts tau_r on the split's LDS CDF (the key #{j : a P_j <= tau_r - lo},
+// App. A, clamped to the split); the chosen keys of a chunk are
+// non-decreasing, so equal keys form runs, and each run's V row is read once
+// and added with its length by one of the wave's four 16-lane slots, U rows
+// in flight each.  keyl/runl: the wave's run keys and start lanes (LDS).
+// Returns the head's partial sum O_h = sum_j c_{h,j} V_j (Sec. 2) reduced over
+// the four slots in lanes 0..15 (8 columns each).
+template <typename E, bool PAGED, int MODE>
+__device__ __forceinline__ void row_head_value(const FusedArgs &a, const HeadClaim &c,
+                                               const float *uh, const float *Ph, int nrows,
+                                               int start, int b, int kvh, int64_t rowq,
+                                               int16_t *keyl, uint8_t *runl, float (&acc)[8]) {
+  constexpr int U = 4;
+  const int lane = threadIdx.x & 63, slot = lane >> 4, col = lane & 15;
+  const E *V = static_cast<const E *>(a.kv.v);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = 0.0f;
+  int n = 0;
+  if (lane < 2)
+    n = count_below<MODE>(uh, MODE == kSys ? uh[0] : 0.0f, a.S, a.invS, c.Z, (float)a.S / c.Z,
+                          lane ? c.hi : c.lo);
+  const int rlo = __builtin_amdgcn_readlane(n, 0), rhi = __builtin_amdgcn_readlane(n, 1);
+  for (int c0 = rlo; c0 < rhi; c0 += 64) {
+    const int r = c0 + lane, nv = min(64, rhi - c0);
+    int j = -1;
+    if (r < rhi) {
+      const float tau = tau_of<MODE>(uh, r, a.invS, c.Z);
+      const int pos = lds_cdf_count(Ph, nrows, c.a, tau - c.lo);
+      j = pos < nrows ? pos : nrows - 1;
+      if (a.idx_out) a.idx_out[rowq * a.S + r] = start + j;
+    }
+    const int jp = __shfl_up(j, 1);
+    const bool first = r < rhi && (lane == 0 || j != jp);
+    const unsigned long long m = __ballot(first);
+    const int nruns = __popcll(m);
+    if (first) {
+      const int q = __popcll(m & ((1ull << lane) - 1ull));
+      keyl[q] = (int16_t)j;
+      runl[q] = (uint8_t)lane;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");  // the lists, for the whole wave
+    __builtin_amdgcn_wave_barrier();
+    for (int q0 = 0; q0 < nruns; q0 += 4 * U) {
+      Chunk<E> ch[U];
+      float w[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int q = q0 + slot + 4 * u;
+        if (q < nruns) {
+          const int p0 = runl[q], p1 = q + 1 < nruns ? runl[q + 1] : nv;
+          ch[u] = Chunk<E>::load(V + row_offset<PAGED>(a.kv, b, kvh, start + keyl[q]) + col * 8);
+          w[u] = (float)(p1 - p0);
+        } else {
+          ch[u] = Chunk<E>::zero();
+          w[u] = 0.0f;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        float f[8];
+        ch[u].to_float(f);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i] = fmaf(w[u], f[i], acc[i]);
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");  // lists are rewritten next chunk
+    __builtin_amdgcn_wave_barrier();
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = xor32_sum(xor16_sum(acc[i]));
+}
+
+// One workgroup per work item (rowkv, t < T), items row-major so that a row's
+// splits are dispatched together.  A split waits at its row's barrier only
+// for splits of its own row; with the dispatcher starting workgroups in
+// index order those have all started or finished before any later row's, so
+// every wait ends (and the wait is bounded regardless).  Counters as in the
+// one-launch kernel: two arrivals per split, base moved on by the merger.
+template <typename E, int G, bool PAGED, int MODE, bool APPEND = false>
+__global__ __launch_bounds__(kThreads)
+__attribute__((amdgpu_waves_per_eu(row_waves<E, G, PAGED>()))) void k_row_sampled(FusedArgs a) {
+  static_assert(MODE == kSys || MODE == kStrat, "closed-form threshold counts");
+  extern __shared__ __attribute__((aligned(16))) float dyn[];
+  constexpr int pitch = kSplitMax;
+  float *P = dyn;  // [G][pitch]: scores, then the split CDF; merge scratch at the end
+  __shared__ float offl[G][2 * kRowTMax + 1];  // per head: offsets [T+1], split factors [T]
+  __shared__ HeadClaim hc[G];
+  __shared__ float mh[G], mtmp[4 * G];
+  __shared__ int16_t keyl[4][64];
+  __shared__ uint8_t runl[4][64];
+  __shared__ int rank_lds;
+
+  const int T = a.T, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int rowkv = blockIdx.x / T, t = blockIdx.x % T;
+  const int b = rowkv / a.Hkv, kvh = rowkv % a.Hkv;
+  const int64_t row0 = (int64_t)b * a.Hq + kvh * G;
+  QE<E> *out = static_cast<QE<E> *>(a.out);
+  // splits of a.Ls keys in every row (the last one shorter), so a short row
+  // takes few splits of full length rather than T tiny ones
+  const int L = seq_len(a.kv, b);
+  const int Ls = a.Ls, Tb = L > 0 ? (L + Ls - 1) / Ls : 0;
+  if (t >= Tb) {
+    if (Tb == 0 && t == 0) {  // empty sequence: zero output, no samples
+      for (int o = tid; o < G * kHeadDim; o += kThreads) store_out(out + row0 * kHeadDim + o, 0.0f);
+      if (a.idx_out)
+        for (int o = tid; o < G * a.S; o += kThreads) a.idx_out[row0 * a.S + o] = -1;
+    }
+    return;
+  }
+  const int start = t * Ls, nrows = min(Ls, L - start);
+  if constexpr (APPEND) append_current<E, PAGED>(a.kv, b, kvh, a.Hkv, start, nrows, L);
+
+  // 1. scores of the G heads into LDS, split max, split CDF and statistics
+  {
+    const QRegs<E, G> qr = load_q<E, G>(static_cast<const QE<E> *>(a.q), b, a.Hq, kvh, tid & 15);
+    const float ksc = kv_scales<E>(a.kv, b, kvh, a.Hkv).x;  // FP8 cache: K scale
+    float mx[G];
+    score_tile<E, G, PAGED, 4>(a.kv, b, kvh, start, nrows, qr,
+                                                    a.scale_log2 * ksc, P, pitch, mx);
+    block_max_heads<G>(mx, mtmp, mh);
+  }
+  // the row's counter base: it moves on only after every split of the row,
+  // this one included, has arrived twice, so it can be read this late
+  unsigned long long *sync = a.sync + (int64_t)rowkv * (kSyncStride / 2);
+  const unsigned long long base =
+      __hip_atomic_load(sync + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  for (int h = wave; h < G; h += kThreads / 64) {
+    float *Ph = P + h * pitch;
+    wave_split_cdf_m(Ph, nrows, lane, mh[h]);
+    if (lane == 0) st_coherent(a.stats + (row0 + h) * T + t, make_float2(mh[h], Ph[nrows - 1]));
+  }
+  wait_stores();
+  __syncthreads();
+  unsigned long long arrived = 0;
+  if (tid == 0)
+    arrived = __hip_atomic_fetch_add(sync, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1;
+  row_wait_unless(sync, base + (unsigned long long)Tb, arrived, a.err);
+
+  // 2. global offsets of each head, then its claims and V gather by wave h
+  for (int h = wave; h < G; h += kThreads / 64) {
+    float *oh = offl[h], *ah = offl[h] + (T + 1);
+    head_offsets_wave<true>(a.stats + (row0 + h) * T, Tb, lane, oh, ah);
+    if (lane == 0) hc[h] = HeadClaim{oh[t], t == Tb - 1 ? kInf : oh[t + 1], oh[Tb], ah[t]};
+  }
+  __syncthreads();
+  float *part = a.part + ((int64_t)rowkv * T + t) * G * kHeadDim;
+  const int upr = MODE == kStrat ? a.S : 1;  // uniforms per head
+  for (int h = wave; h < G; h += kThreads / 64) {
+    float acc[8];
+    row_head_value<E, PAGED, MODE>(a, hc[h], a.u + (row0 + h) * upr, P + h * pitch, nrows, start,
+                                   b, kvh, row0 + h, keyl[wave], runl[wave], acc);
+    if (lane < 16) {
+      float2 *d = reinterpret_cast<float2 *>(part + h * kHeadDim + lane * 8);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) st_coherent(d + i, make_float2(acc[2 * i], acc[2 * i + 1]));
+    }
+  }
+
+  // 3. arrive again; the row's last arrival merges O = (1/S) sum_t o_t
+  const int rank = row_arrive(sync, base + (unsigned long long)Tb, &rank_lds);
+  if (rank != Tb - 1) return;
+  if (tid == 0)
+    __hip_atomic_store(sync + 1, base + 2ull * Tb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const float *part_row = a.part + (int64_t)rowkv * T * G * kHeadDim;
+  const float scale = a.invS * kv_scales<E>(a.kv, b, kvh, a.Hkv).y;  // FP8 cache: V scale
+  if constexpr (G == 4) {
+    merge_group4<16>(part_row, Tb, scale, out + row0 * kHeadDim);
+  } else {
+    for (int h = 0; h < G; ++h)
+      merge_head<QE<E>, G>(part_row, h, Tb, nullptr, nullptr, scale, P, out + (row0 + h) * kHeadDim);
+  }
+}
+
+template <typename E>
+hipError_t launch_rows_e(const Plan &p, const KvView &kv, const void *q, float scale_log2,
+                         int mode, const float *u, int32_t *idx_out, void *out, char *ws,
+                         hipStream_t st) {
+  if (p.T > kRowTMax || (mode != kSys && mode != kStrat)) return hipErrorInvalidValue;
+  FusedArgs args = make_args(p, kv, q, out, scale_log2, ws);
+  args.u = u;
+  args.idx_out = idx_out;
+  return with_g_paged(p.G, kv.bt != nullptr, [&](auto gc, auto paged) -> hipError_t {
+    constexpr int G = decltype(gc)::value;
+    constexpr bool PG = decltype(paged)::value;
+    const bool ap = kv.k_new != nullptr;
+    const void *fn =
+        mode == kStrat ? (ap ? reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kStrat, true>)
+                             : reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kStrat>))
+                       : (ap ? reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kSys, true>)
+                             : reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kSys>));
+    void *params[] = {&args};
+    const size_t lds = (size_t)G * kSplitMax * 4;
+    const CallTimer tm = call_timer();
+    return hipExtLaunchKernel(fn, dim3(p.B * p.Hkv * p.T), dim3(kThreads), params, lds, st,
+                              tm.start, tm.stop, 0);
+  });
+}
+
+}  // namespace santa

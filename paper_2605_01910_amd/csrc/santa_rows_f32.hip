@@ -1,0 +1,8 @@
+// santa_rows_f32.hip -- scheduled sampled kernels instantiated for float32 elements.
+#include "santa_rows.h"
+
+namespace santa {
+
+template hipError_t launch_rows_e<float>(const Plan &, const KvView &, const void *, float, int, const float *, int32_t *, void *, char *, hipStream_t);
+
+}  // namespace santa

@@ -10,45 +10,6 @@ namespace santa {
 // ---------------------------------------------------------------------------
 // Small-batch sampled step
 // ---------------------------------------------------------------------------
-// #{j < nrows : a P_j <= x} over a non-decreasing LDS CDF P (nrows <=
-// kSplitMax = 1024) in three dependent steps instead of ten: the number of
-// 256-key quarters whose last value is <= x (three reads), then the 16-key
-// chunks of that quarter whose last value is <= x (16 reads issued together),
-// then the keys of that chunk (four 16-byte reads).  Entries at or past nrows
-// hold stale values and are never counted.
-__device__ __forceinline__ int lds_cdf_count(const float *Ph, int nrows, float a, float x) {
-  static_assert(kSplitMax == 1024, "three levels of 4 x 16 x 16 keys");
-  // every read is inside the 1024-entry row, so the reads of a level are
-  // unconditional and issued together; the tests use non-short-circuit '&'
-  float w[16];
-#pragma unroll
-  for (int k = 1; k < 4; ++k) w[k] = Ph[256 * k - 1];
-  int q = 0;
-#pragma unroll
-  for (int k = 1; k < 4; ++k) q += ((256 * k - 1 < nrows) & (a * w[k] <= x)) ? 1 : 0;
-  const float *pq = Ph + 256 * q + 15;
-#pragma unroll
-  for (int i = 0; i < 16; ++i) w[i] = pq[16 * i];
-  int c2 = 0;
-#pragma unroll
-  for (int i = 0; i < 16; ++i) c2 += ((256 * q + 16 * i + 15 < nrows) & (a * w[i] <= x)) ? 1 : 0;
-  if (c2 == 16) return 256 * (q + 1);  // only when the quarter is the last: q = 3
-  const int j0 = 256 * q + 16 * c2;
-  const float4 *pc = reinterpret_cast<const float4 *>(Ph + j0);
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const float4 t = pc[i];
-    w[4 * i] = t.x;
-    w[4 * i + 1] = t.y;
-    w[4 * i + 2] = t.z;
-    w[4 * i + 3] = t.w;
-  }
-  int c3 = 0;
-#pragma unroll
-  for (int i = 0; i < 16; ++i) c3 += ((j0 + i < nrows) & (a * w[i] <= x)) ? 1 : 0;
-  return j0 + c3;
-}
-
 // Claims and inverse CDF of one split for thresholds held in LDS without a
 // closed-form count (the i.i.d. mode's sorted T_r Z; G*S <= kUStageMax): the
 // G*S thresholds are numbered n = r*G + h (the G heads of one r on
@@ -79,37 +40,6 @@ __device__ __forceinline__ bool claim_scan(const HeadClaim *hc, const float *ul,
     }
   }
   return __syncthreads_or(any) != 0;
-}
-
-// Number of one head's thresholds below y, N(y) = #{r < S : tau_r < y}, for
-// sorted thresholds (kSys, kStrat; uniforms in LDS).  tau_r is non-decreasing
-// in r (its fp32 evaluation is monotone), so N is its closed-form estimate --
-// kSys: ceil(y S/Z - u); kStrat: floor(y S/Z) + 1, the strata up to y's --
-// corrected until tau_{N-1} < y <= tau_N holds for tau as evaluated by the
-// claims (tau_of).  The estimate is off by at most one step of fp32 rounding
-// for S below 2^23: both neighbours are checked at once, and a loop only runs
-// when a check fails.  u0 is the head's uniform (kSys); sZ = S / Z; y = +inf
-// gives S.
-template <int MODE>
-__device__ __forceinline__ int count_below(const float *uh, float u0, int S, float invS, float Z,
-                                           float sZ, float y) {
-  static_assert(MODE == kSys || MODE == kStrat, "sorted thresholds with a closed form");
-  auto tau = [&](int r) {
-    return MODE == kSys ? threshold(r, u0, invS, Z) : tau_of<MODE>(uh, r, invS, Z);
-  };
-  const float q = fminf(y * sZ, (float)S + 2.0f);
-  int n = MODE == kSys ? (int)ceilf(q - u0) : (int)floorf(q) + 1;
-  n = min(max(n, 0), S);
-  const float tm = n > 0 ? tau(n - 1) : -kInf;
-  const float tp = n < S ? tau(n) : kInf;
-  if (tm >= y) {
-    --n;
-    while (n > 0 && tau(n - 1) >= y) --n;
-  } else if (tp < y) {
-    ++n;
-    while (n < S && tau(n) < y) ++n;
-  }
-  return n;
 }
 
 // Claimed ranges of one split for sorted thresholds (kSys, kStrat; uniforms
@@ -263,33 +193,6 @@ __device__ __forceinline__ int compact_union_mask(const unsigned *kmask, int nwo
   }
   __syncthreads();
   return total;
-}
-
-// Merge of the four heads of a group (G = 4) by one workgroup, the row's last
-// arrival: thread (h, c) sums columns 2c and 2c + 1 of head h over the row's Tb
-// split partials in split order, O = (1/S) sum_t o_t (Sec. 3.1), with up to 32
-// partials in flight per thread.
-template <typename OE>
-__device__ __forceinline__ void merge_group4(const float *part_row, int Tb, float scale,
-                                             OE *out_row0) {
-  constexpr int G = 4;
-  const int tid = threadIdx.x, h = tid >> 6, o = (tid & 63) * 2;
-  const float2 *ph = reinterpret_cast<const float2 *>(part_row + h * kHeadDim + o);
-  float sx = 0.0f, sy = 0.0f;
-  for (int t0 = 0; t0 < Tb; t0 += 32) {
-    float2 v[32];
-#pragma unroll
-    for (int i = 0; i < 32; ++i)
-      v[i] = t0 + i < Tb ? ld_coherent(ph + (int64_t)(t0 + i) * (G * kHeadDim / 2))
-                         : make_float2(0.0f, 0.0f);
-#pragma unroll
-    for (int i = 0; i < 32; ++i) {
-      sx += v[i].x;
-      sy += v[i].y;
-    }
-  }
-  store_out(out_row0 + h * kHeadDim + o, sx * scale);
-  store_out(out_row0 + h * kHeadDim + o + 1, sy * scale);
 }
 
 // Value stage of one split with one query head per wave (G >= 4), for a short

@@ -24,9 +24,10 @@ SANTA_BF16, SANTA_F32 = 0, 1
 SANTA_KV_AS_Q, SANTA_KV_FP8_E4M3 = 0, 1
 (SANTA_KIND_DENSE, SANTA_KIND_SYSTEMATIC, SANTA_KIND_STRATIFIED, SANTA_KIND_BERNOULLI,
  SANTA_KIND_FLASH, SANTA_KIND_IID) = range(6)
-SANTA_PATH_AUTO, SANTA_PATH_ONE_LAUNCH, SANTA_PATH_TWO_LAUNCH, SANTA_PATH_MULTI = range(4)
+(SANTA_PATH_AUTO, SANTA_PATH_ONE_LAUNCH, SANTA_PATH_TWO_LAUNCH, SANTA_PATH_MULTI,
+ SANTA_PATH_SCHEDULED) = range(5)
 PATHS = {"auto": SANTA_PATH_AUTO, "one": SANTA_PATH_ONE_LAUNCH, "two": SANTA_PATH_TWO_LAUNCH,
-         "multi": SANTA_PATH_MULTI}
+         "multi": SANTA_PATH_MULTI, "rows": SANTA_PATH_SCHEDULED}
 
 # every symbol include/santa.h declares
 EXPORTS = ("santa_workspace_size", "santa_workspace_init", "santa_decode_dense",

@@ -129,3 +129,49 @@ def test_stream_read_validation():
     assert lib.santa_stream_read(ok_buf, 1000, ok_sink, None) == S.SANTA_ERR_INVALID_ARG
     assert lib.santa_stream_read(P(0x100008), 1024, ok_sink, None) == S.SANTA_ERR_INVALID_ARG
     assert b"aligned" in lib.santa_last_error()
+
+
+def _plan(shape, kv, Sn, kind, path="auto", splits=0):
+    with S.options(path, splits):
+        return S.santa_plan_info(shape, kv, Sn, kind)
+
+
+def test_path_choice_by_size_cache_and_kind():
+    """The host picks a path without launching anything: the scheduled path
+    for systematic and stratified steps where it measured fastest (S <= 1024
+    above 256 workgroups, S <= 512 below; paged caches up to 8192 workgroups,
+    FP8 up to 2048), else the persistent launch within one resident round and
+    the two-launch path beyond it; i.i.d. and Bernoulli steps never take the
+    scheduled path, nor does a row that needs more than 64 splits."""
+    sysk, strat, iid = S.SANTA_KIND_SYSTEMATIC, S.SANTA_KIND_STRATIFIED, S.SANTA_KIND_IID
+    rows, two, one = "k_row_sampled", "k_stream_cdf + k_value_heads", "k_fused_sampled"
+    p1 = _plan(_shape(B=1), _kv(), 256, strat)
+    assert (p1["path"], p1["kernels"], p1["splits"]) == (S.SANTA_PATH_SCHEDULED, rows, 32)
+    assert _plan(_shape(B=1), _kv(), 512, sysk)["kernels"] == rows
+    assert _plan(_shape(B=1), _kv(), 1024, sysk)["kernels"] == one
+    assert _plan(_shape(B=1), _kv(), 2048, strat)["kernels"] == one
+    for B in (2, 16):
+        for kind in (sysk, strat):
+            p = _plan(_shape(B=B), _kv(), 256, kind)
+            assert (p["path"], p["kernels"]) == (S.SANTA_PATH_SCHEDULED, rows), (B, p)
+    assert _plan(_shape(B=16), _kv(), 1024, sysk)["kernels"] == rows
+    assert _plan(_shape(B=16), _kv(), 2048, sysk)["kernels"] == two
+    assert _plan(_shape(B=16), _kv(), 256, iid)["kernels"] == two
+    assert _plan(_shape(B=1), _kv(), 256, iid)["kernels"] == one
+    paged = _kv(n=65536, bt=16, ps=16, mp=4096)
+    assert _plan(_shape(B=16), paged, 256, sysk)["kernels"] == rows
+    assert _plan(_shape(B=64), paged, 256, sysk)["kernels"] == two
+    fp8 = _kv()
+    fp8.kv_dtype, fp8.k_scale, fp8.v_scale = S.SANTA_KV_FP8_E4M3, 16, 16
+    assert _plan(_shape(B=8), fp8, 256, sysk)["kernels"] == rows
+    assert _plan(_shape(B=16), fp8, 256, sysk)["kernels"] == two
+    assert _plan(_shape(B=16), fp8, 256, sysk, "rows")["kernels"] == "k_row_sampled"
+    # forced paths, and the scheduled option's limit of 64 splits per row
+    assert _plan(_shape(B=1), _kv(), 256, strat, "rows")["kernels"] == "k_row_sampled"
+    assert _plan(_shape(B=16), _kv(), 256, sysk, "two")["kernels"] == "k_stream_cdf + k_value_heads"
+    assert _plan(_shape(B=16), _kv(), 256, sysk, "one")["kernels"] == "k_fused_sampled"
+    p128 = _plan(_shape(B=16), _kv(n=131072), 256, sysk, "rows")
+    assert p128["splits"] > 64 and p128["kernels"] == "k_stream_cdf + k_value_heads"
+    # the scheduled path keeps the one-launch path's workspace layout
+    assert (_plan(_shape(B=16), _kv(), 256, strat, "rows")["workspace"] ==
+            _plan(_shape(B=16), _kv(), 256, strat, "one")["workspace"])

@@ -22,6 +22,8 @@ CASES = {
     "iid_one_launch": (2, "iid", dict(B=2, n=2000, S=96, ctx_len=[2000, 640]), "one"),
     "sys_paged": (4, "systematic", dict(B=3, len_lo=700, len_hi=3000), "one"),
     "sys_paged_two_launch": (4, "systematic", dict(B=3, len_lo=700, len_hi=3000), "two"),
+    "strat_scheduled": (2, "stratified", dict(B=3, n=2500, S=64, ctx_len=[2500, 1, 999]), "rows"),
+    "sys_paged_scheduled": (4, "systematic", dict(B=3, len_lo=700, len_hi=3000), "rows"),
     "dense": (2, "dense", dict(B=2, n=3000, ctx_len=[3000, 1234]), "one"),
     "dense_paged": (4, "dense", dict(B=3, len_lo=900, len_hi=2600), "one"),
     "flash": (2, "flash", dict(B=2, n=3000, ctx_len=[3000, 1500]), "one"),

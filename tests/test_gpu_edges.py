@@ -58,7 +58,16 @@ def test_cfg3_full_idx_null_bitwise(kind):
     log(f"  {check_sampled(w, out, idx, kind)}")
 
 
-@pytest.mark.parametrize("path", ["one", "two"])
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("kind", ["systematic", "stratified"])
+def test_cfg3_full_scheduled_idx_null_bitwise(kind):
+    w = make_workload(3, seed=0, kind=kind, S=256)
+    log(f"[idx NULL] cfg3 full {kind} S=256, scheduled path")
+    out, idx = _null_vs_idx(w, kind, "rows")
+    log(f"  {check_sampled(w, out, idx, kind)}")
+
+
+@pytest.mark.parametrize("path", ["one", "two", "rows"])
 @pytest.mark.parametrize("kind", ["systematic", "stratified"])
 @pytest.mark.parametrize("uval", [0.0, float(ONE_MINUS)])
 def test_extreme_uniforms(uval, kind, path):
@@ -73,7 +82,7 @@ def test_extreme_uniforms(uval, kind, path):
     assert np.all(idx[:, -1] < np.repeat(w.ctx_len, w.Hq))
 
 
-@pytest.mark.parametrize("path", ["one", "two"])
+@pytest.mark.parametrize("path", ["one", "two", "rows"])
 @pytest.mark.parametrize("L", [4096, 1000])
 def test_uniform_scores_S_equals_L_every_index_once(L, path):
     """q = 0 makes every score 0: p is uniform, and systematic sampling with
@@ -88,7 +97,7 @@ def test_uniform_scores_S_equals_L_every_index_once(L, path):
     check_sampled(w, out, idx, exact=True)
 
 
-@pytest.mark.parametrize("path", ["one", "two"])
+@pytest.mark.parametrize("path", ["one", "two", "rows"])
 @pytest.mark.parametrize("kind", ["systematic", "stratified"])
 @pytest.mark.parametrize("sink", [60.0, 120.0])
 def test_dominant_sink_takes_every_threshold(sink, kind, path):

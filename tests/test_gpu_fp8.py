@@ -53,7 +53,7 @@ CASES = {
 }
 
 
-@pytest.mark.parametrize("path", ["one", "two"])
+@pytest.mark.parametrize("path", ["one", "two", "rows"])
 @pytest.mark.parametrize("case", sorted(CASES))
 def test_fp8_parity(case, path):
     cfg, kind, over = CASES[case]

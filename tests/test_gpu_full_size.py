@@ -7,6 +7,7 @@ sequences of 4k..64k keys) included."""
 import numpy as np
 import pytest
 
+from paper_2605_01910_amd import santa as S
 from tests.gpu_util import check_dense, check_sampled, log, run
 from workload import make_workload
 
@@ -44,15 +45,28 @@ def test_cfg3_full_every_row(S):
         log(f"  dense {check_dense(w, d)}")
 
 
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("kind", ["systematic", "stratified"])
+def test_cfg3_full_scheduled_every_row(kind):
+    w = make_workload(3, seed=0, kind=kind, S=256)
+    log(f"[full cfg3, scheduled] B={w.B} n={w.n_max} {w.kind} S={w.S}")
+    with S.options("rows"):
+        out, idx, _ = run(w)
+    log(f"  sampled {check_sampled(w, out, idx)}")
+
+
 @pytest.mark.timeout(900)
-def test_cfg4_paged_full_every_row():
+@pytest.mark.parametrize("path", ["auto", "rows"])
+def test_cfg4_paged_full_every_row(path):
     w = make_workload(4, seed=0)
     log(f"[full cfg4] B={w.B} n_max={w.n_max} ctx {w.ctx_len.min()}..{w.ctx_len.max()} "
         f"rows={w.B * w.Hq}")
-    out, idx, _ = run(w)
-    log(f"  sampled {check_sampled(w, out, idx)}")
-    d, _, _ = run(w, "dense")
-    log(f"  dense {check_dense(w, d)}")
+    with S.options(path):
+        out, idx, _ = run(w)
+    log(f"  sampled ({path}) {check_sampled(w, out, idx)}")
+    if path == "auto":
+        d, _, _ = run(w, "dense")
+        log(f"  dense {check_dense(w, d)}")
 
 
 @pytest.mark.timeout(300)

@@ -190,6 +190,42 @@ def test_two_launch_sampled_parity(case):
 
 
 @pytest.mark.parametrize("case", sorted(SAMPLED_CASES))
+def test_scheduled_sampled_parity(case):
+    """The scheduled path (one hardware-scheduled launch, a workgroup per
+    split keeping its CDF in LDS across the row barrier) forced on every
+    sampled case; cases with more than 64 splits per row take the two-launch
+    path under the same option."""
+    cfg, kind, over = SAMPLED_CASES[case]
+    log(f"[scheduled/{kind}] {case} cfg={cfg} {over}")
+    w = make_workload(cfg, seed=25, kind=kind, **over)
+    with S.options("rows"):
+        out, idx, _ = run(w, kind)
+    log(f"  {check_sampled(w, out, idx, kind)}")
+
+
+def test_scheduled_many_rows_reuses_counters():
+    """The scheduled path over far more workgroups than are resident at once:
+    ragged rows (one empty), G in {4, 8}, and three calls in a row on one
+    workspace (the row counters move on by two arrivals per split)."""
+    lens = [(37 * i * i + 11 * i) % 9000 for i in range(24)]
+    lens[3] = 0
+    lens[7] = 9000
+    for over in (dict(), dict(Hq=32, Hkv=4)):
+        w = make_workload(3, B=24, n=9000, kind="stratified", S=128, ctx_len=lens, seed=56,
+                          **over)
+        dw = DeviceWorkload(w)
+        with S.options("rows"):
+            plan = S.santa_plan_info(dw.shape, dw.kv, w.S, S.SANTA_KIND_STRATIFIED)
+            assert plan["kernels"] == "k_row_sampled", plan
+            ws = S.alloc_workspace(dw.shape, dw.kv, w.S, S.SANTA_KIND_STRATIFIED)
+            log(f"[scheduled rows] B={w.B} G={w.G} n={w.n_max} T={plan['splits']}")
+            for _ in range(3):
+                out, idx, _ = run(w, dw=dw, ws=ws)
+                check_sampled(w, out, idx)
+        assert S.workspace_error(ws) == 0
+
+
+@pytest.mark.parametrize("case", sorted(SAMPLED_CASES))
 def test_one_launch_sampled_parity(case):
     """The small-batch sampled path forced on every sampled case."""
     cfg, kind, over = SAMPLED_CASES[case]
@@ -228,12 +264,12 @@ def test_workspace_shared_by_both_sampled_paths():
     w = make_workload(2, B=4, n=3000, kind="stratified", S=128, seed=55)
     dw = DeviceWorkload(w)
     spaces = [S.alloc_workspace(dw.shape, dw.kv, 1, S.SANTA_KIND_DENSE)]
-    for path in ("one", "two"):
+    for path in ("one", "two", "rows"):
         with S.options(path):
             spaces.append(S.alloc_workspace(dw.shape, dw.kv, w.S, S.SANTA_KIND_STRATIFIED))
     ws = max(spaces, key=lambda x: x.numel())
-    log("[workspace] one, two, dense, one")
-    for path in ("one", "two", "dense", "one"):
+    log("[workspace] one, two, rows, dense, one, rows")
+    for path in ("one", "two", "rows", "dense", "one", "rows"):
         if path == "dense":
             d, _, _ = run(w, "dense", dw=dw, ws=ws)
             check_dense(w, d)
@@ -252,15 +288,15 @@ def test_workspace_shared_by_every_kind():
     ds, db = DeviceWorkload(ws_), DeviceWorkload(wb)
     spaces = [S.alloc_workspace(db.shape, db.kv, wb.S, S.SANTA_KIND_BERNOULLI),
               S.alloc_workspace(ds.shape, ds.kv, 1, S.SANTA_KIND_DENSE)]
-    for path in ("one", "two", "multi"):
+    for path in ("one", "two", "multi", "rows"):
         with S.options(path):
             spaces.append(S.alloc_workspace(ds.shape, ds.kv, ws_.S, S.SANTA_KIND_SYSTEMATIC))
     ws = max(spaces, key=lambda x: x.numel())
-    order = ["one", "bernoulli", "one", "multi", "one", "two", "bernoulli", "two",
-             "dense", "multi", "one"]
+    order = ["one", "bernoulli", "rows", "one", "multi", "one", "two", "bernoulli", "two",
+             "rows", "dense", "multi", "rows", "one"]
     log(f"[workspace] {' '.join(order)}")
     for step in order:
-        with S.options(step if step in ("one", "two", "multi") else "auto"):
+        with S.options(step if step in ("one", "two", "multi", "rows") else "auto"):
             if step == "bernoulli":
                 out, idx, _ = run(wb, "bernoulli", dw=db, ws=ws)
                 check_sampled(wb, out, idx, "bernoulli")

@@ -45,7 +45,7 @@ CALLS = [
 ]
 
 
-@pytest.mark.parametrize("path", ["auto", "two"])
+@pytest.mark.parametrize("path", ["auto", "two", "rows"])
 def test_noalloc_matches_workspace_call(path):
     with S.options(path):
         for i, (name, over) in enumerate(CALLS):
