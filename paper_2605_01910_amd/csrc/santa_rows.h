@@ -22,8 +22,11 @@ constexpr int row_waves() {
 
 // Value stage of head h in split t, by one wave, for sorted thresholds with a
 // closed-form count (kSys, kStrat): lanes 0 and 1 count the head's thresholds
-// below lo and hi (count_below; uniforms read from global memory), so the
-// split claims r in [N(lo), N(hi)).  The claims are taken 64 at a time: lane
+// below lo and hi (count_below), so the split claims r in [N(lo), N(hi)).
+// ureg: the head's uniforms fetched before the row barrier -- kSys: u in
+// ureg[0]; kStrat with S <= 256 and staged (one head per wave): u_r in
+// ureg[r / 64] of lane r % 64, read with lane shuffles; otherwise u_r comes
+// from global memory.  The claims are taken 64 at a time: lane
 // l inverts tau_r on the split's LDS CDF (the key #{j : a P_j <= tau_r - lo},
 // App. A, clamped to the split); the chosen keys of a chunk are
 // non-decreasing, so equal keys form runs, and each run's V row is read once
@@ -33,9 +36,10 @@ constexpr int row_waves() {
 // the four slots in lanes 0..15 (8 columns each).
 template <typename E, bool PAGED, int MODE>
 __device__ __forceinline__ void row_head_value(const FusedArgs &a, const HeadClaim &c,
-                                               const float *uh, const float *Ph, int nrows,
-                                               int start, int b, int kvh, int64_t rowq,
-                                               int16_t *keyl, uint8_t *runl, float (&acc)[8]) {
+                                               const float *uh, const float (&ureg)[4], bool staged,
+                                               const float *Ph, int nrows, int start, int b,
+                                               int kvh, int64_t rowq, int16_t *keyl,
+                                               uint8_t *runl, float (&acc)[8]) {
   constexpr int U = 4;
   const int lane = threadIdx.x & 63, slot = lane >> 4, col = lane & 15;
   const E *V = static_cast<const E *>(a.kv.v);
@@ -43,14 +47,22 @@ __device__ __forceinline__ void row_head_value(const FusedArgs &a, const HeadCla
   for (int i = 0; i < 8; ++i) acc[i] = 0.0f;
   int n = 0;
   if (lane < 2)
-    n = count_below<MODE>(uh, MODE == kSys ? uh[0] : 0.0f, a.S, a.invS, c.Z, (float)a.S / c.Z,
+    n = count_below<MODE>(uh, MODE == kSys ? ureg[0] : 0.0f, a.S, a.invS, c.Z, (float)a.S / c.Z,
                           lane ? c.hi : c.lo);
   const int rlo = __builtin_amdgcn_readlane(n, 0), rhi = __builtin_amdgcn_readlane(n, 1);
+  const bool regs = MODE == kSys || (staged && a.S <= 4 * 64);
   for (int c0 = rlo; c0 < rhi; c0 += 64) {
     const int r = c0 + lane, nv = min(64, rhi - c0);
+    float ur = ureg[0];
+    if (MODE == kStrat && regs) {  // u_r from lane r % 64 (every lane takes part)
+      const int src = r & 63, k = (r >> 6) & 3;
+      const float v0 = __shfl(ureg[0], src), v1 = __shfl(ureg[1], src);
+      const float v2 = __shfl(ureg[2], src), v3 = __shfl(ureg[3], src);
+      ur = k == 0 ? v0 : (k == 1 ? v1 : (k == 2 ? v2 : v3));
+    }
     int j = -1;
     if (r < rhi) {
-      const float tau = tau_of<MODE>(uh, r, a.invS, c.Z);
+      const float tau = threshold(r, (MODE == kStrat && !regs) ? uh[r] : ur, a.invS, c.Z);
       const int pos = lds_cdf_count(Ph, nrows, c.a, tau - c.lo);
       j = pos < nrows ? pos : nrows - 1;
       if (a.idx_out) a.idx_out[rowq * a.S + r] = start + j;
@@ -160,6 +172,18 @@ __attribute__((amdgpu_waves_per_eu(row_waves<E, G, PAGED>()))) void k_row_sample
   unsigned long long arrived = 0;
   if (tid == 0)
     arrived = __hip_atomic_fetch_add(sync, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1;
+  // the uniforms of head `wave` (G <= 4), fetched while the row arrives
+  const int upr = MODE == kStrat ? a.S : 1;  // uniforms per head
+  float ureg[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (G <= 4 && wave < G) {
+    const float *uw = a.u + (row0 + wave) * upr;
+    if (MODE == kSys) {
+      ureg[0] = uw[0];
+    } else if (a.S <= 4 * 64) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) ureg[k] = lane + 64 * k < a.S ? uw[lane + 64 * k] : 0.0f;
+    }
+  }
   row_wait_unless(sync, base + (unsigned long long)Tb, arrived, a.err);
 
   // 2. global offsets of each head, then its claims and V gather by wave h
@@ -170,11 +194,14 @@ __attribute__((amdgpu_waves_per_eu(row_waves<E, G, PAGED>()))) void k_row_sample
   }
   __syncthreads();
   float *part = a.part + ((int64_t)rowkv * T + t) * G * kHeadDim;
-  const int upr = MODE == kStrat ? a.S : 1;  // uniforms per head
   for (int h = wave; h < G; h += kThreads / 64) {
     float acc[8];
-    row_head_value<E, PAGED, MODE>(a, hc[h], a.u + (row0 + h) * upr, P + h * pitch, nrows, start,
-                                   b, kvh, row0 + h, keyl[wave], runl[wave], acc);
+    const float *uh = a.u + (row0 + h) * upr;
+    if (G > 4) {  // two heads per wave: the head's own uniforms, from global memory
+      ureg[0] = MODE == kSys ? uh[0] : 0.0f;
+    }
+    row_head_value<E, PAGED, MODE>(a, hc[h], uh, ureg, G <= 4, P + h * pitch, nrows, start, b,
+                                   kvh, row0 + h, keyl[wave], runl[wave], acc);
     if (lane < 16) {
       float2 *d = reinterpret_cast<float2 *>(part + h * kHeadDim + lane * 8);
 #pragma unroll
