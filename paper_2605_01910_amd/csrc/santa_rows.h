@@ -26,20 +26,21 @@ constexpr int row_waves() {
 // ureg: the head's uniforms fetched before the row barrier -- kSys: u in
 // ureg[0]; kStrat with S <= 256 and staged (one head per wave): u_r in
 // ureg[r / 64] of lane r % 64, read with lane shuffles; otherwise u_r comes
-// from global memory.  The claims are taken 64 at a time: lane
-// l inverts tau_r on the split's LDS CDF (the key #{j : a P_j <= tau_r - lo},
-// App. A, clamped to the split); the chosen keys of a chunk are
-// non-decreasing, so equal keys form runs, and each run's V row is read once
-// and added with its length by one of the wave's four 16-lane slots, U rows
-// in flight each.  keyl/runl: the wave's run keys and start lanes (LDS).
-// Returns the head's partial sum O_h = sum_j c_{h,j} V_j (Sec. 2) reduced over
-// the four slots in lanes 0..15 (8 columns each).
+// from global memory.  The claims are taken 64 at a time: lane l inverts
+// tau_r on the split's LDS CDF (the key #{j : a P_j <= tau_r - lo}, App. A,
+// clamped to the split).  The chosen keys are non-decreasing in r, so equal
+// keys form runs; the runs of successive chunks go to a list of (key, count)
+// in LDS (keyl, cntl: 64 entries), gathered when the next chunk's runs would
+// not fit and at the end: each listed V row is read once per entry and added
+// with its count by one of the wave's four 16-lane slots, U rows in flight
+// each.  Returns the head's partial sum O_h = sum_j c_{h,j} V_j
+// (Sec. 2) reduced over the four slots in lanes 0..15 (8 columns each).
 template <typename E, bool PAGED, int MODE>
 __device__ __forceinline__ void row_head_value(const FusedArgs &a, const HeadClaim &c,
                                                const float *uh, const float (&ureg)[4], bool staged,
                                                const float *Ph, int nrows, int start, int b,
-                                               int kvh, int64_t rowq, int16_t *keyl,
-                                               uint8_t *runl, float (&acc)[8]) {
+                                               int kvh, int64_t rowq, int16_t *keyl, int *cntl,
+                                               float (&acc)[8]) {
   constexpr int U = 4;
   const int lane = threadIdx.x & 63, slot = lane >> 4, col = lane & 15;
   const E *V = static_cast<const E *>(a.kv.v);
@@ -51,43 +52,20 @@ __device__ __forceinline__ void row_head_value(const FusedArgs &a, const HeadCla
                           lane ? c.hi : c.lo);
   const int rlo = __builtin_amdgcn_readlane(n, 0), rhi = __builtin_amdgcn_readlane(n, 1);
   const bool regs = MODE == kSys || (staged && a.S <= 4 * 64);
-  for (int c0 = rlo; c0 < rhi; c0 += 64) {
-    const int r = c0 + lane, nv = min(64, rhi - c0);
-    float ur = ureg[0];
-    if (MODE == kStrat && regs) {  // u_r from lane r % 64 (every lane takes part)
-      const int src = r & 63, k = (r >> 6) & 3;
-      const float v0 = __shfl(ureg[0], src), v1 = __shfl(ureg[1], src);
-      const float v2 = __shfl(ureg[2], src), v3 = __shfl(ureg[3], src);
-      ur = k == 0 ? v0 : (k == 1 ? v1 : (k == 2 ? v2 : v3));
-    }
-    int j = -1;
-    if (r < rhi) {
-      const float tau = threshold(r, (MODE == kStrat && !regs) ? uh[r] : ur, a.invS, c.Z);
-      const int pos = lds_cdf_count(Ph, nrows, c.a, tau - c.lo);
-      j = pos < nrows ? pos : nrows - 1;
-      if (a.idx_out) a.idx_out[rowq * a.S + r] = start + j;
-    }
-    const int jp = __shfl_up(j, 1);
-    const bool first = r < rhi && (lane == 0 || j != jp);
-    const unsigned long long m = __ballot(first);
-    const int nruns = __popcll(m);
-    if (first) {
-      const int q = __popcll(m & ((1ull << lane) - 1ull));
-      keyl[q] = (int16_t)j;
-      runl[q] = (uint8_t)lane;
-    }
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");  // the lists, for the whole wave
+  auto sync_lists = [] {  // list writes visible to the whole wave, in order
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     __builtin_amdgcn_wave_barrier();
-    for (int q0 = 0; q0 < nruns; q0 += 4 * U) {
+  };
+  auto gather = [&](int nl) {  // add the nl listed rows with their counts
+    for (int q0 = 0; q0 < nl; q0 += 4 * U) {
       Chunk<E> ch[U];
       float w[U];
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int q = q0 + slot + 4 * u;
-        if (q < nruns) {
-          const int p0 = runl[q], p1 = q + 1 < nruns ? runl[q + 1] : nv;
+        if (q < nl) {
           ch[u] = Chunk<E>::load(V + row_offset<PAGED>(a.kv, b, kvh, start + keyl[q]) + col * 8);
-          w[u] = (float)(p1 - p0);
+          w[u] = (float)cntl[q];
         } else {
           ch[u] = Chunk<E>::zero();
           w[u] = 0.0f;
@@ -101,8 +79,45 @@ __device__ __forceinline__ void row_head_value(const FusedArgs &a, const HeadCla
         for (int i = 0; i < 8; ++i) acc[i] = fmaf(w[u], f[i], acc[i]);
       }
     }
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");  // lists are rewritten next chunk
-    __builtin_amdgcn_wave_barrier();
+  };
+  int nl = 0;  // entries in the list (the same in every lane)
+  for (int c0 = rlo;; c0 += 64) {  // one pass past the last chunk gathers the rest
+    const bool done = c0 >= rhi;
+    const int r = c0 + lane, nv = min(64, rhi - c0);
+    int j = -1;
+    if (!done) {
+      float ur = ureg[0];
+      if (MODE == kStrat && regs) {  // u_r from lane r % 64 (every lane takes part)
+        const int src = r & 63, k = (r >> 6) & 3;
+        const float v0 = __shfl(ureg[0], src), v1 = __shfl(ureg[1], src);
+        const float v2 = __shfl(ureg[2], src), v3 = __shfl(ureg[3], src);
+        ur = k == 0 ? v0 : (k == 1 ? v1 : (k == 2 ? v2 : v3));
+      }
+      if (r < rhi) {
+        const float tau = threshold(r, (MODE == kStrat && !regs) ? uh[r] : ur, a.invS, c.Z);
+        const int pos = lds_cdf_count(Ph, nrows, c.a, tau - c.lo);
+        j = pos < nrows ? pos : nrows - 1;
+        if (a.idx_out) a.idx_out[rowq * a.S + r] = start + j;
+      }
+    }
+    const int jp = __shfl_up(j, 1);
+    const bool first = !done && r < rhi && (lane == 0 || j != jp);
+    const unsigned long long m = __ballot(first);
+    const int nruns = __popcll(m);
+    if (done || nl + nruns > 64) {  // the end, or the list is full: gather it
+      gather(nl);
+      sync_lists();
+      nl = 0;
+      if (done) break;
+    }
+    if (first) {
+      const unsigned long long rest = lane < 63 ? m >> (lane + 1) : 0ull;
+      const int e = nl + __popcll(m & ((1ull << lane) - 1ull));
+      keyl[e] = (int16_t)j;
+      cntl[e] = rest ? __builtin_ctzll(rest) + 1 : nv - lane;
+    }
+    nl += nruns;
+    sync_lists();
   }
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc[i] = xor32_sum(xor16_sum(acc[i]));
@@ -125,7 +140,7 @@ __attribute__((amdgpu_waves_per_eu(row_waves<E, G, PAGED>()))) void k_row_sample
   __shared__ HeadClaim hc[G];
   __shared__ float mh[G], mtmp[4 * G];
   __shared__ int16_t keyl[4][64];
-  __shared__ uint8_t runl[4][64];
+  __shared__ int cntl[4][64];
   __shared__ int rank_lds;
 
   const int T = a.T, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -201,7 +216,7 @@ __attribute__((amdgpu_waves_per_eu(row_waves<E, G, PAGED>()))) void k_row_sample
       ureg[0] = MODE == kSys ? uh[0] : 0.0f;
     }
     row_head_value<E, PAGED, MODE>(a, hc[h], uh, ureg, G <= 4, P + h * pitch, nrows, start, b,
-                                   kvh, row0 + h, keyl[wave], runl[wave], acc);
+                                   kvh, row0 + h, keyl[wave], cntl[wave], acc);
     if (lane < 16) {
       float2 *d = reinterpret_cast<float2 *>(part + h * kHeadDim + lane * 8);
 #pragma unroll
