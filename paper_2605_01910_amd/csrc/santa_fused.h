@@ -79,12 +79,16 @@ struct FusedArgs {
   int S_tile;     // flash: samples per tile and head
   int Tmax;       // flash: tiles of the longest row, ceil(n_k / tile)
   int Ls;         // scheduled sampled path: keys per split of every row (multiple of 64)
+  int direct;     // scheduled sampled path: every wave polls the row's statistics mailbox
 };
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kSpinLimit = 1 << 22;
+// Scheduled sampled path: grids of at most this many workgroups (one per CU
+// of the MI355X) wait at the row barrier by polling the statistics directly.
+constexpr int kDirectPollMax = 256;
 constexpr int kAlign = 64;         // split lengths and stash rows are multiples of this many keys
 constexpr int kBlock = 32;         // keys per block of the two-level CDF search
 constexpr int kGatherUnroll = 8;   // V rows in flight per row slot in k_value_heads
@@ -222,17 +226,16 @@ __device__ __forceinline__ void row_wait_unless(const unsigned long long *sync,
 // One wave: global offsets of one head over the row's Tb splits.  off[0..Tb]
 // receives Off_0 = 0, Off_{t+1} = Off_t + a_t l_t with a_t = exp2(m_t - m*),
 // made exactly non-decreasing; al[t] receives a_t.  Returns m*.  Lane l owns
-// splits l*ch .. l*ch+ch-1 (ch <= kMaxSplits / 64).
-template <bool COHERENT>
-__device__ __forceinline__ float head_offsets_wave(const float2 *st, int Tb, int lane, float *off,
-                                                   float *al) {
+// splits l*ch .. l*ch+ch-1 (ch <= kMaxSplits / 64), with (m_t, l_t) = ld(t).
+template <typename LD>
+__device__ __forceinline__ float head_offsets_from(LD ld, int Tb, int lane, float *off, float *al) {
   constexpr int CHM = kMaxSplits / 64;
   const int ch = (Tb + 63) >> 6;
   const int t0 = lane * ch;
   float2 sv[CHM];
 #pragma unroll
   for (int i = 0; i < CHM; ++i)
-    sv[i] = (i < ch && t0 + i < Tb) ? ld2<COHERENT>(st + t0 + i) : make_float2(-kInf, 0.0f);
+    sv[i] = (i < ch && t0 + i < Tb) ? ld(t0 + i) : make_float2(-kInf, 0.0f);
   float m = -kInf;
 #pragma unroll
   for (int i = 0; i < CHM; ++i) m = fmaxf(m, sv[i].x);
@@ -261,6 +264,13 @@ __device__ __forceinline__ float head_offsets_wave(const float2 *st, int Tb, int
   }
   if (lane == 0) off[0] = 0.0f;
   return m;
+}
+
+// The same over statistics in global memory, st[t] = (m_t, l_t).
+template <bool COHERENT>
+__device__ __forceinline__ float head_offsets_wave(const float2 *st, int Tb, int lane, float *off,
+                                                   float *al) {
+  return head_offsets_from([&](int t) { return ld2<COHERENT>(st + t); }, Tb, lane, off, al);
 }
 
 // out_h = scale * sum_t w_t part[t][h*128 + o] (w_t = 1 if w is null), divided

@@ -13,7 +13,12 @@ constexpr int kThreads = 256;   // threads per workgroup (4 waves of 64)
 constexpr int kSplitMax = 1024; // largest KV split (keys) handled by one workgroup
 constexpr int kMaxSplits = 256; // largest number of splits per row in the fused kernels
 constexpr int kRowTMax = 64;    // largest number of splits per row of the scheduled sampled path
-constexpr int kSyncStride = 64; // ints per row of fused-path counters (256 B apart)
+// Per KV row, the fused paths keep a sync block of kSyncStride ints: the
+// counters in the first 256 bytes, then (at u64 index kMailOffset) the
+// scheduled sampled path's statistics mailbox, one u64 per (head < 8, split <
+// kRowTMax), zero whenever no call is running.
+constexpr int kMailOffset = 32;
+constexpr int kSyncStride = 2 * kMailOffset + 2 * 8 * kRowTMax;
 constexpr int kSyncRowsMax = 4096; // KV rows (batch * kv heads) of the fused paths' counter area
 constexpr int kErrBytes = 128;    // the error flag's section
 
@@ -50,9 +55,10 @@ struct Plan {
   size_t off_blist;  // int    [B*Hkv*128]  Bernoulli feature list
   size_t off_bn;     // int    [B*Hkv]      Bernoulli feature count
   size_t off_err;    // int    [1]          fused: a wait gave up
-  size_t off_sync;   // u64    [kSyncRowsMax*kSyncStride/2] fused: per-row counters; the area
-                     // has the same offset and size in every layout, so calls of any kind
-                     // and shape find their counters where earlier calls left them
+  size_t off_sync;   // u64    [kSyncRowsMax*kSyncStride/2] fused: per-row sync blocks
+                     // (counters, mailbox); the area has the same offset and size in every
+                     // layout, so calls of any kind and shape find their counters where
+                     // earlier calls left them
   size_t total;
 };
 

@@ -20,12 +20,44 @@ constexpr int row_waves() {
   return sizeof(E) == 2 && G <= 4 && !PAGED ? 8 : (G <= 4 ? 4 : 2);
 }
 
+// Statistics mailbox of one row: word (h, t) holds the bits of (m_t, l_t) of
+// head h in split t, l_t in the high half.  l_t >= 1 (the split's largest
+// key adds exp2(0)), so a word whose high half is zero is empty.  Each word is
+// written and read whole with 64-bit atomics, so a reader that sees it
+// non-empty sees both values; the row's merger empties the words after every
+// split has read them.
+__device__ __forceinline__ void post_stats(unsigned long long *w, float m, float l) {
+  const unsigned long long v = ((unsigned long long)__float_as_uint(l) << 32) | __float_as_uint(m);
+  __hip_atomic_store(w, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// One wave: lane t < Tb waits for word t (bounded spin; on giving up the
+// error flag is set and the caller's results are not valid) and returns its
+// (m_t, l_t).
+__device__ __forceinline__ float2 wait_stats(const unsigned long long *w, int Tb, int lane,
+                                             int *err) {
+  unsigned long long v = 0;
+  for (int spins = 0;; ++spins) {
+    if (lane < Tb && (v >> 32) == 0)
+      v = __hip_atomic_load(const_cast<unsigned long long *>(w + lane), __ATOMIC_RELAXED,
+                            __HIP_MEMORY_SCOPE_AGENT);
+    if (__all(lane >= Tb || (v >> 32) != 0)) break;
+    if (spins > kSpinLimit) {
+      if (lane == 0) atomicOr(err, 1);
+      break;
+    }
+    __builtin_amdgcn_s_sleep(1);
+  }
+  return make_float2(__uint_as_float((unsigned)v), __uint_as_float((unsigned)(v >> 32)));
+}
+
 // Value stage of head h in split t, by one wave, for sorted thresholds with a
-// closed-form count (kSys, kStrat): lanes 0 and 1 count the head's thresholds
-// below lo and hi (count_below), so the split claims r in [N(lo), N(hi)).
-// ureg: the head's uniforms fetched before the row barrier -- kSys: u in
-// ureg[0]; kStrat with S <= 256 and staged (one head per wave): u_r in
-// ureg[r / 64] of lane r % 64, read with lane shuffles; otherwise u_r comes
+// closed-form count (kSys, kStrat): the split claims r in [N(lo), N(hi)),
+// N(y) = #{r : tau_r < y}.  ureg: the head's uniforms fetched before the row
+// barrier -- kSys: u in ureg[0]; kStrat with S <= 256 and staged (one head
+// per wave): u_r in ureg[r / 64] of lane r % 64, so every lane counts its own
+// thresholds and the claims read u_r with lane shuffles; otherwise lanes 0
+// and 1 evaluate N(lo) and N(hi) in closed form (count_below) and u_r comes
 // from global memory.  The claims are taken 64 at a time: lane l inverts
 // tau_r on the split's LDS CDF (the key #{j : a P_j <= tau_r - lo}, App. A,
 // clamped to the split).  The chosen keys are non-decreasing in r, so equal
@@ -46,12 +78,24 @@ __device__ __forceinline__ void row_head_value(const FusedArgs &a, const HeadCla
   const E *V = static_cast<const E *>(a.kv.v);
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc[i] = 0.0f;
-  int n = 0;
-  if (lane < 2)
-    n = count_below<MODE>(uh, MODE == kSys ? ureg[0] : 0.0f, a.S, a.invS, c.Z, (float)a.S / c.Z,
-                          lane ? c.hi : c.lo);
-  const int rlo = __builtin_amdgcn_readlane(n, 0), rhi = __builtin_amdgcn_readlane(n, 1);
   const bool regs = MODE == kSys || (staged && a.S <= 4 * 64);
+  int rlo = 0, rhi = 0;
+  if (MODE == kStrat && regs) {  // N(lo), N(hi) counted over the uniforms in registers
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int r = lane + 64 * k;
+      const float tau = r < a.S ? threshold(r, ureg[k], a.invS, c.Z) : kInf;
+      rlo += __popcll(__ballot(tau < c.lo));
+      rhi += __popcll(__ballot(tau < c.hi));
+    }
+  } else {
+    int n = 0;
+    if (lane < 2)
+      n = count_below<MODE>(uh, MODE == kSys ? ureg[0] : 0.0f, a.S, a.invS, c.Z,
+                            (float)a.S / c.Z, lane ? c.hi : c.lo);
+    rlo = __builtin_amdgcn_readlane(n, 0);
+    rhi = __builtin_amdgcn_readlane(n, 1);
+  }
   auto sync_lists = [] {  // list writes visible to the whole wave, in order
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -124,11 +168,17 @@ __device__ __forceinline__ void row_head_value(const FusedArgs &a, const HeadCla
 }
 
 // One workgroup per work item (rowkv, t < T), items row-major so that a row's
-// splits are dispatched together.  A split waits at its row's barrier only
-// for splits of its own row; with the dispatcher starting workgroups in
-// index order those have all started or finished before any later row's, so
-// every wait ends (and the wait is bounded regardless).  Counters as in the
-// one-launch kernel: two arrivals per split, base moved on by the merger.
+// splits are dispatched together.  A split waits only for splits of its own
+// row; with the dispatcher starting workgroups in index order those have all
+// started or finished before any later row's, so every wait ends (and the
+// wait is bounded regardless).  Row barrier, direct (grids of at most
+// kDirectPollMax workgroups, one per CU): the split posts its statistics to
+// the row's mailbox and each wave polls its head's words of all Tb splits;
+// the partial sums take one arrival per split on the row counter (sync[0];
+// sync[1] holds its value at the start of the call), and the merger moves the
+// base on and empties the mailbox.  Otherwise, where waiting workgroups share
+// CUs with streaming ones, thread 0 polls the counter: two arrivals per
+// split, after the statistics and after the partial sums.
 template <typename E, int G, bool PAGED, int MODE, bool APPEND = false>
 __global__ __launch_bounds__(kThreads)
 __attribute__((amdgpu_waves_per_eu(row_waves<E, G, PAGED>()))) void k_row_sampled(FusedArgs a) {
@@ -137,7 +187,6 @@ __attribute__((amdgpu_waves_per_eu(row_waves<E, G, PAGED>()))) void k_row_sample
   constexpr int pitch = kSplitMax;
   float *P = dyn;  // [G][pitch]: scores, then the split CDF; merge scratch at the end
   __shared__ float offl[G][2 * kRowTMax + 1];  // per head: offsets [T+1], split factors [T]
-  __shared__ HeadClaim hc[G];
   __shared__ float mh[G], mtmp[4 * G];
   __shared__ int16_t keyl[4][64];
   __shared__ int cntl[4][64];
@@ -173,20 +222,26 @@ __attribute__((amdgpu_waves_per_eu(row_waves<E, G, PAGED>()))) void k_row_sample
     block_max_heads<G>(mx, mtmp, mh);
   }
   // the row's counter base: it moves on only after every split of the row,
-  // this one included, has arrived twice, so it can be read this late
+  // this one included, has made its last arrival, so it can be read this late
   unsigned long long *sync = a.sync + (int64_t)rowkv * (kSyncStride / 2);
+  unsigned long long *mail = sync + kMailOffset;
   const unsigned long long base =
       __hip_atomic_load(sync + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   for (int h = wave; h < G; h += kThreads / 64) {
     float *Ph = P + h * pitch;
     wave_split_cdf_m(Ph, nrows, lane, mh[h]);
-    if (lane == 0) st_coherent(a.stats + (row0 + h) * T + t, make_float2(mh[h], Ph[nrows - 1]));
+    if (lane == 0) {
+      if (a.direct) post_stats(mail + h * kRowTMax + t, mh[h], Ph[nrows - 1]);
+      else st_coherent(a.stats + (row0 + h) * T + t, make_float2(mh[h], Ph[nrows - 1]));
+    }
   }
-  wait_stores();
-  __syncthreads();
   unsigned long long arrived = 0;
-  if (tid == 0)
-    arrived = __hip_atomic_fetch_add(sync, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1;
+  if (!a.direct) {  // first arrival, once the statistics are stored
+    wait_stores();
+    __syncthreads();
+    if (tid == 0)
+      arrived = __hip_atomic_fetch_add(sync, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1;
+  }
   // the uniforms of head `wave` (G <= 4), fetched while the row arrives
   const int upr = MODE == kStrat ? a.S : 1;  // uniforms per head
   float ureg[4] = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -199,24 +254,27 @@ __attribute__((amdgpu_waves_per_eu(row_waves<E, G, PAGED>()))) void k_row_sample
       for (int k = 0; k < 4; ++k) ureg[k] = lane + 64 * k < a.S ? uw[lane + 64 * k] : 0.0f;
     }
   }
-  row_wait_unless(sync, base + (unsigned long long)Tb, arrived, a.err);
-
-  // 2. global offsets of each head, then its claims and V gather by wave h
-  for (int h = wave; h < G; h += kThreads / 64) {
-    float *oh = offl[h], *ah = offl[h] + (T + 1);
-    head_offsets_wave<true>(a.stats + (row0 + h) * T, Tb, lane, oh, ah);
-    if (lane == 0) hc[h] = HeadClaim{oh[t], t == Tb - 1 ? kInf : oh[t + 1], oh[Tb], ah[t]};
-  }
-  __syncthreads();
+  // 2. the row barrier, then per head, by wave h: global offsets, its claims
+  // and V gather.  Direct: the wave polls its head's mailbox words.
+  // Otherwise thread 0 polls the counter and the waves read the statistics.
+  if (!a.direct) row_wait_unless(sync, base + (unsigned long long)Tb, arrived, a.err);
   float *part = a.part + ((int64_t)rowkv * T + t) * G * kHeadDim;
   for (int h = wave; h < G; h += kThreads / 64) {
+    float2 sv = make_float2(0.0f, 0.0f);
+    if (a.direct) sv = wait_stats(mail + h * kRowTMax, Tb, lane, a.err);
+    else if (lane < Tb) sv = ld_coherent(a.stats + (row0 + h) * T + lane);
+    float *oh = offl[h], *ah = offl[h] + (T + 1);
+    head_offsets_from([&](int) { return sv; }, Tb, lane, oh, ah);  // Tb <= 64: split t in lane t
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    const HeadClaim c{oh[t], t == Tb - 1 ? kInf : oh[t + 1], oh[Tb], ah[t]};
     float acc[8];
     const float *uh = a.u + (row0 + h) * upr;
     if (G > 4) {  // two heads per wave: the head's own uniforms, from global memory
       ureg[0] = MODE == kSys ? uh[0] : 0.0f;
     }
-    row_head_value<E, PAGED, MODE>(a, hc[h], uh, ureg, G <= 4, P + h * pitch, nrows, start, b,
-                                   kvh, row0 + h, keyl[wave], cntl[wave], acc);
+    row_head_value<E, PAGED, MODE>(a, c, uh, ureg, G <= 4, P + h * pitch, nrows, start, b, kvh,
+                                   row0 + h, keyl[wave], cntl[wave], acc);
     if (lane < 16) {
       float2 *d = reinterpret_cast<float2 *>(part + h * kHeadDim + lane * 8);
 #pragma unroll
@@ -224,11 +282,17 @@ __attribute__((amdgpu_waves_per_eu(row_waves<E, G, PAGED>()))) void k_row_sample
     }
   }
 
-  // 3. arrive again; the row's last arrival merges O = (1/S) sum_t o_t
-  const int rank = row_arrive(sync, base + (unsigned long long)Tb, &rank_lds);
+  // 3. last arrival of the split; the row's last one merges
+  // O = (1/S) sum_t o_t, and (direct) empties the mailbox
+  const unsigned long long arrivals = a.direct ? Tb : 2ull * Tb;  // of this call
+  const int rank = row_arrive(sync, base + arrivals - Tb, &rank_lds);
   if (rank != Tb - 1) return;
   if (tid == 0)
-    __hip_atomic_store(sync + 1, base + 2ull * Tb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(sync + 1, base + arrivals, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (a.direct)
+    for (int i = tid; i < G * Tb; i += kThreads)
+      __hip_atomic_store(mail + (i / Tb) * kRowTMax + i % Tb, 0ull, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
   const float *part_row = a.part + (int64_t)rowkv * T * G * kHeadDim;
   const float scale = a.invS * kv_scales<E>(a.kv, b, kvh, a.Hkv).y;  // FP8 cache: V scale
   if constexpr (G == 4) {
@@ -245,6 +309,7 @@ hipError_t launch_rows_e(const Plan &p, const KvView &kv, const void *q, float s
                          hipStream_t st) {
   if (p.T > kRowTMax || (mode != kSys && mode != kStrat)) return hipErrorInvalidValue;
   FusedArgs args = make_args(p, kv, q, out, scale_log2, ws);
+  args.direct = (int64_t)p.B * p.Hkv * p.T <= kDirectPollMax;
   args.u = u;
   args.idx_out = idx_out;
   return with_g_paged(p.G, kv.bt != nullptr, [&](auto gc, auto paged) -> hipError_t {
