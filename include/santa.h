@@ -311,10 +311,9 @@ santa_status_t santa_stream_read(const void *buf, size_t bytes, uint32_t *sink, 
  * choose by problem size.
  *   SANTA_PATH_AUTO        by measured speed: systematic and stratified steps
  *                          with at most 64 splits per row take the scheduled
- *                          path for S <= 1024 on grids (KV rows x splits) above
- *                          256 workgroups and for S <= 512 below that, paged
- *                          caches up to 8192 workgroups, FP8 caches up to
- *                          2048; other sampled steps whose rows fit one
+ *                          path for S <= 1024 (paged caches up to 8192
+ *                          workgroups, KV rows x splits, FP8 caches up to
+ *                          2048); other sampled steps whose rows fit one
  *                          resident round of about 1024 workgroups take one
  *                          persistent launch, larger ones the two-launch path;
  *   SANTA_PATH_ONE_LAUNCH  sampled steps: one persistent launch (k_fused_sampled);

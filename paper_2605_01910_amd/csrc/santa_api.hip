@@ -169,14 +169,13 @@ santa::Plan make_plan(const santa_shape_t *sh, const santa_kv_t *kv, int S, int 
     // systematic and stratified steps take the scheduled path (its row offsets
     // live in LDS, so at most kRowTMax splits per row) when asked for, and by
     // default where it measured faster than both other paths: budgets up to
-    // 1024 on grids of more than 256 workgroups, budgets up to 512 below that;
-    // paged caches up to 8192 workgroups and FP8 caches up to 2048 (beyond
-    // those the two-launch path was faster)
+    // 1024; paged caches up to 8192 workgroups and FP8 caches up to 2048
+    // (beyond those the two-launch path was faster)
     const bool rows_ok = (kind == SANTA_KIND_SYSTEMATIC || kind == SANTA_KIND_STRATIFIED) &&
                          p.T <= santa::kRowTMax;
     const int64_t grid = (int64_t)p.B * p.Hkv * p.T;
-    const bool rows_auto = rows_ok && S <= 1024 && (grid > 256 || S <= 512) &&
-                           (!kv->block_table || grid <= 8192) && (p.elem != 2 || grid <= 2048);
+    const bool rows_auto = rows_ok && S <= 1024 && (!kv->block_table || grid <= 8192) &&
+                           (p.elem != 2 || grid <= 2048);
     p.rows = g_opts.path == SANTA_PATH_SCHEDULED ? rows_ok
                                                  : (g_opts.path == SANTA_PATH_AUTO && rows_auto);
     // other sampled steps whose rows do not fit in one resident round of about

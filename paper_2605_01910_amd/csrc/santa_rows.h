@@ -51,6 +51,37 @@ __device__ __forceinline__ float2 wait_stats(const unsigned long long *w, int Tb
   return make_float2(__uint_as_float((unsigned)v), __uint_as_float((unsigned)(v >> 32)));
 }
 
+// merge_group4 for a workgroup with Tb * 4 * 128 floats of free LDS at lds
+// (16-byte aligned): every partial is copied straight into LDS
+// (global_load_lds, agent-coherent like ld_coherent; 1 KiB, half a split, per
+// wave instruction), so the merge takes one round trip, and then summed in
+// split order, as merge_group4 does.
+template <typename OE>
+__device__ __forceinline__ void merge_group4_lds(const float *part_row, int Tb, float scale,
+                                                 float *lds, OE *out_row0) {
+  constexpr int G = 4, SPL = G * kHeadDim;  // floats per split
+  constexpr int kCoherent = 16;               // sc1, as agent-scope loads
+  typedef __attribute__((address_space(3))) void *lds_ptr;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const char *src = reinterpret_cast<const char *>(part_row);
+  for (int k = wave; k < 2 * Tb; k += kThreads / 64)
+    __builtin_amdgcn_global_load_lds(src + k * 1024 + lane * 16,
+                                     (lds_ptr)(reinterpret_cast<char *>(lds) + k * 1024), 16, 0,
+                                     kCoherent);
+  wait_stores();  // vmcnt(0): this wave's copies have landed in LDS
+  __syncthreads();
+  const int h = wave, o = lane * 2;
+  const float2 *l2 = reinterpret_cast<const float2 *>(lds + h * kHeadDim + o);
+  float sx = 0.0f, sy = 0.0f;
+  for (int t = 0; t < Tb; ++t) {
+    const float2 w = l2[t * (SPL / 2)];
+    sx += w.x;
+    sy += w.y;
+  }
+  store_out(out_row0 + h * kHeadDim + o, sx * scale);
+  store_out(out_row0 + h * kHeadDim + o + 1, sy * scale);
+}
+
 // Value stage of head h in split t, by one wave, for sorted thresholds with a
 // closed-form count (kSys, kStrat): the split claims r in [N(lo), N(hi)),
 // N(y) = #{r : tau_r < y}.  ureg: the head's uniforms fetched before the row
@@ -296,7 +327,8 @@ __attribute__((amdgpu_waves_per_eu(row_waves<E, G, PAGED>()))) void k_row_sample
   const float *part_row = a.part + (int64_t)rowkv * T * G * kHeadDim;
   const float scale = a.invS * kv_scales<E>(a.kv, b, kvh, a.Hkv).y;  // FP8 cache: V scale
   if constexpr (G == 4) {
-    merge_group4<16>(part_row, Tb, scale, out + row0 * kHeadDim);
+    if (a.direct) merge_group4_lds(part_row, Tb, scale, P, out + row0 * kHeadDim);
+    else merge_group4<16>(part_row, Tb, scale, out + row0 * kHeadDim);
   } else {
     for (int h = 0; h < G; ++h)
       merge_head<QE<E>, G>(part_row, h, Tb, nullptr, nullptr, scale, P, out + (row0 + h) * kHeadDim);
@@ -322,7 +354,10 @@ hipError_t launch_rows_e(const Plan &p, const KvView &kv, const void *q, float s
                        : (ap ? reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kSys, true>)
                              : reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kSys>));
     void *params[] = {&args};
-    const size_t lds = (size_t)G * kSplitMax * 4;
+    // direct grids of G = 4 merge through LDS (merge_group4_lds: T partials,
+    // at most 128 KiB, within the 160 KiB of a CU)
+    const size_t lds = std::max((size_t)G * kSplitMax * 4,
+                                args.direct && G == 4 ? (size_t)p.T * G * kHeadDim * 4 : 0);
     const CallTimer tm = call_timer();
     return hipExtLaunchKernel(fn, dim3(p.B * p.Hkv * p.T), dim3(kThreads), params, lds, st,
                               tm.start, tm.stop, 0);

@@ -138,9 +138,8 @@ def _plan(shape, kv, Sn, kind, path="auto", splits=0):
 
 def test_path_choice_by_size_cache_and_kind():
     """The host picks a path without launching anything: the scheduled path
-    for systematic and stratified steps where it measured fastest (S <= 1024
-    above 256 workgroups, S <= 512 below; paged caches up to 8192 workgroups,
-    FP8 up to 2048), else the persistent launch within one resident round and
+    for systematic and stratified steps where it measured fastest (S <= 1024;
+    paged caches up to 8192 workgroups, FP8 up to 2048), else the persistent launch within one resident round and
     the two-launch path beyond it; i.i.d. and Bernoulli steps never take the
     scheduled path, nor does a row that needs more than 64 splits."""
     sysk, strat, iid = S.SANTA_KIND_SYSTEMATIC, S.SANTA_KIND_STRATIFIED, S.SANTA_KIND_IID
@@ -148,7 +147,8 @@ def test_path_choice_by_size_cache_and_kind():
     p1 = _plan(_shape(B=1), _kv(), 256, strat)
     assert (p1["path"], p1["kernels"], p1["splits"]) == (S.SANTA_PATH_SCHEDULED, rows, 32)
     assert _plan(_shape(B=1), _kv(), 512, sysk)["kernels"] == rows
-    assert _plan(_shape(B=1), _kv(), 1024, sysk)["kernels"] == one
+    assert _plan(_shape(B=1), _kv(), 1024, sysk)["kernels"] == rows
+    assert _plan(_shape(B=1), _kv(), 1024, strat)["kernels"] == rows
     assert _plan(_shape(B=1), _kv(), 2048, strat)["kernels"] == one
     for B in (2, 16):
         for kind in (sysk, strat):
