@@ -204,9 +204,10 @@ def test_scheduled_sampled_parity(case):
 
 
 def test_scheduled_many_rows_reuses_counters():
-    """The scheduled path over far more workgroups than are resident at once:
-    ragged rows (one empty), G in {4, 8}, and three calls in a row on one
-    workspace (the row counters move on by two arrivals per split)."""
+    """The scheduled path over far more workgroups than are resident at once
+    (its counter barrier): ragged rows (one empty), G in {4, 8}, and three
+    calls in a row on one workspace (the row counters move on by two
+    arrivals per split)."""
     lens = [(37 * i * i + 11 * i) % 9000 for i in range(24)]
     lens[3] = 0
     lens[7] = 9000
@@ -222,6 +223,40 @@ def test_scheduled_many_rows_reuses_counters():
             for _ in range(3):
                 out, idx, _ = run(w, dw=dw, ws=ws)
                 check_sampled(w, out, idx)
+        assert S.workspace_error(ws) == 0
+
+
+def test_scheduled_direct_barrier_many_splits_and_mode_changes():
+    """The scheduled path's direct row barrier (grids of at most 256
+    workgroups: statistics mailbox, LDS merge) at 64 splits per row with G in
+    {4, 8}, ragged rows, three calls in a row on one workspace, and calls of
+    the counter barrier (a larger grid) interleaved on the same workspace: the
+    mailbox must be empty again after every call and the counters consistent
+    across the two arrival counts."""
+    cases = [dict(B=1, Hq=16, Hkv=4, n=65536, S=256),
+             dict(B=1, Hq=32, Hkv=4, n=65536, S=256),
+             dict(B=2, Hq=8, Hkv=2, n=65536, S=128, ctx_len=[65536, 23001])]
+    big = make_workload(3, B=24, n=9000, kind="systematic", S=128, seed=58)
+    with S.options("rows"):
+        dwb = DeviceWorkload(big)
+        calls = [(big, dwb, S.SANTA_KIND_SYSTEMATIC)]
+        for over in cases:
+            w = make_workload(3, kind="stratified", seed=57, **over)
+            calls.append((w, DeviceWorkload(w), S.SANTA_KIND_STRATIFIED))
+        # one workspace, sized for the call that needs the most
+        sizes = [S.santa_workspace_size(d.shape, d.kv, w.S, k) for w, d, k in calls]
+        w0, d0, k0 = calls[sizes.index(max(sizes))]
+        ws = S.alloc_workspace(d0.shape, d0.kv, w0.S, k0)
+        for w, dw, kind in calls[1:]:
+            plan = S.santa_plan_info(dw.shape, dw.kv, w.S, kind)
+            assert plan["kernels"] == "k_row_sampled" and plan["splits"] == 64, plan
+            log(f"[scheduled direct] B={w.B} G={w.G} n={w.n_max} T={plan['splits']}")
+            for _ in range(3):
+                out, idx, _ = run(w, dw=dw, ws=ws)
+                check_sampled(w, out, idx)
+            log(f"[scheduled counter] B={big.B} G={big.G} n={big.n_max}")
+            out, idx, _ = run(big, dw=dwb, ws=ws)
+            check_sampled(big, out, idx)
         assert S.workspace_error(ws) == 0
 
 
