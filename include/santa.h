@@ -313,7 +313,9 @@ santa_status_t santa_stream_read(const void *buf, size_t bytes, uint32_t *sink, 
  *                          with at most 64 splits per row take the scheduled
  *                          path for S <= 1024 (paged caches up to 8192
  *                          workgroups, KV rows x splits, FP8 caches up to
- *                          2048); other sampled steps whose rows fit one
+ *                          2048), i.i.d. steps too for S <= 256 at
+ *                          num_q_heads / num_kv_heads <= 4; other sampled
+ *                          steps whose rows fit one
  *                          resident round of about 1024 workgroups take one
  *                          persistent launch, larger ones the two-launch path;
  *   SANTA_PATH_ONE_LAUNCH  sampled steps: one persistent launch (k_fused_sampled);
@@ -322,7 +324,9 @@ santa_status_t santa_stream_read(const void *buf, size_t bytes, uint32_t *sink, 
  *   SANTA_PATH_MULTI       every step: the multi-kernel variant (score/CDF,
  *                          offsets, sampling and merge kernels);
  *   SANTA_PATH_SCHEDULED   systematic and stratified steps with at most 64
- *                          splits per row: one hardware-scheduled launch, a
+ *                          splits per row, and i.i.d. steps among them with
+ *                          S <= 256 at num_q_heads / num_kv_heads <= 4: one
+ *                          hardware-scheduled launch, a
  *                          workgroup per split that keeps its CDF in LDS across
  *                          a row barrier (k_row_sampled); other sampled steps
  *                          as under AUTO.

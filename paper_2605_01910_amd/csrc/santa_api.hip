@@ -166,12 +166,14 @@ santa::Plan make_plan(const santa_shape_t *sh, const santa_kv_t *kv, int S, int 
     p.Ls = (int)(((p.n_k + p.T - 1) / p.T + 63) & ~63);
     const bool sampled = kind != SANTA_KIND_DENSE;
     const bool big = (int64_t)p.B * p.Hkv * p.T > 1024;  // workgroups beyond one resident round
-    // systematic and stratified steps take the scheduled path (its row offsets
-    // live in LDS, so at most kRowTMax splits per row) when asked for, and by
-    // default where it measured faster than both other paths: budgets up to
-    // 1024; paged caches up to 8192 workgroups and FP8 caches up to 2048
-    // (beyond those the two-launch path was faster)
-    const bool rows_ok = (kind == SANTA_KIND_SYSTEMATIC || kind == SANTA_KIND_STRATIFIED) &&
+    // systematic and stratified steps, and i.i.d. steps with S <= 256 at G <= 4
+    // (their sorted thresholds held in registers), take the scheduled path
+    // (its row offsets live in LDS, so at most kRowTMax splits per row) when
+    // asked for, and by default where it measured faster than both other
+    // paths: budgets up to 1024; paged caches up to 8192 workgroups and FP8
+    // caches up to 2048 (beyond those the two-launch path was faster)
+    const bool rows_ok = (kind == SANTA_KIND_SYSTEMATIC || kind == SANTA_KIND_STRATIFIED ||
+                          (kind == SANTA_KIND_IID && p.G <= 4 && S <= 256)) &&
                          p.T <= santa::kRowTMax;
     const int64_t grid = (int64_t)p.B * p.Hkv * p.T;
     const bool rows_auto = rows_ok && S <= 1024 && (!kv->block_table || grid <= 8192) &&

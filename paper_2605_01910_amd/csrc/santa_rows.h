@@ -1,5 +1,5 @@
-// santa_rows.h -- the scheduled sampled step (k_row_sampled): systematic and
-// stratified SANTA for batches whose rows do not fit one resident round.  One
+// santa_rows.h -- the scheduled sampled step (k_row_sampled): systematic,
+// stratified and (S <= 256, G <= 4) i.i.d. SANTA.  One
 // workgroup per (row, split), scheduled by the hardware like the two-launch
 // key stream, but the split's CDF stays in LDS: the split publishes its
 // statistics, waits at its row's barrier, claims its thresholds, gathers
@@ -51,6 +51,38 @@ __device__ __forceinline__ float2 wait_stats(const unsigned long long *w, int Tb
   return make_float2(__uint_as_float((unsigned)v), __uint_as_float((unsigned)(v >> 32)));
 }
 
+// Sorted thresholds of the i.i.d. estimator (S <= 256) for one head, by one
+// wave, in the register layout of the stratified uniforms: on entry ureg[k]
+// of lane l holds u_r, r = l + 64 k < S, and uS the row's last uniform u_S; on
+// return ureg[k] holds T_r = C_r / C_S with E_i = -log2(1 - u_i) and C_m =
+// sum_{i <= m} E_i in double (the normalised partial sums of S + 1
+// exponentials are the order statistics of S uniforms; the ln 2 factor
+// cancels).  Each register's 64 partial sums come from a wave scan made
+// non-decreasing by a prefix max and are offset by the sum of the earlier
+// registers, so T is non-decreasing in r and at most 1.
+__device__ __forceinline__ void iid_thresholds_regs(float (&ureg)[4], float uS, int S, int lane) {
+  double carry = 0.0, c[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int r = lane + 64 * k;
+    double incl = r < S ? -(double)__builtin_amdgcn_logf(1.0f - ureg[k]) : 0.0;
+    for (int d = 1; d < 64; d <<= 1) {
+      const double y = __shfl_up(incl, d);
+      incl += lane >= d ? y : 0.0;
+    }
+    for (int d = 1; d < 64; d <<= 1) {
+      const double y = __shfl_up(incl, d);
+      incl = lane >= d ? fmax(incl, y) : incl;
+    }
+    c[k] = carry + incl;
+    carry += __shfl(incl, 63);
+  }
+  const double total = carry - (double)__builtin_amdgcn_logf(1.0f - uS);
+  const double inv = total > 0.0 ? 1.0 / total : 0.0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) ureg[k] = (float)(c[k] * inv);
+}
+
 // merge_group4 for a workgroup with Tb * 4 * 128 floats of free LDS at lds
 // (16-byte aligned): every partial is copied straight into LDS
 // (global_load_lds, agent-coherent like ld_coherent; 1 KiB, half a split, per
@@ -82,14 +114,14 @@ __device__ __forceinline__ void merge_group4_lds(const float *part_row, int Tb, 
   store_out(out_row0 + h * kHeadDim + o + 1, sy * scale);
 }
 
-// Value stage of head h in split t, by one wave, for sorted thresholds with a
-// closed-form count (kSys, kStrat): the split claims r in [N(lo), N(hi)),
-// N(y) = #{r : tau_r < y}.  ureg: the head's uniforms fetched before the row
-// barrier -- kSys: u in ureg[0]; kStrat with S <= 256 and staged (one head
-// per wave): u_r in ureg[r / 64] of lane r % 64, so every lane counts its own
-// thresholds and the claims read u_r with lane shuffles; otherwise lanes 0
-// and 1 evaluate N(lo) and N(hi) in closed form (count_below) and u_r comes
-// from global memory.  The claims are taken 64 at a time: lane l inverts
+// Value stage of head h in split t, by one wave, for sorted thresholds: the
+// split claims r in [N(lo), N(hi)), N(y) = #{r : tau_r < y}.  ureg: the
+// head's uniforms fetched before the row barrier -- kSys: u in ureg[0];
+// kStrat with S <= 256 and staged (one head per wave): u_r in ureg[r / 64]
+// of lane r % 64, so every lane counts its own thresholds and the claims
+// read u_r with lane shuffles; kIid (always so held): the sorted threshold
+// T_r in that place, tau_r = T_r Z; otherwise lanes 0 and 1 evaluate N(lo)
+// and N(hi) in closed form (count_below) and u_r comes from global memory.  The claims are taken 64 at a time: lane l inverts
 // tau_r on the split's LDS CDF (the key #{j : a P_j <= tau_r - lo}, App. A,
 // clamped to the split).  The chosen keys are non-decreasing in r, so equal
 // keys form runs; the runs of successive chunks go to a list of (key, count)
@@ -109,17 +141,22 @@ __device__ __forceinline__ void row_head_value(const FusedArgs &a, const HeadCla
   const E *V = static_cast<const E *>(a.kv.v);
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc[i] = 0.0f;
-  const bool regs = MODE == kSys || (staged && a.S <= 4 * 64);
+  // kIid: always in registers (S <= 256, one head per wave)
+  const bool regs = MODE == kSys || MODE == kIid || (staged && a.S <= 4 * 64);
+  // tau_r from the register value v (u_r, or T_r for kIid)
+  auto tau_reg = [&](int r, float v) {
+    return MODE == kIid ? v * c.Z : threshold(r, v, a.invS, c.Z);
+  };
   int rlo = 0, rhi = 0;
-  if (MODE == kStrat && regs) {  // N(lo), N(hi) counted over the uniforms in registers
+  if (MODE == kIid || (MODE == kStrat && regs)) {  // N(lo), N(hi) over the registers
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int r = lane + 64 * k;
-      const float tau = r < a.S ? threshold(r, ureg[k], a.invS, c.Z) : kInf;
+      const float tau = r < a.S ? tau_reg(r, ureg[k]) : kInf;
       rlo += __popcll(__ballot(tau < c.lo));
       rhi += __popcll(__ballot(tau < c.hi));
     }
-  } else {
+  } else if constexpr (MODE != kIid) {
     int n = 0;
     if (lane < 2)
       n = count_below<MODE>(uh, MODE == kSys ? ureg[0] : 0.0f, a.S, a.invS, c.Z,
@@ -162,14 +199,16 @@ __device__ __forceinline__ void row_head_value(const FusedArgs &a, const HeadCla
     int j = -1;
     if (!done) {
       float ur = ureg[0];
-      if (MODE == kStrat && regs) {  // u_r from lane r % 64 (every lane takes part)
+      if (MODE != kSys && regs) {  // u_r (T_r) from lane r % 64 (every lane takes part)
         const int src = r & 63, k = (r >> 6) & 3;
         const float v0 = __shfl(ureg[0], src), v1 = __shfl(ureg[1], src);
         const float v2 = __shfl(ureg[2], src), v3 = __shfl(ureg[3], src);
         ur = k == 0 ? v0 : (k == 1 ? v1 : (k == 2 ? v2 : v3));
       }
       if (r < rhi) {
-        const float tau = threshold(r, (MODE == kStrat && !regs) ? uh[r] : ur, a.invS, c.Z);
+        const float tau = MODE == kIid ? ur * c.Z
+                                       : threshold(r, (MODE == kStrat && !regs) ? uh[r] : ur,
+                                                   a.invS, c.Z);
         const int pos = lds_cdf_count(Ph, nrows, c.a, tau - c.lo);
         j = pos < nrows ? pos : nrows - 1;
         if (a.idx_out) a.idx_out[rowq * a.S + r] = start + j;
@@ -213,7 +252,8 @@ __device__ __forceinline__ void row_head_value(const FusedArgs &a, const HeadCla
 template <typename E, int G, bool PAGED, int MODE, bool APPEND = false>
 __global__ __launch_bounds__(kThreads)
 __attribute__((amdgpu_waves_per_eu(row_waves<E, G, PAGED>()))) void k_row_sampled(FusedArgs a) {
-  static_assert(MODE == kSys || MODE == kStrat, "closed-form threshold counts");
+  static_assert(MODE == kSys || MODE == kStrat || (MODE == kIid && G <= 4),
+                "thresholds with a closed-form count or in registers");
   extern __shared__ __attribute__((aligned(16))) float dyn[];
   constexpr int pitch = kSplitMax;
   float *P = dyn;  // [G][pitch]: scores, then the split CDF; merge scratch at the end
@@ -273,8 +313,9 @@ __attribute__((amdgpu_waves_per_eu(row_waves<E, G, PAGED>()))) void k_row_sample
     if (tid == 0)
       arrived = __hip_atomic_fetch_add(sync, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1;
   }
-  // the uniforms of head `wave` (G <= 4), fetched while the row arrives
-  const int upr = MODE == kStrat ? a.S : 1;  // uniforms per head
+  // the uniforms of head `wave` (G <= 4), fetched while the row arrives;
+  // i.i.d.: turned into the head's sorted thresholds
+  const int upr = MODE == kStrat ? a.S : (MODE == kIid ? a.S + 1 : 1);  // uniforms per head
   float ureg[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   if (G <= 4 && wave < G) {
     const float *uw = a.u + (row0 + wave) * upr;
@@ -283,6 +324,7 @@ __attribute__((amdgpu_waves_per_eu(row_waves<E, G, PAGED>()))) void k_row_sample
     } else if (a.S <= 4 * 64) {
 #pragma unroll
       for (int k = 0; k < 4; ++k) ureg[k] = lane + 64 * k < a.S ? uw[lane + 64 * k] : 0.0f;
+      if (MODE == kIid) iid_thresholds_regs(ureg, uw[a.S], a.S, lane);
     }
   }
   // 2. the row barrier, then per head, by wave h: global offsets, its claims
@@ -339,7 +381,9 @@ template <typename E>
 hipError_t launch_rows_e(const Plan &p, const KvView &kv, const void *q, float scale_log2,
                          int mode, const float *u, int32_t *idx_out, void *out, char *ws,
                          hipStream_t st) {
-  if (p.T > kRowTMax || (mode != kSys && mode != kStrat)) return hipErrorInvalidValue;
+  if (p.T > kRowTMax || (mode != kSys && mode != kStrat && mode != kIid) ||
+      (mode == kIid && (p.G > 4 || p.S > 4 * 64)))
+    return hipErrorInvalidValue;
   FusedArgs args = make_args(p, kv, q, out, scale_log2, ws);
   args.direct = (int64_t)p.B * p.Hkv * p.T <= kDirectPollMax;
   args.u = u;
@@ -348,11 +392,18 @@ hipError_t launch_rows_e(const Plan &p, const KvView &kv, const void *q, float s
     constexpr int G = decltype(gc)::value;
     constexpr bool PG = decltype(paged)::value;
     const bool ap = kv.k_new != nullptr;
-    const void *fn =
-        mode == kStrat ? (ap ? reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kStrat, true>)
-                             : reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kStrat>))
-                       : (ap ? reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kSys, true>)
-                             : reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kSys>));
+    const void *fn = nullptr;
+    if (mode == kStrat)
+      fn = ap ? reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kStrat, true>)
+              : reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kStrat>);
+    else if (mode == kSys)
+      fn = ap ? reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kSys, true>)
+              : reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kSys>);
+    if constexpr (G <= 4)
+      if (mode == kIid)
+        fn = ap ? reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kIid, true>)
+                : reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kIid>);
+    if (!fn) return hipErrorInvalidValue;
     void *params[] = {&args};
     // direct grids of G = 4 merge through LDS (merge_group4_lds: T partials,
     // at most 128 KiB, within the 160 KiB of a CU)

@@ -1,6 +1,8 @@
 """GPU parity of santa_decode_iid (SANTA with i.i.d. draws, Sec. 2, Eq.
 "stochastic-add-only-attn"; thresholds by exponential spacings) against the
-CPU oracle through the C ABI, on both sampled launch paths: indices
+CPU oracle through the C ABI, on the three sampled launch paths (the
+scheduled one takes S <= 256 at G <= 4, holding the sorted thresholds in
+registers; G = 8 falls back to the one-launch path there): indices
 bit-exact up to the 1e-5 band, outputs within 2e-2 of the oracle's gather of
 the GPU's own indices.  Cases cover ragged and empty rows, S = 1, G = 8,
 the paged cache, and the full Llama-3.1-8B 32k shape."""
@@ -24,7 +26,7 @@ CASES = {
 }
 
 
-@pytest.mark.parametrize("path", ["one", "two"])
+@pytest.mark.parametrize("path", ["one", "two", "rows"])
 @pytest.mark.parametrize("case", sorted(CASES))
 def test_iid_parity(case, path):
     cfg, over = CASES[case]
@@ -44,8 +46,10 @@ def test_iid_repeat_calls_are_bitwise_identical():
 
 
 @pytest.mark.timeout(300)
-def test_iid_full_size_llama8b_32k():
+@pytest.mark.parametrize("path", ["one", "rows"])
+def test_iid_full_size_llama8b_32k(path):
     w = make_workload(2, seed=0, kind="iid", S=256)
-    log(f"[iid full] n={w.n_max} S={w.S}")
-    out, idx, _ = run(w, "iid")
+    log(f"[iid full/{path}] n={w.n_max} S={w.S}")
+    with S.options(path):
+        out, idx, _ = run(w, "iid")
     log(f"  {check_sampled(w, out, idx, 'iid')}")
