@@ -126,6 +126,15 @@ santa_status_t check_kv(const santa_kv_t *kv, const santa_shape_t *sh, bool need
   return SANTA_OK;
 }
 
+// The flash step takes the scheduled kernel (k_row_flash: no barrier before
+// the value stage, one arrival per split) under the automatic and scheduled
+// paths for G <= 4 and at most kRowTMax splits per row; k_fused_dense's flash
+// mode otherwise.
+static bool flash_rows(const santa::Plan &p) {
+  return p.fused && (g_opts.path == SANTA_PATH_AUTO || g_opts.path == SANTA_PATH_SCHEDULED) &&
+         p.G <= 4 && p.T <= santa::kRowTMax;
+}
+
 santa::Plan make_plan(const santa_shape_t *sh, const santa_kv_t *kv, int S, int kind) {
   santa::Plan p{};
   p.B = sh->batch;
@@ -155,8 +164,10 @@ santa::Plan make_plan(const santa_shape_t *sh, const santa_kv_t *kv, int S, int 
   p.off_err = take(santa::kErrBytes);
   p.off_sync = take((size_t)santa::kSyncRowsMax * santa::kSyncStride * 4);
   const bool fused = g_opts.path != SANTA_PATH_MULTI;
-  const bool small_budget = (kind == SANTA_KIND_SYSTEMATIC || kind == SANTA_KIND_STRATIFIED ||
-                             kind == SANTA_KIND_IID) && S <= 1024;
+  // (kind FLASH: the scheduled flash kernel's plan, the dense layout with the
+  // small budget's split count, which is never more than the dense step's)
+  const bool small_budget = ((kind == SANTA_KIND_SYSTEMATIC || kind == SANTA_KIND_STRATIFIED ||
+                              kind == SANTA_KIND_IID) && S <= 1024) || kind == SANTA_KIND_FLASH;
   const int Tf = fused_splits((int64_t)p.B * p.Hkv, p.n_k, small_budget ? 256 : 512);
   if (kind != SANTA_KIND_BERNOULLI && fused && Tf <= santa::kMaxSplits &&
       (int64_t)p.B * p.Hkv <= santa::kSyncRowsMax) {
@@ -164,7 +175,7 @@ santa::Plan make_plan(const santa_shape_t *sh, const santa_kv_t *kv, int S, int 
     p.T = Tf;
     // rows use ceil(L_b / T) keys per split rounded up to 64; Ls is the longest
     p.Ls = (int)(((p.n_k + p.T - 1) / p.T + 63) & ~63);
-    const bool sampled = kind != SANTA_KIND_DENSE;
+    const bool sampled = kind != SANTA_KIND_DENSE && kind != SANTA_KIND_FLASH;
     const bool big = (int64_t)p.B * p.Hkv * p.T > 1024;  // workgroups beyond one resident round
     // systematic and stratified steps, and i.i.d. steps with S <= 256 at G <= 4
     // (their sorted thresholds held in registers), take the scheduled path
@@ -496,7 +507,9 @@ santa_status_t santa_decode_flash(const void *q, const santa_kv_t *kv, const san
     return fail(SANTA_ERR_INVALID_ARG, "tile must be a power of two in [16, 1024]");
   if (S_tile < 1 || S_tile > 4096) return fail(SANTA_ERR_INVALID_ARG, "S_tile must be in [1, 4096]");
   if (!u) return fail(SANTA_ERR_INVALID_ARG, "u is NULL");
-  const santa::Plan p = make_plan(shape, kv, 0, SANTA_KIND_DENSE);
+  santa::Plan p = make_plan(shape, kv, 0, SANTA_KIND_DENSE);
+  const bool rows = flash_rows(p);
+  if (rows) p = make_plan(shape, kv, 0, SANTA_KIND_FLASH);
   s = check_ws(p, ws, ws_bytes);
   if (s == SANTA_OK && kv->k_new && !p.fused)
     s = fail(SANTA_ERR_UNSUPPORTED, "the fused append (k_new, v_new) needs the fused path");
@@ -506,7 +519,7 @@ santa_status_t santa_decode_flash(const void *q, const santa_kv_t *kv, const san
   if (!p.fused) return fail(SANTA_ERR_UNSUPPORTED, "the flash step needs the fused launch layout");
   return hip_status(santa::launch_fused_flash(p, make_view(kv), q, log2_scale(scale), ilog2(tile),
                                               S_tile, u, idx_out, out, static_cast<char *>(ws),
-                                              static_cast<hipStream_t>(stream)));
+                                              static_cast<hipStream_t>(stream), rows));
 }
 
 santa_status_t santa_stream_read(const void *buf, size_t bytes, uint32_t *sink, void *stream) {
@@ -553,7 +566,9 @@ santa_status_t santa_plan_info(const santa_shape_t *shape, const santa_kv_t *kv,
   const int32_t plan_kind = kind == SANTA_KIND_FLASH ? SANTA_KIND_DENSE : kind;
   if (plan_kind != SANTA_KIND_DENSE && (S < 1 || S > (1 << 24)))
     return fail(SANTA_ERR_INVALID_ARG, "S must be in [1, 2^24]");
-  const santa::Plan p = make_plan(shape, kv, S, plan_kind);
+  santa::Plan p = make_plan(shape, kv, S, plan_kind);
+  const bool frows = kind == SANTA_KIND_FLASH && flash_rows(p);
+  if (frows) p = make_plan(shape, kv, S, SANTA_KIND_FLASH);
   info->splits = p.T;
   info->split_len = p.Ls;
   info->workspace = p.total;
@@ -564,6 +579,9 @@ santa_status_t santa_plan_info(const santa_shape_t *shape, const santa_kv_t *kv,
   } else if (kind == SANTA_KIND_BERNOULLI) {
     info->path = SANTA_PATH_TWO_LAUNCH;
     info->kernels = "k_bern_stream + k_value_heads";
+  } else if (frows) {
+    info->path = SANTA_PATH_SCHEDULED;
+    info->kernels = "k_row_flash";
   } else if (kind == SANTA_KIND_DENSE || kind == SANTA_KIND_FLASH) {
     info->path = SANTA_PATH_ONE_LAUNCH;
     info->kernels = kind == SANTA_KIND_DENSE ? "k_fused_dense" : "k_fused_dense (flash mode)";

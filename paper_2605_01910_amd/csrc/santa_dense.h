@@ -9,76 +9,6 @@ namespace santa {
 // ---------------------------------------------------------------------------
 // S2ANTA-flash value stage (Sec. 3.3; App. "S2ANTA-Flash Pseudocode", Kernel 1)
 // ---------------------------------------------------------------------------
-// Tile-local CDFs of one head's split, computed by one wave in place: the
-// split (nrows <= kSplitMax scores in s, log2 units) holds tiles of 2^tl2 keys
-// (16 <= tile; the split starts on a tile boundary).  For tile tau: m_tau =
-// max s, P_j = sum_{i <= j in tau} exp2(s_i - m_tau), written over s[j];
-// tm[tau] = m_tau and tl[tau] = P_last.  Lane l owns keys 16l..16l+15 and a
-// tile spans 2^tl2 / 16 aligned lanes, so the tile max is a butterfly and the
-// tile prefix a segmented scan over those lanes, made non-decreasing by a
-// segmented prefix max (fixed order: equal inputs give equal CDFs).
-__device__ __forceinline__ void wave_tile_cdf(float *s, int nrows, int lane, int tl2, float *tm,
-                                              float *tl) {
-  constexpr int CH = kSplitMax / 64;
-  const int j0 = lane * CH;
-  const int seg = (1 << tl2) / CH;  // lanes per tile, 1 .. 64
-  const int pos = lane & (seg - 1);
-  float x[CH];
-#pragma unroll
-  for (int i = 0; i < CH / 4; ++i) {
-    const float4 v = reinterpret_cast<const float4 *>(s + j0)[i];
-    x[4 * i] = v.x;
-    x[4 * i + 1] = v.y;
-    x[4 * i + 2] = v.z;
-    x[4 * i + 3] = v.w;
-  }
-  float m = -kInf;
-#pragma unroll
-  for (int i = 0; i < CH; ++i) m = (j0 + i < nrows) ? fmaxf(m, x[i]) : m;
-  for (int d = 1; d < seg; d <<= 1) m = fmaxf(m, __shfl_xor(m, d));
-  float acc = 0.0f;
-#pragma unroll
-  for (int i = 0; i < CH; ++i) {
-    acc += (j0 + i < nrows) ? fast_exp2(x[i] - m) : 0.0f;
-    x[i] = acc;
-  }
-  float incl = acc;
-  for (int d = 1; d < seg; d <<= 1) {
-    const float y = __shfl_up(incl, d);
-    incl += pos >= d ? y : 0.0f;
-  }
-  for (int d = 1; d < seg; d <<= 1) {
-    const float y = __shfl_up(incl, d);
-    incl = pos >= d ? fmaxf(incl, y) : incl;
-  }
-  const float prev = __shfl_up(incl, 1);
-  const float base = pos == 0 ? 0.0f : prev;
-  if (j0 < nrows) {
-#pragma unroll
-    for (int i = 0; i < CH / 4; ++i)
-      reinterpret_cast<float4 *>(s + j0)[i] =
-          make_float4(fminf(base + x[4 * i], incl), fminf(base + x[4 * i + 1], incl),
-                      fminf(base + x[4 * i + 2], incl), fminf(base + x[4 * i + 3], incl));
-  }
-  if (pos == seg - 1 && (lane / seg) * (1 << tl2) < nrows) {
-    tm[lane / seg] = m;
-    tl[lane / seg] = incl;
-  }
-}
-
-// #{j < n : P_j <= x} over a non-decreasing LDS CDF (n <= kSplitMax): branch-
-// free binary lifting in a rolled loop.
-__device__ __forceinline__ int lds_count_le(const float *P, int n, float x) {
-  int pos = 0;
-#pragma unroll 1
-  for (int step = 1 << (31 - __clz(n)); step > 0; step >>= 1) {
-    const int np = pos + step;
-    const float v = P[min(np, n) - 1];
-    pos = (np <= n && v <= x) ? np : pos;
-  }
-  return pos;
-}
-
 // Flash draws of one split (Kernel 1): every tile tau of the split and every
 // head h takes S_tile systematic draws on the tile's own distribution: draw i
 // is the key whose tile-CDF interval holds ((i + a)/S_tile) l_tau, a = u of

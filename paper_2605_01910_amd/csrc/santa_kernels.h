@@ -53,9 +53,10 @@ hipError_t launch_fused_bernoulli(const Plan &p, const KvView &kv, const KtView 
 hipError_t launch_fused_dense(const Plan &p, const KvView &kv, const void *q, float scale_log2,
                               void *out, char *ws, hipStream_t st);
 
+// rows: the scheduled flash kernel (k_row_flash) in place of k_fused_dense's flash mode
 hipError_t launch_fused_flash(const Plan &p, const KvView &kv, const void *q, float scale_log2,
                               int tile_log2, int S_tile, const float *u, int32_t *idx_out,
-                              void *out, char *ws, hipStream_t st);
+                              void *out, char *ws, hipStream_t st, bool rows);
 
 // mode: 0 systematic, 1 stratified, 2 i.i.d. (thresholds by exponential spacings)
 hipError_t launch_fused_sampled(const Plan &p, const KvView &kv, const void *q, float scale_log2,

@@ -104,9 +104,11 @@ hipError_t launch_fused_dense(const Plan &p, const KvView &kv, const void *q, fl
 
 hipError_t launch_fused_flash(const Plan &p, const KvView &kv, const void *q, float scale_log2,
                               int tile_log2, int S_tile, const float *u, int32_t *idx_out,
-                              void *out, char *ws, hipStream_t st) {
+                              void *out, char *ws, hipStream_t st, bool rows) {
   return with_elem(p, [&](auto eptr) -> hipError_t {
     using E = std::remove_pointer_t<decltype(eptr)>;
+    if (rows)
+      return launch_row_flash_e<E>(p, kv, q, scale_log2, tile_log2, S_tile, u, idx_out, out, ws, st);
     return launch_flash_e<E>(p, kv, q, scale_log2, tile_log2, S_tile, u, idx_out, out, ws, st);
   });
 }

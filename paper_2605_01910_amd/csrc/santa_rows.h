@@ -114,6 +114,93 @@ __device__ __forceinline__ void merge_group4_lds(const float *part_row, int Tb, 
   store_out(out_row0 + h * kHeadDim + o + 1, sy * scale);
 }
 
+// A claim of the value stage: split-local key j and weight factor f.
+struct Claim {
+  int j;
+  float f;
+};
+
+// One wave: claims r in [r0, r1), 64 per pass.  claim(r, ok) is called by
+// every lane of a pass (ok: r < r1; the call may use lane shuffles) and
+// returns claim r's key and factor (read only where ok).  The keys of
+// successive claims are non-decreasing, so equal keys form runs with one
+// factor; the runs of successive passes go to a per-wave list (keyl, cntl:
+// 64 entries of key and weight count * factor) in LDS, gathered when the next
+// pass's runs would not fit and at the end: each listed V row is read once per
+// entry and added with its weight by one of the wave's four 16-lane slots, U
+// rows in flight each.  acc: the weighted sum of V rows, reduced over the four
+// slots in lanes 0..15 (8 columns each).
+template <typename E, bool PAGED, typename CL>
+__device__ __forceinline__ void wave_claims_gather(const FusedArgs &a, int b, int kvh, int start,
+                                                   int r0, int r1, CL claim, int16_t *keyl,
+                                                   float *cntl, float (&acc)[8]) {
+  constexpr int U = 4;
+  const int lane = threadIdx.x & 63, slot = lane >> 4, col = lane & 15;
+  const E *V = static_cast<const E *>(a.kv.v);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = 0.0f;
+  auto sync_lists = [] {  // list writes visible to the whole wave, in order
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+  };
+  auto gather = [&](int nl) {  // add the nl listed rows with their weights
+    for (int q0 = 0; q0 < nl; q0 += 4 * U) {
+      Chunk<E> ch[U];
+      float w[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int q = q0 + slot + 4 * u;
+        if (q < nl) {
+          ch[u] = Chunk<E>::load(V + row_offset<PAGED>(a.kv, b, kvh, start + keyl[q]) + col * 8);
+          w[u] = cntl[q];
+        } else {
+          ch[u] = Chunk<E>::zero();
+          w[u] = 0.0f;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        float f[8];
+        ch[u].to_float(f);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i] = fmaf(w[u], f[i], acc[i]);
+      }
+    }
+  };
+  int nl = 0;  // entries in the list (the same in every lane)
+  for (int c0 = r0;; c0 += 64) {  // one pass past the last claims gathers the rest
+    const bool done = c0 >= r1;
+    const int r = c0 + lane, nv = min(64, r1 - c0);
+    int j = -1;
+    float f = 0.0f;
+    if (!done) {
+      const Claim cl = claim(r, r < r1);
+      j = r < r1 ? cl.j : -1;
+      f = cl.f;
+    }
+    const int jp = __shfl_up(j, 1);
+    const bool first = !done && r < r1 && (lane == 0 || j != jp);
+    const unsigned long long m = __ballot(first);
+    const int nruns = __popcll(m);
+    if (done || nl + nruns > 64) {  // the end, or the list is full: gather it
+      gather(nl);
+      sync_lists();
+      nl = 0;
+      if (done) break;
+    }
+    if (first) {
+      const unsigned long long rest = lane < 63 ? m >> (lane + 1) : 0ull;
+      const int e = nl + __popcll(m & ((1ull << lane) - 1ull));
+      keyl[e] = (int16_t)j;
+      cntl[e] = (float)(rest ? __builtin_ctzll(rest) + 1 : nv - lane) * f;
+    }
+    nl += nruns;
+    sync_lists();
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = xor32_sum(xor16_sum(acc[i]));
+}
+
 // Value stage of head h in split t, by one wave, for sorted thresholds: the
 // split claims r in [N(lo), N(hi)), N(y) = #{r : tau_r < y}.  ureg: the
 // head's uniforms fetched before the row barrier -- kSys: u in ureg[0];
@@ -121,26 +208,17 @@ __device__ __forceinline__ void merge_group4_lds(const float *part_row, int Tb, 
 // of lane r % 64, so every lane counts its own thresholds and the claims
 // read u_r with lane shuffles; kIid (always so held): the sorted threshold
 // T_r in that place, tau_r = T_r Z; otherwise lanes 0 and 1 evaluate N(lo)
-// and N(hi) in closed form (count_below) and u_r comes from global memory.  The claims are taken 64 at a time: lane l inverts
-// tau_r on the split's LDS CDF (the key #{j : a P_j <= tau_r - lo}, App. A,
-// clamped to the split).  The chosen keys are non-decreasing in r, so equal
-// keys form runs; the runs of successive chunks go to a list of (key, count)
-// in LDS (keyl, cntl: 64 entries), gathered when the next chunk's runs would
-// not fit and at the end: each listed V row is read once per entry and added
-// with its count by one of the wave's four 16-lane slots, U rows in flight
-// each.  Returns the head's partial sum O_h = sum_j c_{h,j} V_j
-// (Sec. 2) reduced over the four slots in lanes 0..15 (8 columns each).
+// and N(hi) in closed form (count_below) and u_r comes from global memory.
+// Claim r takes the key #{j : a P_j <= tau_r - lo} of the split's LDS CDF
+// (App. A, clamped to the split) with weight 1.  Returns the head's partial
+// sum O_h = sum_j c_{h,j} V_j (Sec. 2) in lanes 0..15.
 template <typename E, bool PAGED, int MODE>
 __device__ __forceinline__ void row_head_value(const FusedArgs &a, const HeadClaim &c,
                                                const float *uh, const float (&ureg)[4], bool staged,
                                                const float *Ph, int nrows, int start, int b,
-                                               int kvh, int64_t rowq, int16_t *keyl, int *cntl,
+                                               int kvh, int64_t rowq, int16_t *keyl, float *cntl,
                                                float (&acc)[8]) {
-  constexpr int U = 4;
-  const int lane = threadIdx.x & 63, slot = lane >> 4, col = lane & 15;
-  const E *V = static_cast<const E *>(a.kv.v);
-#pragma unroll
-  for (int i = 0; i < 8; ++i) acc[i] = 0.0f;
+  const int lane = threadIdx.x & 63;
   // kIid: always in registers (S <= 256, one head per wave)
   const bool regs = MODE == kSys || MODE == kIid || (staged && a.S <= 4 * 64);
   // tau_r from the register value v (u_r, or T_r for kIid)
@@ -164,77 +242,63 @@ __device__ __forceinline__ void row_head_value(const FusedArgs &a, const HeadCla
     rlo = __builtin_amdgcn_readlane(n, 0);
     rhi = __builtin_amdgcn_readlane(n, 1);
   }
-  auto sync_lists = [] {  // list writes visible to the whole wave, in order
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    __builtin_amdgcn_wave_barrier();
+  auto claim = [&](int r, bool ok) {
+    float ur = ureg[0];
+    if (MODE != kSys && regs) {  // u_r (T_r) from lane r % 64 (every lane takes part)
+      const int src = r & 63, k = (r >> 6) & 3;
+      const float v0 = __shfl(ureg[0], src), v1 = __shfl(ureg[1], src);
+      const float v2 = __shfl(ureg[2], src), v3 = __shfl(ureg[3], src);
+      ur = k == 0 ? v0 : (k == 1 ? v1 : (k == 2 ? v2 : v3));
+    }
+    int j = 0;
+    if (ok) {
+      const float tau = MODE == kIid ? ur * c.Z
+                                     : threshold(r, (MODE == kStrat && !regs) ? uh[r] : ur,
+                                                 a.invS, c.Z);
+      const int pos = lds_cdf_count(Ph, nrows, c.a, tau - c.lo);
+      j = pos < nrows ? pos : nrows - 1;
+      if (a.idx_out) a.idx_out[rowq * a.S + r] = start + j;
+    }
+    return Claim{j, 1.0f};
   };
-  auto gather = [&](int nl) {  // add the nl listed rows with their counts
-    for (int q0 = 0; q0 < nl; q0 += 4 * U) {
-      Chunk<E> ch[U];
-      float w[U];
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int q = q0 + slot + 4 * u;
-        if (q < nl) {
-          ch[u] = Chunk<E>::load(V + row_offset<PAGED>(a.kv, b, kvh, start + keyl[q]) + col * 8);
-          w[u] = (float)cntl[q];
-        } else {
-          ch[u] = Chunk<E>::zero();
-          w[u] = 0.0f;
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        float f[8];
-        ch[u].to_float(f);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) acc[i] = fmaf(w[u], f[i], acc[i]);
-      }
+  wave_claims_gather<E, PAGED>(a, b, kvh, start, rlo, rhi, claim, keyl, cntl, acc);
+}
+
+// S2ANTA-flash value stage of head h in split t, by one wave (Sec. 3.3; App.
+// "S2ANTA-Flash Pseudocode", Kernel 1): every tile tau of the split takes
+// S_tile systematic draws on its own CDF (tile CDFs in Ph, tile maxima tm and
+// sums tl): draw i is the key whose tile-CDF interval holds ((i + a)/S_tile)
+// l_tau, a = the head's uniform of the tile (App. A's inverse CDF, clamped to
+// the tile), with weight exp2(m_tau - m_w) l_tau / S_tile (m_w: the split
+// maximum), so that the split's partial sum is o_w = sum_tau exp2(m_tau -
+// m_w) l_tau O_tau with O_tau the tile estimate.  Draw d = tau * S_tile + i;
+// its key is non-decreasing in d.
+template <typename E, bool PAGED>
+__device__ __forceinline__ void row_head_flash(const FusedArgs &a, const float *Ph,
+                                               const float *tm, const float *tl, float mw,
+                                               int nrows, int start, int b, int kvh, int64_t rowq,
+                                               int16_t *keyl, float *cntl, float (&acc)[8]) {
+  const int tl2 = a.tile_log2, St = a.S_tile;
+  const int ntile = (nrows + (1 << tl2) - 1) >> tl2;
+  const int gt0 = start >> tl2;  // global index of the split's first tile
+  const float invSt = 1.0f / (float)St;
+  const float *uh = a.u + rowq * a.Tmax + gt0;
+  auto claim = [&](int d, bool ok) {
+    int j = 0;
+    float f = 0.0f;
+    if (ok) {
+      const int tau = d / St, is = d - tau * St;
+      const int t0 = tau << tl2, n = min(1 << tl2, nrows - t0);
+      const float l = tl[tau];
+      const float x = (((float)is + uh[tau]) * invSt) * l;
+      const int k = lds_count_le(Ph + t0, n, x);
+      j = t0 + (k < n ? k : n - 1);
+      f = fast_exp2(tm[tau] - mw) * l * invSt;
+      if (a.idx_out) a.idx_out[(rowq * a.Tmax + gt0 + tau) * St + is] = start + j;
     }
+    return Claim{j, f};
   };
-  int nl = 0;  // entries in the list (the same in every lane)
-  for (int c0 = rlo;; c0 += 64) {  // one pass past the last chunk gathers the rest
-    const bool done = c0 >= rhi;
-    const int r = c0 + lane, nv = min(64, rhi - c0);
-    int j = -1;
-    if (!done) {
-      float ur = ureg[0];
-      if (MODE != kSys && regs) {  // u_r (T_r) from lane r % 64 (every lane takes part)
-        const int src = r & 63, k = (r >> 6) & 3;
-        const float v0 = __shfl(ureg[0], src), v1 = __shfl(ureg[1], src);
-        const float v2 = __shfl(ureg[2], src), v3 = __shfl(ureg[3], src);
-        ur = k == 0 ? v0 : (k == 1 ? v1 : (k == 2 ? v2 : v3));
-      }
-      if (r < rhi) {
-        const float tau = MODE == kIid ? ur * c.Z
-                                       : threshold(r, (MODE == kStrat && !regs) ? uh[r] : ur,
-                                                   a.invS, c.Z);
-        const int pos = lds_cdf_count(Ph, nrows, c.a, tau - c.lo);
-        j = pos < nrows ? pos : nrows - 1;
-        if (a.idx_out) a.idx_out[rowq * a.S + r] = start + j;
-      }
-    }
-    const int jp = __shfl_up(j, 1);
-    const bool first = !done && r < rhi && (lane == 0 || j != jp);
-    const unsigned long long m = __ballot(first);
-    const int nruns = __popcll(m);
-    if (done || nl + nruns > 64) {  // the end, or the list is full: gather it
-      gather(nl);
-      sync_lists();
-      nl = 0;
-      if (done) break;
-    }
-    if (first) {
-      const unsigned long long rest = lane < 63 ? m >> (lane + 1) : 0ull;
-      const int e = nl + __popcll(m & ((1ull << lane) - 1ull));
-      keyl[e] = (int16_t)j;
-      cntl[e] = rest ? __builtin_ctzll(rest) + 1 : nv - lane;
-    }
-    nl += nruns;
-    sync_lists();
-  }
-#pragma unroll
-  for (int i = 0; i < 8; ++i) acc[i] = xor32_sum(xor16_sum(acc[i]));
+  wave_claims_gather<E, PAGED>(a, b, kvh, start, 0, ntile * St, claim, keyl, cntl, acc);
 }
 
 // One workgroup per work item (rowkv, t < T), items row-major so that a row's
@@ -260,7 +324,7 @@ __attribute__((amdgpu_waves_per_eu(row_waves<E, G, PAGED>()))) void k_row_sample
   __shared__ float offl[G][2 * kRowTMax + 1];  // per head: offsets [T+1], split factors [T]
   __shared__ float mh[G], mtmp[4 * G];
   __shared__ int16_t keyl[4][64];
-  __shared__ int cntl[4][64];
+  __shared__ float cntl[4][64];
   __shared__ int rank_lds;
 
   const int T = a.T, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -375,6 +439,170 @@ __attribute__((amdgpu_waves_per_eu(row_waves<E, G, PAGED>()))) void k_row_sample
     for (int h = 0; h < G; ++h)
       merge_head<QE<E>, G>(part_row, h, Tb, nullptr, nullptr, scale, P, out + (row0 + h) * kHeadDim);
   }
+}
+
+// S2ANTA-flash on the scheduled skeleton (Sec. 3.3; App. "S2ANTA-Flash
+// Pseudocode", Kernels 1 and 2), G <= 4: one workgroup per (row, split),
+// splits of a.Ls keys rounded up to whole tiles.  No barrier stands before
+// the value stage: each head's wave builds its tile CDFs (wave_tile_cdf),
+// takes its draws (row_head_flash) and publishes o_w and (m_w, l_w), l_w =
+// sum_tau exp2(m_tau - m_w) l_tau; one arrival per split on the row counter,
+// and the row's last arrival merges O = sum_t a_t o_t / sum_t a_t l_t with
+// a_t = exp2(m_t - m*) (Kernel 2), through LDS copies of the partials on
+// direct grids.
+template <typename E, int G, bool PAGED, bool APPEND = false>
+__global__ __launch_bounds__(kThreads)
+__attribute__((amdgpu_waves_per_eu(row_waves<E, G, PAGED>()))) void k_row_flash(FusedArgs a) {
+  static_assert(G <= 4, "one head per wave");
+  extern __shared__ __attribute__((aligned(16))) float dyn[];
+  constexpr int pitch = kSplitMax, TS = kSplitMax / 16;
+  float *P = dyn;  // [G][pitch]: scores, then the tile CDFs; merge copies at the end
+  __shared__ float tst[G][2][TS];  // per head: tile maxima, tile sums
+  __shared__ float mh[G], mtmp[4 * G];
+  __shared__ float al[G][kRowTMax], den[G];
+  __shared__ int16_t keyl[4][64];
+  __shared__ float cntl[4][64];
+  __shared__ int rank_lds;
+
+  const int T = a.T, tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform in the wave
+  const int rowkv = blockIdx.x / T, t = blockIdx.x % T;
+  const int b = rowkv / a.Hkv, kvh = rowkv % a.Hkv;
+  const int64_t row0 = (int64_t)b * a.Hq + kvh * G;
+  QE<E> *out = static_cast<QE<E> *>(a.out);
+  const int L = seq_len(a.kv, b);
+  const int tl2 = a.tile_log2, align = max(kAlign, 1 << tl2);
+  const int Ls = (a.Ls + align - 1) / align * align, Tb = L > 0 ? (L + Ls - 1) / Ls : 0;
+  // tiles no split covers (past the row's length) have no draws
+  if (a.idx_out && (t == Tb - 1 || (Tb == 0 && t == 0))) {
+    const int t_end = (L + (1 << tl2) - 1) >> tl2;
+    const int nt = (a.Tmax - t_end) * a.S_tile;
+    for (int i = tid; i < G * nt; i += kThreads) {
+      const int h = i / nt, k = i - h * nt;
+      a.idx_out[((row0 + h) * a.Tmax + t_end) * a.S_tile + k] = -1;
+    }
+  }
+  if (t >= Tb) {
+    if (Tb == 0 && t == 0)  // empty sequence: zero output
+      for (int o = tid; o < G * kHeadDim; o += kThreads) store_out(out + row0 * kHeadDim + o, 0.0f);
+    return;
+  }
+  const int start = t * Ls, nrows = min(Ls, L - start);
+  if constexpr (APPEND) append_current<E, PAGED>(a.kv, b, kvh, a.Hkv, start, nrows, L);
+  {
+    const QRegs<E, G> qr = load_q<E, G>(static_cast<const QE<E> *>(a.q), b, a.Hq, kvh, tid & 15);
+    const float ksc = kv_scales<E>(a.kv, b, kvh, a.Hkv).x;  // FP8 cache: K scale
+    float mx[G];
+    score_tile<E, G, PAGED, 4>(a.kv, b, kvh, start, nrows, qr, a.scale_log2 * ksc, P, pitch, mx);
+    block_max_heads<G>(mx, mtmp, mh);
+  }
+  unsigned long long *sync = a.sync + (int64_t)rowkv * (kSyncStride / 2);
+  const unsigned long long base =
+      __hip_atomic_load(sync + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  float *part = a.part + ((int64_t)rowkv * T + t) * G * kHeadDim;
+  if (wave < G) {
+    const int h = wave;
+    float *Ph = P + h * pitch;
+    wave_tile_cdf(Ph, nrows, lane, tl2, tst[h][0], tst[h][1]);
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    const int ntile = (nrows + (1 << tl2) - 1) >> tl2;
+    float l = 0.0f;
+    for (int tau = lane; tau < ntile; tau += 64) l += fast_exp2(tst[h][0][tau] - mh[h]) * tst[h][1][tau];
+    l = wave_sum(l);
+    float acc[8];
+    row_head_flash<E, PAGED>(a, Ph, tst[h][0], tst[h][1], mh[h], nrows, start, b, kvh, row0 + h,
+                             keyl[wave], cntl[wave], acc);
+    if (lane < 16) {
+      float2 *d = reinterpret_cast<float2 *>(part + h * kHeadDim + lane * 8);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) st_coherent(d + i, make_float2(acc[2 * i], acc[2 * i + 1]));
+    }
+    if (lane == 0) st_coherent(a.stats + (row0 + h) * T + t, make_float2(mh[h], l));
+  }
+
+  // one arrival; the row's last arrival merges
+  const int rank = row_arrive(sync, base, &rank_lds);
+  if (rank != Tb - 1) return;
+  if (tid == 0)
+    __hip_atomic_store(sync + 1, base + (unsigned long long)Tb, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+  const float *part_row = a.part + (int64_t)rowkv * T * G * kHeadDim;
+  const float vsc = kv_scales<E>(a.kv, b, kvh, a.Hkv).y;  // FP8 cache: V scale
+  constexpr int SPL = G * kHeadDim;  // floats per split: whole KiB for G >= 2
+  const bool in_lds = G >= 2 && a.direct;
+  if (in_lds) {  // all partials of the row into LDS (1 KiB per wave instruction)
+    typedef __attribute__((address_space(3))) void *lds_ptr;
+    const char *src = reinterpret_cast<const char *>(part_row);
+    const int nk = Tb * (SPL / 256);  // 1 KiB pieces
+    for (int k = wave; k < nk; k += kThreads / 64)
+      __builtin_amdgcn_global_load_lds(src + k * 1024 + lane * 16,
+                                       (lds_ptr)(reinterpret_cast<char *>(P) + k * 1024), 16, 0,
+                                       16 /* sc1: agent-coherent */);
+  }
+  if (wave < G) {  // a_t and the denominator of head `wave`
+    const float2 st = lane < Tb ? ld_coherent(a.stats + (row0 + wave) * T + lane)
+                                : make_float2(-kInf, 0.0f);
+    const float m = wave_max(st.x);
+    const float at = lane < Tb ? fast_exp2(st.x - m) : 0.0f;
+    const float d = wave_sum(at * st.y);
+    if (lane < Tb) al[wave][lane] = at;
+    if (lane == 0) den[wave] = d;
+  }
+  wait_stores();  // vmcnt(0): the copies into LDS have landed as well
+  __syncthreads();
+  for (int o2 = tid; o2 < SPL / 2; o2 += kThreads) {  // column pairs; split order, 16 in flight
+    const int o = 2 * o2, h = o / kHeadDim;
+    float sx = 0.0f, sy = 0.0f;
+    for (int t0 = 0; t0 < Tb; t0 += 16) {
+      float2 v[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        v[i] = t0 + i >= Tb ? make_float2(0.0f, 0.0f)
+               : in_lds     ? *reinterpret_cast<const float2 *>(P + (t0 + i) * SPL + o)
+                            : ld_coherent(reinterpret_cast<const float2 *>(part_row + (int64_t)(t0 + i) * SPL + o));
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        if (t0 + i < Tb) {
+          sx = fmaf(al[h][t0 + i], v[i].x, sx);
+          sy = fmaf(al[h][t0 + i], v[i].y, sy);
+        }
+    }
+    store_out(out + row0 * kHeadDim + o, sx * vsc / den[h]);
+    store_out(out + row0 * kHeadDim + o + 1, sy * vsc / den[h]);
+  }
+}
+
+template <typename E>
+hipError_t launch_row_flash_e(const Plan &p, const KvView &kv, const void *q, float scale_log2,
+                              int tile_log2, int S_tile, const float *u, int32_t *idx_out,
+                              void *out, char *ws, hipStream_t st) {
+  if (p.T > kRowTMax || p.G > 4) return hipErrorInvalidValue;
+  FusedArgs args = make_args(p, kv, q, out, scale_log2, ws);
+  args.direct = (int64_t)p.B * p.Hkv * p.T <= kDirectPollMax;
+  args.u = u;
+  args.idx_out = idx_out;
+  args.tile_log2 = tile_log2;
+  args.S_tile = S_tile;
+  args.Tmax = (p.n_k + (1 << tile_log2) - 1) >> tile_log2;
+  return with_g_paged(p.G, kv.bt != nullptr, [&](auto gc, auto paged) -> hipError_t {
+    constexpr int G = decltype(gc)::value;
+    constexpr bool PG = decltype(paged)::value;
+    if constexpr (G > 4) {
+      return hipErrorInvalidValue;
+    } else {
+      const void *fn = kv.k_new ? reinterpret_cast<const void *>(&k_row_flash<E, G, PG, true>)
+                                : reinterpret_cast<const void *>(&k_row_flash<E, G, PG>);
+      void *params[] = {&args};
+      // direct grids of G >= 2 merge through LDS copies of the T partials
+      // (at most 128 KiB)
+      const size_t lds = std::max((size_t)G * kSplitMax * 4,
+                                  args.direct && G >= 2 ? (size_t)p.T * G * kHeadDim * 4 : 0);
+      const CallTimer tm = call_timer();
+      return hipExtLaunchKernel(fn, dim3(p.B * p.Hkv * p.T), dim3(kThreads), params, lds, st,
+                                tm.start, tm.stop, 0);
+    }
+  });
 }
 
 template <typename E>

@@ -1,8 +1,9 @@
-// santa_rows_f32.hip -- scheduled sampled kernels instantiated for float32 elements.
+// santa_rows_f32.hip -- scheduled sampled and flash kernels instantiated for float32 elements.
 #include "santa_rows.h"
 
 namespace santa {
 
 template hipError_t launch_rows_e<float>(const Plan &, const KvView &, const void *, float, int, const float *, int32_t *, void *, char *, hipStream_t);
+template hipError_t launch_row_flash_e<float>(const Plan &, const KvView &, const void *, float, int, int, const float *, int32_t *, void *, char *, hipStream_t);
 
 }  // namespace santa

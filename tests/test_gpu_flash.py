@@ -10,6 +10,7 @@ import numpy as np
 import pytest
 import torch
 
+from paper_2605_01910_amd import santa as S
 from tests.gpu_util import DeviceWorkload, check_flash, log, run
 from workload import make_workload
 
@@ -28,22 +29,28 @@ CASES = {
 }
 
 
+@pytest.mark.parametrize("path", ["one", "rows"])
 @pytest.mark.parametrize("case", sorted(CASES))
-def test_flash_parity(case):
+def test_flash_parity(case, path):
+    """Both flash kernels: k_fused_dense's flash mode ("one") and the
+    scheduled k_row_flash ("rows"; G = 8 keeps the first)."""
     cfg, over = CASES[case]
-    log(f"[flash] {case} cfg={cfg} {over}")
+    log(f"[flash/{path}] {case} cfg={cfg} {over}")
     w = make_workload(cfg, seed=61, kind="flash", **over)
-    out, idx, _ = run(w, "flash")
+    with S.options(path):
+        out, idx, _ = run(w, "flash")
     log(f"  {check_flash(w, out, idx)}")
 
 
-def test_flash_large_batch_launch():
+@pytest.mark.parametrize("path", ["one", "rows"])
+def test_flash_large_batch_launch(path):
     """More rows than one resident round: one workgroup per split."""
     lens = [(37 * i * i + 11 * i) % 9000 for i in range(24)]
     lens[3] = 0
     w = make_workload(3, B=24, n=9000, kind="flash", ctx_len=lens, tile=256, S_tile=4, seed=62)
-    log(f"[flash] large batch B={w.B}")
-    out, idx, _ = run(w, "flash")
+    log(f"[flash/{path}] large batch B={w.B}")
+    with S.options(path):
+        out, idx, _ = run(w, "flash")
     log(f"  {check_flash(w, out, idx)}")
 
 
@@ -56,12 +63,14 @@ def test_flash_repeat_calls_are_bitwise_identical():
 
 
 @pytest.mark.timeout(300)
-def test_flash_full_size_llama8b_32k():
+@pytest.mark.parametrize("path", ["one", "rows"])
+def test_flash_full_size_llama8b_32k(path):
     """Batch 1, 32 query / 8 KV heads, n_k = 32768, tiles of 256 keys, S = 2048
     draws per head (16 per tile), every row."""
     w = make_workload(2, seed=0, kind="flash", tile=256, S_tile=16)
-    log(f"[flash full] n={w.n_max} tile={w.tile} S_tile={w.S_tile}")
-    out, idx, _ = run(w, "flash")
+    log(f"[flash full/{path}] n={w.n_max} tile={w.tile} S_tile={w.S_tile}")
+    with S.options(path):
+        out, idx, _ = run(w, "flash")
     log(f"  {check_flash(w, out, idx)}")
 
 
