@@ -365,6 +365,7 @@ FAMILY_SOURCES = {
     "k_stream_cdf + k_value_heads": ["csrc/santa_stream.h", "csrc/santa_stream_*.hip"],
     "k_bern_stream + k_value_heads": ["csrc/santa_stream.h", "csrc/santa_stream_*.hip"],
     "k_row_sampled": ["csrc/santa_rows.h", "csrc/santa_rows_*.hip"],
+    "k_row_flash": ["csrc/santa_rows.h", "csrc/santa_rows_*.hip"],
 }
 # counter runs per workload: (cfg, file under profiles/)
 TRAFFIC_FILES = {2: "traffic_llama8b_32k_b1.json", 3: "traffic_llama8b_32k_b16.json",
