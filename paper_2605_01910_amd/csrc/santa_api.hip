@@ -175,6 +175,8 @@ santa::Plan make_plan(const santa_shape_t *sh, const santa_kv_t *kv, int S, int 
     p.T = Tf;
     // rows use ceil(L_b / T) keys per split rounded up to 64; Ls is the longest
     p.Ls = (int)(((p.n_k + p.T - 1) / p.T + 63) & ~63);
+    // only splits that hold keys (short caches: fewer than T splits of 64 keys)
+    p.T = (int)((p.n_k + p.Ls - 1) / p.Ls);
     const bool sampled = kind != SANTA_KIND_DENSE && kind != SANTA_KIND_FLASH;
     const bool big = (int64_t)p.B * p.Hkv * p.T > 1024;  // workgroups beyond one resident round
     // systematic and stratified steps, and i.i.d. steps with S <= 256 at G <= 4
