@@ -1,10 +1,11 @@
-// santa_rows.h -- the scheduled sampled step (k_row_sampled): systematic,
-// stratified and (S <= 256, G <= 4) i.i.d. SANTA.  One
-// workgroup per (row, split), scheduled by the hardware like the two-launch
-// key stream, but the split's CDF stays in LDS: the split publishes its
-// statistics, waits at its row's barrier, claims its thresholds, gathers
-// their V rows and publishes partial sums; the row's last arrival merges.
-// No CDF stash goes through HBM.  Shared pieces are in santa_fused.h.
+// santa_rows.h -- the scheduled kernels: k_row_sampled (systematic,
+// stratified and, for S <= 256 at G <= 4, i.i.d. SANTA) and k_row_flash
+// (S2ANTA-flash, G <= 4).  One workgroup per (row, split), scheduled by the
+// hardware like the two-launch key stream, but the split's CDF stays in LDS:
+// the split publishes its statistics, waits at its row's barrier (flash:
+// none), claims its thresholds, gathers their V rows and publishes partial
+// sums; the row's last arrival merges.  No CDF stash goes through HBM.
+// Shared pieces are in santa_fused.h.
 #pragma once
 
 #include "santa_fused.h"
