@@ -26,7 +26,9 @@ CASES = {
     "sys_paged_scheduled": (4, "systematic", dict(B=3, len_lo=700, len_hi=3000), "rows"),
     "dense": (2, "dense", dict(B=2, n=3000, ctx_len=[3000, 1234]), "one"),
     "dense_paged": (4, "dense", dict(B=3, len_lo=900, len_hi=2600), "one"),
-    "flash": (2, "flash", dict(B=2, n=3000, ctx_len=[3000, 1500]), "one"),
+    "flash": (2, "flash", dict(B=2, n=3000, ctx_len=[3000, 1500]), "rows"),
+    "flash_dense_kernel": (2, "flash", dict(B=2, n=3000, ctx_len=[3000, 1500]), "one"),
+    "iid_scheduled": (2, "iid", dict(B=2, n=2000, S=96, ctx_len=[2000, 640]), "rows"),
     "sys_f32_no_ctx": (1, "systematic", {}, "one"),
 }
 
@@ -49,7 +51,7 @@ def test_fused_append(case):
         k.copy_(4.0 * torch.sign(qg[b]))
         v.fill_(-2.0)
     dw.kv.k_new, dw.kv.v_new = k_new.data_ptr(), v_new.data_ptr()
-    with S.options(path if kind not in ("dense", "flash") else "auto"):
+    with S.options(path if kind != "dense" else "auto"):
         out, idx, _ = run(w, kind, dw=dw)
     torch.cuda.synchronize()
     for b, (k, v) in enumerate(rows):
