@@ -314,7 +314,7 @@ __device__ __forceinline__ void row_head_flash(const FusedArgs &a, const float *
 // base on and empties the mailbox.  Otherwise, where waiting workgroups share
 // CUs with streaming ones, thread 0 polls the counter: two arrivals per
 // split, after the statistics and after the partial sums.
-template <typename E, int G, bool PAGED, int MODE, bool APPEND = false>
+template <typename E, int G, bool PAGED, int MODE, bool APPEND = false, bool USTAGE = false>
 __global__ __launch_bounds__(kThreads)
 __attribute__((amdgpu_waves_per_eu(row_waves<E, G, PAGED>()))) void k_row_sampled(FusedArgs a) {
   static_assert(MODE == kSys || MODE == kStrat || (MODE == kIid && G <= 4),
@@ -379,7 +379,9 @@ __attribute__((amdgpu_waves_per_eu(row_waves<E, G, PAGED>()))) void k_row_sample
       arrived = __hip_atomic_fetch_add(sync, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1;
   }
   // the uniforms of head `wave` (G <= 4), fetched while the row arrives;
-  // i.i.d.: turned into the head's sorted thresholds
+  // i.i.d.: turned into the head's sorted thresholds.  Stratified budgets
+  // above the registers' 256 are copied into LDS after the split CDFs in the
+  // USTAGE form (global_load_lds, 4 bytes per lane, no registers held)
   const int upr = MODE == kStrat ? a.S : (MODE == kIid ? a.S + 1 : 1);  // uniforms per head
   float ureg[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   if (G <= 4 && wave < G) {
@@ -390,6 +392,11 @@ __attribute__((amdgpu_waves_per_eu(row_waves<E, G, PAGED>()))) void k_row_sample
 #pragma unroll
       for (int k = 0; k < 4; ++k) ureg[k] = lane + 64 * k < a.S ? uw[lane + 64 * k] : 0.0f;
       if (MODE == kIid) iid_thresholds_regs(ureg, uw[a.S], a.S, lane);
+    } else if constexpr (MODE == kStrat && USTAGE) {
+      typedef __attribute__((address_space(3))) void *lds_ptr;
+      float *ul = P + G * pitch + wave * a.S;
+      for (int i = 0; i < a.S; i += 64)
+        if (i + lane < a.S) __builtin_amdgcn_global_load_lds(uw + i + lane, (lds_ptr)(ul + i), 4, 0, 0);
     }
   }
   // 2. the row barrier, then per head, by wave h: global offsets, its claims
@@ -410,6 +417,10 @@ __attribute__((amdgpu_waves_per_eu(row_waves<E, G, PAGED>()))) void k_row_sample
     const float *uh = a.u + (row0 + h) * upr;
     if (G > 4) {  // two heads per wave: the head's own uniforms, from global memory
       ureg[0] = MODE == kSys ? uh[0] : 0.0f;
+    }
+    if constexpr (MODE == kStrat && G <= 4 && USTAGE) {  // this wave's LDS copy
+      wait_stores();  // vmcnt(0): the copies into LDS have landed
+      uh = P + G * pitch + h * a.S;
     }
     row_head_value<E, PAGED, MODE>(a, c, uh, ureg, G <= 4, P + h * pitch, nrows, start, b, kvh,
                                    row0 + h, keyl[wave], cntl[wave], acc);
@@ -615,6 +626,8 @@ hipError_t launch_rows_e(const Plan &p, const KvView &kv, const void *q, float s
     return hipErrorInvalidValue;
   FusedArgs args = make_args(p, kv, q, out, scale_log2, ws);
   args.direct = (int64_t)p.B * p.Hkv * p.T <= kDirectPollMax;
+  // stratified uniforms beyond the registers, into LDS on direct grids
+  args.ustage = args.direct && mode == kStrat && p.G <= 4 && p.S > 4 * 64 && p.S <= 2048;
   args.u = u;
   args.idx_out = idx_out;
   return with_g_paged(p.G, kv.bt != nullptr, [&](auto gc, auto paged) -> hipError_t {
@@ -628,16 +641,22 @@ hipError_t launch_rows_e(const Plan &p, const KvView &kv, const void *q, float s
     else if (mode == kSys)
       fn = ap ? reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kSys, true>)
               : reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kSys>);
-    if constexpr (G <= 4)
+    if constexpr (G <= 4) {
       if (mode == kIid)
         fn = ap ? reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kIid, true>)
                 : reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kIid>);
+      if (mode == kStrat && args.ustage)  // uniforms staged in LDS
+        fn = ap ? reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kStrat, true, true>)
+                : reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kStrat, false, true>);
+    }
     if (!fn) return hipErrorInvalidValue;
     void *params[] = {&args};
     // direct grids of G = 4 merge through LDS (merge_group4_lds: T partials,
-    // at most 128 KiB, within the 160 KiB of a CU)
-    const size_t lds = std::max((size_t)G * kSplitMax * 4,
-                                args.direct && G == 4 ? (size_t)p.T * G * kHeadDim * 4 : 0);
+    // at most 128 KiB, within the 160 KiB of a CU); staged stratified
+    // uniforms (at most 2048 per head) follow the split CDFs
+    const size_t lds = std::max({(size_t)G * kSplitMax * 4,
+                                 args.direct && G == 4 ? (size_t)p.T * G * kHeadDim * 4 : 0,
+                                 args.ustage ? (size_t)G * (kSplitMax + p.S) * 4 : 0});
     const CallTimer tm = call_timer();
     return hipExtLaunchKernel(fn, dim3(p.B * p.Hkv * p.T), dim3(kThreads), params, lds, st,
                               tm.start, tm.stop, 0);
