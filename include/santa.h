@@ -313,8 +313,9 @@ santa_status_t santa_stream_read(const void *buf, size_t bytes, uint32_t *sink, 
  *                          with at most 64 splits per row take the scheduled
  *                          path for S <= 1024 (paged caches up to 8192
  *                          workgroups, KV rows x splits, FP8 caches up to
- *                          2048), i.i.d. steps too for S <= 256 at
- *                          num_q_heads / num_kv_heads <= 4; other sampled
+ *                          2048), i.i.d. steps too at num_q_heads /
+ *                          num_kv_heads <= 4 for S <= 256, or larger S on
+ *                          grids of at most 256 workgroups; other sampled
  *                          steps whose rows fit one
  *                          resident round of about 1024 workgroups take one
  *                          persistent launch, larger ones the two-launch path;
@@ -324,8 +325,9 @@ santa_status_t santa_stream_read(const void *buf, size_t bytes, uint32_t *sink, 
  *   SANTA_PATH_MULTI       every step: the multi-kernel variant (score/CDF,
  *                          offsets, sampling and merge kernels);
  *   SANTA_PATH_SCHEDULED   systematic and stratified steps with at most 64
- *                          splits per row, and i.i.d. steps among them with
- *                          S <= 256 at num_q_heads / num_kv_heads <= 4: one
+ *                          splits per row, and i.i.d. steps among them at
+ *                          num_q_heads / num_kv_heads <= 4 (S <= 256, or
+ *                          larger S on grids of at most 256 workgroups): one
  *                          hardware-scheduled launch, a
  *                          workgroup per split that keeps its CDF in LDS across
  *                          a row barrier (k_row_sampled); other sampled steps

@@ -179,16 +179,19 @@ santa::Plan make_plan(const santa_shape_t *sh, const santa_kv_t *kv, int S, int 
     p.T = (int)((p.n_k + p.Ls - 1) / p.Ls);
     const bool sampled = kind != SANTA_KIND_DENSE && kind != SANTA_KIND_FLASH;
     const bool big = (int64_t)p.B * p.Hkv * p.T > 1024;  // workgroups beyond one resident round
-    // systematic and stratified steps, and i.i.d. steps with S <= 256 at G <= 4
-    // (their sorted thresholds held in registers), take the scheduled path
+    // systematic and stratified steps, and i.i.d. steps at G <= 4 whose sorted
+    // thresholds fit registers or LDS (iid_rows), take the scheduled path
     // (its row offsets live in LDS, so at most kRowTMax splits per row) when
     // asked for, and by default where it measured faster than both other
     // paths: budgets up to 1024; paged caches up to 8192 workgroups and FP8
     // caches up to 2048 (beyond those the two-launch path was faster)
-    const bool rows_ok = (kind == SANTA_KIND_SYSTEMATIC || kind == SANTA_KIND_STRATIFIED ||
-                          (kind == SANTA_KIND_IID && p.G <= 4 && S <= 256)) &&
-                         p.T <= santa::kRowTMax;
     const int64_t grid = (int64_t)p.B * p.Hkv * p.T;
+    // i.i.d. thresholds: in registers up to 256 per head, in LDS up to 2048
+    // on grids of at most kDirectPollMax workgroups
+    const bool iid_rows = p.G <= 4 && (S <= 256 || (S <= 2048 && grid <= santa::kDirectPollMax));
+    const bool rows_ok = (kind == SANTA_KIND_SYSTEMATIC || kind == SANTA_KIND_STRATIFIED ||
+                          (kind == SANTA_KIND_IID && iid_rows)) &&
+                         p.T <= santa::kRowTMax;
     const bool rows_auto = rows_ok && S <= 1024 && (!kv->block_table || grid <= 8192) &&
                            (p.elem != 2 || grid <= 2048);
     p.rows = g_opts.path == SANTA_PATH_SCHEDULED ? rows_ok

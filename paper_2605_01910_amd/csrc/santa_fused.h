@@ -86,9 +86,6 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kSpinLimit = 1 << 22;
-// Scheduled sampled path: grids of at most this many workgroups (one per CU
-// of the MI355X) wait at the row barrier by polling the statistics directly.
-constexpr int kDirectPollMax = 256;
 constexpr int kAlign = 64;         // split lengths and stash rows are multiples of this many keys
 constexpr int kBlock = 32;         // keys per block of the two-level CDF search
 constexpr int kGatherUnroll = 8;   // V rows in flight per row slot in k_value_heads

@@ -13,6 +13,10 @@ constexpr int kThreads = 256;   // threads per workgroup (4 waves of 64)
 constexpr int kSplitMax = 1024; // largest KV split (keys) handled by one workgroup
 constexpr int kMaxSplits = 256; // largest number of splits per row in the fused kernels
 constexpr int kRowTMax = 64;    // largest number of splits per row of the scheduled sampled path
+// Scheduled path: grids of at most this many workgroups (one per CU of the
+// MI355X) wait at the row barrier by polling the statistics directly and
+// may hold large threshold sets in LDS.
+constexpr int kDirectPollMax = 256;
 // Per KV row, the fused paths keep a sync block of kSyncStride ints: the
 // counters in the first 256 bytes, then (at u64 index kMailOffset) the
 // scheduled sampled path's statistics mailbox, one u64 per (head < 8, split <

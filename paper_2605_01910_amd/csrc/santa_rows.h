@@ -1,5 +1,5 @@
 // santa_rows.h -- the scheduled kernels: k_row_sampled (systematic,
-// stratified and, for S <= 256 at G <= 4, i.i.d. SANTA) and k_row_flash
+// stratified and, at G <= 4, i.i.d. SANTA) and k_row_flash
 // (S2ANTA-flash, G <= 4).  One workgroup per (row, split), scheduled by the
 // hardware like the two-launch key stream, but the split's CDF stays in LDS:
 // the split publishes its statistics, waits at its row's barrier (flash:
@@ -220,14 +220,14 @@ __device__ __forceinline__ void row_head_value(const FusedArgs &a, const HeadCla
                                                int kvh, int64_t rowq, int16_t *keyl, float *cntl,
                                                float (&acc)[8]) {
   const int lane = threadIdx.x & 63;
-  // kIid: always in registers (S <= 256, one head per wave)
-  const bool regs = MODE == kSys || MODE == kIid || (staged && a.S <= 4 * 64);
+  // kIid: in registers for S <= 256, else in LDS (uh)
+  const bool regs = MODE == kSys || (staged && a.S <= 4 * 64);
   // tau_r from the register value v (u_r, or T_r for kIid)
   auto tau_reg = [&](int r, float v) {
     return MODE == kIid ? v * c.Z : threshold(r, v, a.invS, c.Z);
   };
   int rlo = 0, rhi = 0;
-  if (MODE == kIid || (MODE == kStrat && regs)) {  // N(lo), N(hi) over the registers
+  if (MODE != kSys && regs) {  // N(lo), N(hi) over the registers
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int r = lane + 64 * k;
@@ -235,11 +235,18 @@ __device__ __forceinline__ void row_head_value(const FusedArgs &a, const HeadCla
       rlo += __popcll(__ballot(tau < c.lo));
       rhi += __popcll(__ballot(tau < c.hi));
     }
-  } else if constexpr (MODE != kIid) {
+  } else {
     int n = 0;
-    if (lane < 2)
-      n = count_below<MODE>(uh, MODE == kSys ? ureg[0] : 0.0f, a.S, a.invS, c.Z,
-                            (float)a.S / c.Z, lane ? c.hi : c.lo);
+    if (lane < 2) {
+      const float y = lane ? c.hi : c.lo;
+      if constexpr (MODE == kIid) {  // binary search over the sorted T_r Z
+        for (int step = 1 << (31 - __clz(a.S)); step > 0; step >>= 1)
+          n = (n + step <= a.S && uh[n + step - 1] * c.Z < y) ? n + step : n;
+      } else {
+        n = count_below<MODE>(uh, MODE == kSys ? ureg[0] : 0.0f, a.S, a.invS, c.Z,
+                              (float)a.S / c.Z, y);
+      }
+    }
     rlo = __builtin_amdgcn_readlane(n, 0);
     rhi = __builtin_amdgcn_readlane(n, 1);
   }
@@ -253,7 +260,7 @@ __device__ __forceinline__ void row_head_value(const FusedArgs &a, const HeadCla
     }
     int j = 0;
     if (ok) {
-      const float tau = MODE == kIid ? ur * c.Z
+      const float tau = MODE == kIid ? (regs ? ur : uh[r]) * c.Z
                                      : threshold(r, (MODE == kStrat && !regs) ? uh[r] : ur,
                                                  a.invS, c.Z);
       const int pos = lds_cdf_count(Ph, nrows, c.a, tau - c.lo);
@@ -379,9 +386,10 @@ __attribute__((amdgpu_waves_per_eu(row_waves<E, G, PAGED>()))) void k_row_sample
       arrived = __hip_atomic_fetch_add(sync, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1;
   }
   // the uniforms of head `wave` (G <= 4), fetched while the row arrives;
-  // i.i.d.: turned into the head's sorted thresholds.  Stratified budgets
-  // above the registers' 256 are copied into LDS after the split CDFs in the
-  // USTAGE form (global_load_lds, 4 bytes per lane, no registers held)
+  // i.i.d.: turned into the head's sorted thresholds.  Budgets above the
+  // registers' 256 go to LDS after the split CDFs in the USTAGE form:
+  // stratified uniforms copied (global_load_lds, 4 bytes per lane, no
+  // registers held), i.i.d. thresholds built there (wave_iid_thresholds)
   const int upr = MODE == kStrat ? a.S : (MODE == kIid ? a.S + 1 : 1);  // uniforms per head
   float ureg[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   if (G <= 4 && wave < G) {
@@ -397,6 +405,8 @@ __attribute__((amdgpu_waves_per_eu(row_waves<E, G, PAGED>()))) void k_row_sample
       float *ul = P + G * pitch + wave * a.S;
       for (int i = 0; i < a.S; i += 64)
         if (i + lane < a.S) __builtin_amdgcn_global_load_lds(uw + i + lane, (lds_ptr)(ul + i), 4, 0, 0);
+    } else if constexpr (MODE == kIid && USTAGE) {  // the sorted thresholds, into LDS
+      wave_iid_thresholds(uw, a.S, P + G * pitch + wave * a.S, lane);
     }
   }
   // 2. the row barrier, then per head, by wave h: global offsets, its claims
@@ -418,8 +428,10 @@ __attribute__((amdgpu_waves_per_eu(row_waves<E, G, PAGED>()))) void k_row_sample
     if (G > 4) {  // two heads per wave: the head's own uniforms, from global memory
       ureg[0] = MODE == kSys ? uh[0] : 0.0f;
     }
-    if constexpr (MODE == kStrat && G <= 4 && USTAGE) {  // this wave's LDS copy
+    if constexpr (MODE != kSys && G <= 4 && USTAGE) {  // this wave's LDS copy
       wait_stores();  // vmcnt(0): the copies into LDS have landed
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+      __builtin_amdgcn_wave_barrier();
       uh = P + G * pitch + h * a.S;
     }
     row_head_value<E, PAGED, MODE>(a, c, uh, ureg, G <= 4, P + h * pitch, nrows, start, b, kvh,
@@ -621,13 +633,15 @@ template <typename E>
 hipError_t launch_rows_e(const Plan &p, const KvView &kv, const void *q, float scale_log2,
                          int mode, const float *u, int32_t *idx_out, void *out, char *ws,
                          hipStream_t st) {
-  if (p.T > kRowTMax || (mode != kSys && mode != kStrat && mode != kIid) ||
-      (mode == kIid && (p.G > 4 || p.S > 4 * 64)))
-    return hipErrorInvalidValue;
   FusedArgs args = make_args(p, kv, q, out, scale_log2, ws);
   args.direct = (int64_t)p.B * p.Hkv * p.T <= kDirectPollMax;
-  // stratified uniforms beyond the registers, into LDS on direct grids
-  args.ustage = args.direct && mode == kStrat && p.G <= 4 && p.S > 4 * 64 && p.S <= 2048;
+  // stratified uniforms and i.i.d. thresholds beyond the registers, into LDS
+  // on direct grids
+  args.ustage = args.direct && (mode == kStrat || mode == kIid) && p.G <= 4 && p.S > 4 * 64 &&
+                p.S <= 2048;
+  if (p.T > kRowTMax || (mode != kSys && mode != kStrat && mode != kIid) ||
+      (mode == kIid && (p.G > 4 || (p.S > 4 * 64 && !args.ustage))))
+    return hipErrorInvalidValue;
   args.u = u;
   args.idx_out = idx_out;
   return with_g_paged(p.G, kv.bt != nullptr, [&](auto gc, auto paged) -> hipError_t {
@@ -643,8 +657,11 @@ hipError_t launch_rows_e(const Plan &p, const KvView &kv, const void *q, float s
               : reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kSys>);
     if constexpr (G <= 4) {
       if (mode == kIid)
-        fn = ap ? reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kIid, true>)
-                : reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kIid>);
+        fn = args.ustage
+                 ? (ap ? reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kIid, true, true>)
+                       : reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kIid, false, true>))
+                 : (ap ? reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kIid, true>)
+                       : reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kIid>));
       if (mode == kStrat && args.ustage)  // uniforms staged in LDS
         fn = ap ? reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kStrat, true, true>)
                 : reinterpret_cast<const void *>(&k_row_sampled<E, G, PG, kStrat, false, true>);

@@ -140,7 +140,8 @@ def test_path_choice_by_size_cache_and_kind():
     """The host picks a path without launching anything: the scheduled path
     for systematic and stratified steps where it measured fastest (S <= 1024;
     paged caches up to 8192 workgroups, FP8 up to 2048) and for i.i.d. steps
-    with S <= 256 at G <= 4, else the persistent launch within one resident
+    at G <= 4 with S <= 256, or larger S on grids of at most 256 workgroups,
+    else the persistent launch within one resident
     round and the two-launch path beyond it; Bernoulli steps never take the
     scheduled path, nor does a row that needs more than 64 splits."""
     sysk, strat, iid = S.SANTA_KIND_SYSTEMATIC, S.SANTA_KIND_STRATIFIED, S.SANTA_KIND_IID
@@ -159,9 +160,10 @@ def test_path_choice_by_size_cache_and_kind():
     assert _plan(_shape(B=16), _kv(), 2048, sysk)["kernels"] == two
     assert _plan(_shape(B=16), _kv(), 256, iid)["kernels"] == rows
     assert _plan(_shape(B=1), _kv(), 256, iid)["kernels"] == rows
-    # i.i.d. thresholds live in registers on the scheduled path: S <= 256, G <= 4
-    assert _plan(_shape(B=1), _kv(), 512, iid)["kernels"] == one
-    assert _plan(_shape(B=16), _kv(), 512, iid)["kernels"] == two
+    # i.i.d. thresholds on the scheduled path: in registers up to S = 256, in
+    # LDS above that on grids of at most 256 workgroups, G <= 4
+    assert _plan(_shape(B=1), _kv(), 384, iid)["kernels"] == rows
+    assert _plan(_shape(B=16), _kv(), 384, iid)["kernels"] == two
     assert _plan(_shape(B=1, Hq=16, Hkv=2), _kv(), 256, iid)["kernels"] == one
     paged = _kv(n=65536, bt=16, ps=16, mp=4096)
     assert _plan(_shape(B=16), paged, 256, sysk)["kernels"] == rows

@@ -1,8 +1,9 @@
 """GPU parity of santa_decode_iid (SANTA with i.i.d. draws, Sec. 2, Eq.
 "stochastic-add-only-attn"; thresholds by exponential spacings) against the
 CPU oracle through the C ABI, on the three sampled launch paths (the
-scheduled one takes S <= 256 at G <= 4, holding the sorted thresholds in
-registers; G = 8 falls back to the one-launch path there): indices
+scheduled one takes G <= 4 and holds the sorted thresholds in registers up
+to S = 256, in LDS above that on grids of at most 256 workgroups; other
+cases fall back to the one-launch path there): indices
 bit-exact up to the 1e-5 band, outputs within 2e-2 of the oracle's gather of
 the GPU's own indices.  Cases cover ragged and empty rows, S = 1, G = 8,
 the paged cache, and the full Llama-3.1-8B 32k shape."""
@@ -23,6 +24,10 @@ CASES = {
     "empty_row": (2, dict(B=3, n=600, S=32, ctx_len=[600, 0, 5])),
     "paged": (4, dict(B=3, len_lo=700, len_hi=3000, S=128)),
     "f32_cfg1": (1, dict(S=64)),
+    # thresholds in LDS on the scheduled path (S above 256 on grids of at most
+    # 256 workgroups; the call takes S <= 511 at G = 4)
+    "s300_lds": (2, dict(B=1, n=5000, S=300)),
+    "s511_lds_ragged": (2, dict(B=2, n=9000, ctx_len=[9000, 3333], S=511)),
 }
 
 
