@@ -182,3 +182,23 @@ def test_path_choice_by_size_cache_and_kind():
     # the scheduled path keeps the one-launch path's workspace layout
     assert (_plan(_shape(B=16), _kv(), 256, strat, "rows")["workspace"] ==
             _plan(_shape(B=16), _kv(), 256, strat, "one")["workspace"])
+
+
+def test_flash_path_choice():
+    """S2ANTA-flash takes the scheduled kernel (k_row_flash) under the automatic
+    and scheduled options for G <= 4 and at most 64 splits per row, with the
+    small split budget (32 splits at batch 1, 32k keys); G = 8, more splits or
+    the one-launch / two-launch options keep the flash mode of k_fused_dense.
+    Its plan never needs more workspace than santa_workspace_size reports for
+    the flash kind (the dense layout)."""
+    flash = S.SANTA_KIND_FLASH
+    p = _plan(_shape(B=1), _kv(), 0, flash)
+    assert (p["path"], p["kernels"], p["splits"]) == (S.SANTA_PATH_SCHEDULED, "k_row_flash", 32)
+    assert _plan(_shape(B=16), _kv(), 0, flash, "rows")["kernels"] == "k_row_flash"
+    for opt in ("one", "two"):
+        assert _plan(_shape(B=1), _kv(), 0, flash, opt)["kernels"] == "k_fused_dense (flash mode)"
+    assert _plan(_shape(B=1, Hq=16, Hkv=2), _kv(), 0, flash)["kernels"] == "k_fused_dense (flash mode)"
+    assert _plan(_shape(B=16), _kv(n=131072), 0, flash)["kernels"] == "k_fused_dense (flash mode)"
+    for B in (1, 4, 16):
+        need = ws_size(_shape(B=B), _kv(), 0, flash)
+        assert _plan(_shape(B=B), _kv(), 0, flash)["workspace"] <= need
